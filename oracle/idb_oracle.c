@@ -1,0 +1,298 @@
+/*
+ * CPU oracle for the ID Balancing router step and bias controller.
+ *
+ * TEST INFRASTRUCTURE ONLY.  This file is the plain, slow, obviously correct
+ * reference that the GPU library is checked against.  Only the test suite,
+ * the smoke check and the benchmark's CPU-baseline leg may load it.  It shares
+ * no source, header, helper or table with the GPU library.
+ *
+ * What it computes, and the passage of "ID Balancing: Stable Training of
+ * Extremely Sparse MoE via PID-Based Load Control" each step follows:
+ *
+ *   R1  logits z = W_r x                                   (Sec. 2.2)
+ *   R2  scores s_i = sigma(z_i), logistic sigmoid          (Sec. 2.2; Sec. 4.3 scores
+ *                                                            loss-free routers with the
+ *                                                            sigmoid plus the bias)
+ *   R3  biased score v_i = s_i + b_i, one fp32 addition    (Eq. pid-routing)
+ *   R4  T(x) = the K largest v_i                           (Eq. pid-routing)
+ *   R5  gate weights: selected s_i normalised, no bias     (Sec. 2.2, text after
+ *                                                            Eq. pid-routing)
+ *   R6  n_i = number of tokens assigned to expert i        (Eq. pid-error; Alg. 1)
+ *   C1..C7 the ID bias update                              (Alg. 1; Eq. rapid-integral,
+ *                                                            rapid-delta, rapid-gate,
+ *                                                            rapid-update)
+ *   SIGN mode: DeepSeek's fixed-step integral rule         (Eq. pid-deepseek)
+ *   S1  MaxVio / MinVio                                    (Sec. 4.1, Eq. vio)
+ *
+ * Readings of points the paper leaves open (each is listed in the design
+ * notes of the repository):
+ *   - Top-K ties go to the lowest expert index; the selected experts are
+ *     reported in rank order (v descending, index ascending).
+ *   - IEEE comparison of v, so -0 == +0.
+ *   - gate weight w_r = s_r / den with den the fp32 sum of the selected
+ *     unbiased scores taken in rank order; den == 0 gives w = 1/K.
+ *   - e_i = (nbar - n_i)/nbar evaluated as one correctly rounded fp64 division
+ *     of the exact integer numerator S - E*n_i by S, then rounded to fp32.
+ *   - the gate is the sign test (e_prev > 0 and de > 0) or (e_prev < 0 and
+ *     de < 0), i.e. the truth value of e_prev * de > 0 without an fp32 product.
+ *   - b + K_i e + K_d g de is evaluated left to right in fp32, each product and
+ *     sum rounded, the derivative added only when the gate is open, no FMA.
+ *   - the centering mean uses a fixed pairwise tree: pad b~ with +0 to the next
+ *     power of two P >= E, then a_j <- a_j + a_{j+h} for h = P/2, ..., 1.
+ *   - an empty batch (sum of counts == 0) leaves the state untouched and
+ *     reports status 3; a negative count reports status 1.
+ *
+ * Build: gcc -O2 -ffp-contract=off -fopenmp -shared -fPIC (never -ffast-math:
+ * the fp32 steps must round exactly as written).
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#include <time.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+#define ORACLE_DTYPE_BF16 0
+#define ORACLE_DTYPE_F32 1
+
+#define ORACLE_MODE_ERROR 0 /* ID: integral step K_i * e      */
+#define ORACLE_MODE_SIGN 1  /* DeepSeek: integral step K_i * sign(e) */
+
+#define ORACLE_STATUS_OK 0
+#define ORACLE_STATUS_INVALID 1
+#define ORACLE_STATUS_EMPTY 3
+
+int oracle_num_threads(void) {
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}
+
+/* Exact widening of one input element to double.  bf16 is the upper half of
+ * an IEEE binary32, so shifting its 16 bits up gives the same value. */
+static double load_elem(const void* base, int dtype, int64_t i) {
+    if (dtype == ORACLE_DTYPE_BF16) {
+        uint32_t bits = ((uint32_t)((const uint16_t*)base)[i]) << 16;
+        float f;
+        memcpy(&f, &bits, sizeof f);
+        return (double)f;
+    }
+    return (double)((const float*)base)[i];
+}
+
+/* R1 for one token: z_i = sum_k x_k W_ik, products and sum in double,
+ * k ascending.  x is [T][d] row-major, W is [E][d] row-major. */
+static double logit(const void* x, const void* W, int dtype, int64_t t, int32_t d, int32_t i) {
+    double acc = 0.0;
+    for (int32_t k = 0; k < d; ++k) {
+        double xv = load_elem(x, dtype, t * (int64_t)d + k);
+        double wv = load_elem(W, dtype, (int64_t)i * d + k);
+        acc = acc + xv * wv;
+    }
+    return acc;
+}
+
+/* R2: logistic sigmoid in double, rounded once to fp32. */
+static float sigmoid_ref(double z) {
+    return (float)(1.0 / (1.0 + exp(-z)));
+}
+
+/* R1 (+ R2) for the listed rows (all rows when rows == NULL).
+ * z_out (nullable) gets [nrows][E] doubles; s_out (nullable) gets fp32 scores. */
+void oracle_router_scores(const void* x, const void* W, int dtype, int64_t T, int32_t d, int32_t E,
+                          const int64_t* rows, int64_t nrows, double* z_out, float* s_out) {
+    if (rows == NULL) nrows = T;
+#pragma omp parallel for schedule(dynamic, 4)
+    for (int64_t r = 0; r < nrows; ++r) {
+        int64_t t = rows ? rows[r] : r;
+        for (int32_t i = 0; i < E; ++i) {
+            double z = logit(x, W, dtype, t, d, i);
+            if (z_out) z_out[r * E + i] = z;
+            if (s_out) s_out[r * E + i] = sigmoid_ref(z);
+        }
+    }
+}
+
+/* Strict total order of Eq. pid-routing with the lowest-index tie-break:
+ * does (va, ia) rank above (vb, ib)?  IEEE comparison, so -0 == +0. */
+static int ranks_above(float va, int32_t ia, float vb, int32_t ib) {
+    if (va > vb) return 1;
+    if (va < vb) return 0;
+    return ia < ib;
+}
+
+/* R3-R5 for one token: K passes of "best expert not yet taken". */
+static void select_token(const float* s, const float* bias, int32_t E, int32_t K, unsigned char* taken,
+                         int32_t* idx, float* w) {
+    memset(taken, 0, (size_t)E);
+    for (int32_t r = 0; r < K; ++r) {
+        int32_t best = -1;
+        float best_v = 0.0f;
+        for (int32_t i = 0; i < E; ++i) {
+            if (taken[i]) continue;
+            float v = s[i] + bias[i]; /* R3: exactly one fp32 addition */
+            if (best < 0 || ranks_above(v, i, best_v, best)) {
+                best = i;
+                best_v = v;
+            }
+        }
+        taken[best] = 1;
+        idx[r] = best;
+    }
+    /* R5: weights from the unbiased scores, normalised over the selected set. */
+    float den = 0.0f;
+    for (int32_t r = 0; r < K; ++r) den = den + s[idx[r]];
+    for (int32_t r = 0; r < K; ++r) w[r] = (den == 0.0f) ? 1.0f / (float)K : s[idx[r]] / den;
+}
+
+/* R3-R6 given fp32 scores s [T][E] and bias [E].  idx, w are [T][K] in rank
+ * order; counts [E] is zeroed first unless accumulate != 0. */
+void oracle_select(const float* s, const float* bias, int64_t T, int32_t E, int32_t K, int32_t* idx, float* w,
+                   int32_t* counts, int accumulate) {
+#pragma omp parallel
+    {
+        unsigned char* taken = (unsigned char*)malloc((size_t)E);
+#pragma omp for schedule(static)
+        for (int64_t t = 0; t < T; ++t)
+            select_token(s + t * (int64_t)E, bias, E, K, taken, idx + t * (int64_t)K, w + t * (int64_t)K);
+        free(taken);
+    }
+    if (!accumulate)
+        for (int32_t i = 0; i < E; ++i) counts[i] = 0;
+    for (int64_t t = 0; t < T; ++t)
+        for (int32_t r = 0; r < K; ++r) counts[idx[t * (int64_t)K + r]] += 1; /* R6 */
+}
+
+/* R1-R6 in one call: the whole router step for T tokens (used for timing the
+ * CPU baseline and for free-running closed loops).  s_out is nullable. */
+void oracle_router(const void* x, const void* W, int dtype, const float* bias, int64_t T, int32_t d, int32_t E,
+                   int32_t K, int32_t* idx, float* w, int32_t* counts, int accumulate, float* s_out) {
+#pragma omp parallel
+    {
+        float* s = (float*)malloc(sizeof(float) * (size_t)E);
+        unsigned char* taken = (unsigned char*)malloc((size_t)E);
+#pragma omp for schedule(dynamic, 4)
+        for (int64_t t = 0; t < T; ++t) {
+            for (int32_t i = 0; i < E; ++i) s[i] = sigmoid_ref(logit(x, W, dtype, t, d, i));
+            if (s_out) memcpy(s_out + t * (int64_t)E, s, sizeof(float) * (size_t)E);
+            select_token(s, bias, E, K, taken, idx + t * (int64_t)K, w + t * (int64_t)K);
+        }
+        free(taken);
+        free(s);
+    }
+    if (!accumulate)
+        for (int32_t i = 0; i < E; ++i) counts[i] = 0;
+    for (int64_t t = 0; t < T; ++t)
+        for (int32_t r = 0; r < K; ++r) counts[idx[t * (int64_t)K + r]] += 1;
+}
+
+/* Sign with sign(0) = 0 (Eq. pid-deepseek applies it elementwise). */
+static float sign_of(float e) {
+    if (e > 0.0f) return 1.0f;
+    if (e < 0.0f) return -1.0f;
+    return 0.0f;
+}
+
+/* Fixed pairwise tree sum used by the centering step. */
+static float tree_sum(const float* v, int32_t E) {
+    int32_t P = 1;
+    while (P < E) P *= 2;
+    float* a = (float*)malloc(sizeof(float) * (size_t)P);
+    for (int32_t j = 0; j < P; ++j) a[j] = (j < E) ? v[j] : 0.0f;
+    for (int32_t h = P / 2; h >= 1; h /= 2)
+        for (int32_t j = 0; j < h; ++j) a[j] = a[j] + a[j + h];
+    float sum = a[0];
+    free(a);
+    return sum;
+}
+
+/* One controller call (Alg. 1, one iteration, one layer).
+ * State (bias, e_prev, step) is updated in place; returns and stores status. */
+int oracle_controller(const int32_t* counts, int32_t E, float Ki, float Kd, int mode, int center, float* bias,
+                      float* e_prev, int64_t* step, int32_t* status) {
+    /* C1: total assignments S = E * nbar (Eq. pid-error needs S > 0). */
+    int64_t S = 0;
+    for (int32_t i = 0; i < E; ++i) {
+        if (counts[i] < 0) {
+            *status = ORACLE_STATUS_INVALID;
+            return *status;
+        }
+        S += counts[i];
+    }
+    if (S == 0) {
+        *status = ORACLE_STATUS_EMPTY;
+        return *status;
+    }
+    float* bt = (float*)malloc(sizeof(float) * (size_t)E);
+    float* e = (float*)malloc(sizeof(float) * (size_t)E);
+    for (int32_t i = 0; i < E; ++i) {
+        /* C2: e_i = (nbar - n_i) / nbar = (S - E n_i) / S (Eq. pid-error). */
+        int64_t num = S - (int64_t)E * (int64_t)counts[i];
+        e[i] = (float)((double)num / (double)S);
+        /* C3: change of error (Eq. rapid-delta); e_prev starts at 0. */
+        float de = e[i] - e_prev[i];
+        /* C4: worsening gate (Eq. rapid-gate). */
+        int g = (e_prev[i] > 0.0f && de > 0.0f) || (e_prev[i] < 0.0f && de < 0.0f);
+        /* C5: integral step (Eq. rapid-integral, or Eq. pid-deepseek in SIGN
+         * mode) then the gated derivative step (Eq. rapid-update). */
+        float u = (mode == ORACLE_MODE_SIGN) ? Ki * sign_of(e[i]) : Ki * e[i];
+        float b = bias[i] + u;
+        if (g) {
+            float dterm = Kd * de;
+            b = b + dterm;
+        }
+        bt[i] = b;
+    }
+    /* C6: subtract the mean of b~ (second line of Eq. rapid-update). */
+    if (center) {
+        float m = tree_sum(bt, E) / (float)E;
+        for (int32_t i = 0; i < E; ++i) bias[i] = bt[i] - m;
+    } else {
+        for (int32_t i = 0; i < E; ++i) bias[i] = bt[i];
+    }
+    /* C7 */
+    for (int32_t i = 0; i < E; ++i) e_prev[i] = e[i];
+    *step += 1;
+    *status = ORACLE_STATUS_OK;
+    free(e);
+    free(bt);
+    return *status;
+}
+
+/* S1: MaxVio = (max n - nbar)/nbar, MinVio = (nbar - min n)/nbar (Eq. vio),
+ * each as one fp64 division of an exact integer numerator.  out[0] = MaxVio,
+ * out[1] = MinVio; both NaN for an empty batch. */
+void oracle_load_stats(const int32_t* counts, int32_t E, double* out) {
+    int64_t S = 0;
+    int32_t mx = counts[0], mn = counts[0];
+    for (int32_t i = 0; i < E; ++i) {
+        S += counts[i];
+        if (counts[i] > mx) mx = counts[i];
+        if (counts[i] < mn) mn = counts[i];
+    }
+    if (S == 0) {
+        out[0] = NAN;
+        out[1] = NAN;
+        return;
+    }
+    out[0] = (double)((int64_t)E * mx - S) / (double)S;
+    out[1] = (double)(S - (int64_t)E * mn) / (double)S;
+}
+
+/* Wall-clock seconds of one whole oracle step (R1-R6, C1-C7, S1) on the host,
+ * for the CPU baseline.  Uses the OpenMP thread count in effect. */
+double oracle_step_seconds(const void* x, const void* W, int dtype, int64_t T, int32_t d, int32_t E, int32_t K,
+                           float Ki, float Kd, float* bias, float* e_prev, int64_t* step, int32_t* status,
+                           int32_t* idx, float* w, int32_t* counts, double* stats) {
+    struct timespec t0, t1;
+    clock_gettime(CLOCK_MONOTONIC, &t0);
+    oracle_router(x, W, dtype, bias, T, d, E, K, idx, w, counts, 0, NULL);
+    oracle_controller(counts, E, Ki, Kd, ORACLE_MODE_ERROR, 1, bias, e_prev, step, status);
+    oracle_load_stats(counts, E, stats);
+    clock_gettime(CLOCK_MONOTONIC, &t1);
+    return (double)(t1.tv_sec - t0.tv_sec) + 1e-9 * (double)(t1.tv_nsec - t0.tv_nsec);
+}
