@@ -1,0 +1,191 @@
+/*
+ * idb.h -- C ABI of the ID Balancing router step for AMD MI355X (gfx950).
+ *
+ * The calls follow the paper's statement of the problem ("ID Balancing: Stable
+ * Training of Extremely Sparse MoE via PID-Based Load Control"):
+ *
+ *   router    z = W_r x, s = sigmoid(z), T(x) = TopK(s + b), gate weights from
+ *             the unbiased s, per-expert load counts n           (Sec. 2.2,
+ *             Eq. pid-routing, Eq. pid-error)
+ *   controller  e = (nbar - n)/nbar, de = e - e_prev, g = 1[e_prev de > 0],
+ *             b += K_i e + K_d g de, b -= mean(b)                 (Alg. 1,
+ *             Eq. rapid-integral, rapid-delta, rapid-gate, rapid-update)
+ *   statistics  MaxVio, MinVio                                    (Sec. 4.1, Eq. vio)
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * - Memory: every pointer argument that is not a host struct is a DEVICE
+ *   pointer on the device that owns `stream`.  The caller allocates and owns
+ *   all buffers; the library allocates nothing and keeps no state between
+ *   calls.  Calls are reentrant and thread-safe.
+ * - Asynchrony: every call only enqueues work on `stream` (0 = the null
+ *   stream) and returns without synchronising.  Outputs are valid once the
+ *   stream reaches that point.
+ * - Errors: arguments are checked before anything is enqueued.  On an invalid
+ *   argument the call returns IDB_ERR_INVALID_ARG (or IDB_ERR_UNSUPPORTED for
+ *   a valid but unsupported shape), enqueues nothing and leaves every output
+ *   untouched; these checks make no HIP call.  A failed launch returns
+ *   IDB_ERR_HIP.  idb_last_error() gives a message for the last failing call on
+ *   the calling thread.  Errors that depend on data (an empty batch) cannot be
+ *   returned synchronously; the controller writes them to its device status.
+ * - Layouts are row-major and densely packed.  x, W_g and workspace must be
+ *   16-byte aligned; every other buffer 4-byte aligned (8 for int64/double).
+ * - NaN or infinite inputs are a caller error and are not checked.
+ * - Determinism: for the same inputs and variant, every output is bit-identical
+ *   run to run; integer counts are exact.
+ */
+#ifndef IDB_H
+#define IDB_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum idb_status {
+    IDB_OK = 0,
+    IDB_ERR_INVALID_ARG = 1, /* bad pointer, size, alignment or workspace       */
+    IDB_ERR_UNSUPPORTED = 2, /* valid request outside what the kernels handle   */
+    IDB_ERR_EMPTY_BATCH = 3, /* device status only: all counts zero, no update  */
+    IDB_ERR_HIP = 4          /* a HIP launch failed                             */
+} idb_status;
+
+typedef enum idb_dtype {
+    IDB_DTYPE_BF16 = 0, /* x and W_g hold bfloat16 values                     */
+    IDB_DTYPE_F32 = 1   /* x and W_g hold fp32 values                         */
+} idb_dtype;
+
+typedef enum idb_integral_mode {
+    IDB_INTEGRAL_ERROR = 0, /* ID Balancing: integral step K_i * e (Eq. rapid-integral)   */
+    IDB_INTEGRAL_SIGN = 1   /* DeepSeek loss-free: K_i * sign(e), sign(0) = 0 (Eq. pid-deepseek) */
+} idb_integral_mode;
+
+/* Controller configuration (host struct). */
+typedef struct idb_controller_cfg {
+    int32_t E;             /* number of routed experts, 1 <= E <= 1024             */
+    float Ki;              /* integral gain K_i >= 0, shared by all experts          */
+    float Kd;              /* derivative gain K_d >= 0                               */
+    int32_t integral_mode; /* idb_integral_mode                                       */
+    int32_t center;        /* 1: subtract the mean after the update (Eq. rapid-update) */
+} idb_controller_cfg;
+
+/* Controller state (host struct of device pointers, caller-owned).  The full
+ * state of Alg. 1 is (bias, e_prev); step counts successful updates.  Start
+ * from bias = e_prev = 0, step = 0.  Saving and restoring these buffers
+ * checkpoints the controller exactly. */
+typedef struct idb_controller_state {
+    float* bias;     /* [E] expert bias b; also the routing input of the next step */
+    float* e_prev;   /* [E] normalised load error of the previous update            */
+    int64_t* step;   /* [1] number of successful updates                           */
+    int32_t* status; /* [1] idb_status of the last update (OK, EMPTY_BATCH, INVALID_ARG) */
+} idb_controller_state;
+
+/* ---------------------------------------------------------------------------
+ * Router step (Sec. 2.2; Eq. pid-routing; Eq. pid-error counts).
+ *
+ *   x           [T][d] hidden states, dtype as given, 16-byte aligned.
+ *   W_g         [E][d] router matrix W_r, same dtype.
+ *   bias        [E] fp32 expert bias b, read only (frozen within the step).
+ *   T, d, E, K  tokens, hidden size, experts, experts per token.
+ *               1 <= T <= 2^26; 1 <= K <= E; E <= 1024, E % 32 == 0 and
+ *               K <= 32 (else IDB_ERR_UNSUPPORTED); d % 64 == 0 (bf16) or
+ *               d % 32 == 0 (fp32), d <= 65536.
+ *   expert_idx  [T][K] int32 out: the K experts with the largest s + b
+ *               (fp32 add), in rank order: larger s + b first, lower expert
+ *               index first among equal values (-0 == +0).
+ *   gate_w      [T][K] fp32 out: gate_w[t][r] = s[t][idx_r] / den, den the
+ *               fp32 sum of the selected unbiased scores in rank order
+ *               (den == 0 gives 1/K).
+ *   counts      [E] int32: counts[i] += number of tokens routed to expert i.
+ *               Zeroed first unless accumulate_counts != 0 (microbatch
+ *               summing, Alg. 1).
+ *   scores_dump nullable [T][E] fp32 out, 16-byte aligned: the scores s the
+ *               selection used (debug / parity; the arithmetic is unchanged).
+ *   workspace   device scratch of at least idb_router_workspace_bytes().
+ *   variant     0 = automatic tiling; other values force a tiling (see
+ *               idb_router_variant_info).  Every variant gives identical
+ *               outputs.
+ * The T x E score matrix is never written to memory unless scores_dump is set.
+ * ------------------------------------------------------------------------- */
+size_t idb_router_workspace_bytes(int64_t T, int32_t d, int32_t E, int32_t K, idb_dtype dtype, int32_t variant);
+
+idb_status idb_router_forward(const void* x, const void* W_g, idb_dtype dtype, const float* bias, int64_t T,
+                              int32_t d, int32_t E, int32_t K, int32_t* expert_idx, float* gate_w,
+                              int32_t* counts, int32_t accumulate_counts, float* scores_dump, void* workspace,
+                              size_t workspace_bytes, int32_t variant, hipStream_t stream);
+
+/* The two launches idb_router_forward makes, exposed so a caller can time or
+ * overlap them separately.  Same arguments; calling score_select then merge
+ * on one stream is exactly idb_router_forward.
+ *   score_select: gate contraction, sigmoid, biased Top-K per expert slice
+ *                 (and, when the tiling covers all experts in one slice, the
+ *                 final outputs); zeroes counts unless accumulating.
+ *   merge:        merges the slices' candidates into the final Top-K, gate
+ *                 weights and counts; enqueues nothing for single-slice
+ *                 tilings. */
+idb_status idb_router_score_select(const void* x, const void* W_g, idb_dtype dtype, const float* bias, int64_t T,
+                                   int32_t d, int32_t E, int32_t K, int32_t* expert_idx, float* gate_w,
+                                   int32_t* counts, int32_t accumulate_counts, float* scores_dump,
+                                   void* workspace, size_t workspace_bytes, int32_t variant, hipStream_t stream);
+idb_status idb_router_merge(int64_t T, int32_t d, int32_t E, int32_t K, idb_dtype dtype, int32_t* expert_idx,
+                            float* gate_w, int32_t* counts, void* workspace, size_t workspace_bytes,
+                            int32_t variant, hipStream_t stream);
+
+/* Tiling of a variant for a shape: out[0] = tokens per workgroup, out[1] =
+ * expert slices, out[2] = waves per workgroup, out[3] = 32-expert blocks per
+ * wave, out[4] = resolved variant id.  Returns IDB_ERR_UNSUPPORTED when the
+ * variant cannot run the shape.  Host only, no HIP call. */
+idb_status idb_router_variant_info(int64_t T, int32_t d, int32_t E, int32_t K, idb_dtype dtype, int32_t variant,
+                                   int32_t out[5]);
+
+/* ---------------------------------------------------------------------------
+ * Selection from given scores (Eq. pid-routing and the gate-weight rule of
+ * Sec. 2.2, then the counts of Eq. pid-error): the router step without the
+ * gate contraction.  scores [T][E] fp32, bias [E] fp32; outputs as for
+ * idb_router_forward.  1 <= T <= 2^26, 1 <= K <= E; E <= 1024 and K <= 32
+ * (else IDB_ERR_UNSUPPORTED).  Any E in that range.
+ * ------------------------------------------------------------------------- */
+idb_status idb_select_from_scores(const float* scores, const float* bias, int64_t T, int32_t E, int32_t K,
+                                  int32_t* expert_idx, float* gate_w, int32_t* counts, int32_t accumulate_counts,
+                                  hipStream_t stream);
+
+/* ---------------------------------------------------------------------------
+ * One ID controller update (Alg. 1, one iteration of one MoE layer; in SIGN
+ * mode Eq. pid-deepseek).  counts [E] int32 are the loads summed over
+ * microbatches (and data-parallel ranks).  With S = sum(counts):
+ *   e_i  = (S - E n_i) / S, one correctly rounded fp64 division, then fp32
+ *   de_i = e_i - e_prev_i
+ *   g_i  = (e_prev_i > 0 and de_i > 0) or (e_prev_i < 0 and de_i < 0)
+ *   b~_i = (b_i + K_i e_i) [+ K_d de_i if g_i], fp32, left to right, no FMA
+ *   if center: b_i = b~_i - m, m = (fixed pairwise tree sum of b~ padded with
+ *              +0 to a power of two) / E; else b_i = b~_i
+ *   e_prev = e; step += 1; status = IDB_OK
+ * S == 0: status = IDB_ERR_EMPTY_BATCH; a negative count: status =
+ * IDB_ERR_INVALID_ARG; in both cases bias, e_prev and step are unchanged.
+ * One single-workgroup launch.
+ * ------------------------------------------------------------------------- */
+idb_status idb_controller_update(const int32_t* counts, const idb_controller_cfg* cfg,
+                                 const idb_controller_state* state, hipStream_t stream);
+
+/* ---------------------------------------------------------------------------
+ * Load statistics (Sec. 4.1, Eq. vio) from counts [E] int32, 1 <= E <= 1<<20:
+ *   out[0] = MaxVio = (E max n - S) / S,  out[1] = MinVio = (S - E min n) / S,
+ * each one fp64 division of an exact integer numerator; NaN for S == 0.
+ * out is a device double[2].
+ * ------------------------------------------------------------------------- */
+idb_status idb_load_stats(const int32_t* counts, int32_t E, double* out_maxvio_minvio, hipStream_t stream);
+
+/* Static description of a status code; message of the last failing call on
+ * this thread (empty string if none). */
+const char* idb_status_string(idb_status s);
+const char* idb_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* IDB_H */

@@ -1,0 +1,224 @@
+"""Python binding of the C ABI in ``include/idb.h`` (libidb.so).
+
+Argument marshalling only: torch tensors supply device pointers and the
+current HIP stream; every step of the router and controller runs in the HIP
+kernels behind the ABI.  There is no fallback: if ``libidb.so`` is missing or
+the arguments are rejected, the call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libidb.so")
+
+IDB_OK = 0
+IDB_ERR_INVALID_ARG = 1
+IDB_ERR_UNSUPPORTED = 2
+IDB_ERR_EMPTY_BATCH = 3
+IDB_ERR_HIP = 4
+
+IDB_DTYPE_BF16 = 0
+IDB_DTYPE_F32 = 1
+IDB_INTEGRAL_ERROR = 0
+IDB_INTEGRAL_SIGN = 1
+
+EXPORTED = (
+    "idb_router_workspace_bytes", "idb_router_forward", "idb_router_score_select", "idb_router_merge",
+    "idb_router_variant_info", "idb_select_from_scores", "idb_controller_update", "idb_load_stats",
+    "idb_status_string", "idb_last_error",
+)
+
+
+class IdbError(RuntimeError):
+    def __init__(self, fn: str, status: int, msg: str):
+        super().__init__(f"{fn}: status {status}: {msg}")
+        self.status = status
+
+
+class idb_controller_cfg(ctypes.Structure):
+    _fields_ = [("E", ctypes.c_int32), ("Ki", ctypes.c_float), ("Kd", ctypes.c_float),
+                ("integral_mode", ctypes.c_int32), ("center", ctypes.c_int32)]
+
+
+class idb_controller_state(ctypes.Structure):
+    _fields_ = [("bias", ctypes.c_void_p), ("e_prev", ctypes.c_void_p), ("step", ctypes.c_void_p),
+                ("status", ctypes.c_void_p)]
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """Load libidb.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2609_39137_amd.build`")
+    L = ctypes.CDLL(LIB_PATH)
+    P, i64, i32, sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_size_t
+    router_args = [P, P, i32, P, i64, i32, i32, i32, P, P, P, i32, P, P, sz, i32, P]
+    L.idb_router_workspace_bytes.argtypes = [i64, i32, i32, i32, i32, i32]
+    L.idb_router_workspace_bytes.restype = sz
+    for name in ("idb_router_forward", "idb_router_score_select"):
+        getattr(L, name).argtypes = router_args
+        getattr(L, name).restype = ctypes.c_int
+    L.idb_router_merge.argtypes = [i64, i32, i32, i32, i32, P, P, P, P, sz, i32, P]
+    L.idb_router_merge.restype = ctypes.c_int
+    L.idb_router_variant_info.argtypes = [i64, i32, i32, i32, i32, i32, P]
+    L.idb_router_variant_info.restype = ctypes.c_int
+    L.idb_select_from_scores.argtypes = [P, P, i64, i32, i32, P, P, P, i32, P]
+    L.idb_select_from_scores.restype = ctypes.c_int
+    L.idb_controller_update.argtypes = [P, ctypes.POINTER(idb_controller_cfg), ctypes.POINTER(idb_controller_state), P]
+    L.idb_controller_update.restype = ctypes.c_int
+    L.idb_load_stats.argtypes = [P, i32, P, P]
+    L.idb_load_stats.restype = ctypes.c_int
+    L.idb_status_string.argtypes = [ctypes.c_int]
+    L.idb_status_string.restype = ctypes.c_char_p
+    L.idb_last_error.argtypes = []
+    L.idb_last_error.restype = ctypes.c_char_p
+    _lib = L
+    return L
+
+
+def idb_status_string(status: int) -> str:
+    return lib().idb_status_string(status).decode()
+
+
+def idb_last_error() -> str:
+    return lib().idb_last_error().decode()
+
+
+def _check(fn: str, status: int) -> None:
+    if status != IDB_OK:
+        raise IdbError(fn, status, f"{idb_status_string(status)}: {idb_last_error()}")
+
+
+def _stream(stream) -> int | None:
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def _ptr(t: torch.Tensor | None) -> int | None:
+    if t is None:
+        return None
+    if not t.is_cuda or not t.is_contiguous():
+        raise ValueError("tensors passed to libidb must be contiguous device tensors")
+    return t.data_ptr()
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.bfloat16:
+        return IDB_DTYPE_BF16
+    if t.dtype == torch.float32:
+        return IDB_DTYPE_F32
+    raise TypeError(f"router inputs must be bfloat16 or float32, got {t.dtype}")
+
+
+# ---------------------------------------------------------------------------- router
+
+
+def idb_router_workspace_bytes(T: int, d: int, E: int, K: int, dtype: int, variant: int = 0) -> int:
+    return int(lib().idb_router_workspace_bytes(T, d, E, K, dtype, variant))
+
+
+def idb_router_variant_info(T: int, d: int, E: int, K: int, dtype: int, variant: int = 0) -> dict:
+    out = (ctypes.c_int32 * 5)()
+    _check("idb_router_variant_info", lib().idb_router_variant_info(T, d, E, K, dtype, variant, out))
+    return {"tokens_per_wg": out[0], "slices": out[1], "waves": out[2], "blocks_per_wave": out[3], "variant": out[4]}
+
+
+def _router_call(fn: str, x, W_g, bias, K, expert_idx, gate_w, counts, accumulate, scores_dump, workspace,
+                 variant, stream):
+    T, d = x.shape
+    E = W_g.shape[0]
+    if W_g.shape[1] != d or W_g.dtype != x.dtype or bias.shape != (E,) or bias.dtype != torch.float32:
+        raise ValueError("router operands disagree in shape or dtype")
+    if expert_idx.shape != (T, K) or gate_w.shape != (T, K) or counts.shape != (E,):
+        raise ValueError("router outputs have the wrong shape")
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    st = getattr(lib(), fn)(_ptr(x), _ptr(W_g), _dtype_code(x), _ptr(bias), T, d, E, K, _ptr(expert_idx),
+                            _ptr(gate_w), _ptr(counts), int(bool(accumulate)), _ptr(scores_dump),
+                            _ptr(workspace), ws_bytes, int(variant), _stream(stream))
+    _check(fn, st)
+
+
+def idb_router_forward(x, W_g, bias, K, expert_idx, gate_w, counts, accumulate=False, scores_dump=None,
+                       workspace=None, variant=0, stream=None):
+    """Router step (gate contraction, sigmoid, biased Top-K, gate weights, counts) on ``stream``."""
+    _router_call("idb_router_forward", x, W_g, bias, K, expert_idx, gate_w, counts, accumulate, scores_dump,
+                 workspace, variant, stream)
+
+
+def idb_router_score_select(x, W_g, bias, K, expert_idx, gate_w, counts, accumulate=False, scores_dump=None,
+                            workspace=None, variant=0, stream=None):
+    _router_call("idb_router_score_select", x, W_g, bias, K, expert_idx, gate_w, counts, accumulate, scores_dump,
+                 workspace, variant, stream)
+
+
+def idb_router_merge(T, d, E, K, dtype, expert_idx, gate_w, counts, workspace=None, variant=0, stream=None):
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    st = lib().idb_router_merge(T, d, E, K, dtype, _ptr(expert_idx), _ptr(gate_w), _ptr(counts), _ptr(workspace),
+                                ws_bytes, int(variant), _stream(stream))
+    _check("idb_router_merge", st)
+
+
+# ---------------------------------------------------------------------------- selection
+
+
+def idb_select_from_scores(scores, bias, K, expert_idx, gate_w, counts, accumulate=False, stream=None):
+    T, E = scores.shape
+    if scores.dtype != torch.float32 or bias.shape != (E,) or expert_idx.shape != (T, K) or counts.shape != (E,):
+        raise ValueError("select operands have the wrong shape or dtype")
+    st = lib().idb_select_from_scores(_ptr(scores), _ptr(bias), T, E, K, _ptr(expert_idx), _ptr(gate_w),
+                                      _ptr(counts), int(bool(accumulate)), _stream(stream))
+    _check("idb_select_from_scores", st)
+
+
+# ---------------------------------------------------------------------------- controller
+
+
+@dataclass
+class ControllerCfg:
+    E: int
+    Ki: float = 6e-3
+    Kd: float = 6e-3
+    integral_mode: int = IDB_INTEGRAL_ERROR
+    center: bool = True
+
+    def c(self) -> idb_controller_cfg:
+        return idb_controller_cfg(self.E, self.Ki, self.Kd, self.integral_mode, int(bool(self.center)))
+
+
+class ControllerState:
+    """Device-resident controller state (bias, e_prev, step, status), zero-initialised."""
+
+    def __init__(self, E: int, device="cuda"):
+        self.bias = torch.zeros(E, dtype=torch.float32, device=device)
+        self.e_prev = torch.zeros(E, dtype=torch.float32, device=device)
+        self.step = torch.zeros(1, dtype=torch.int64, device=device)
+        self.status = torch.zeros(1, dtype=torch.int32, device=device)
+
+    def c(self) -> idb_controller_state:
+        return idb_controller_state(_ptr(self.bias), _ptr(self.e_prev), _ptr(self.step), _ptr(self.status))
+
+
+def idb_controller_update(counts, cfg: ControllerCfg, state: ControllerState, stream=None):
+    """One ID controller update of ``state`` from ``counts`` on ``stream``."""
+    c_cfg, c_state = cfg.c(), state.c()
+    st = lib().idb_controller_update(_ptr(counts), ctypes.byref(c_cfg), ctypes.byref(c_state), _stream(stream))
+    _check("idb_controller_update", st)
+
+
+def idb_load_stats(counts, out, stream=None):
+    """MaxVio, MinVio of ``counts`` into the device double[2] ``out``."""
+    if out.dtype != torch.float64 or out.numel() != 2:
+        raise ValueError("out must be a float64 tensor of 2 elements")
+    st = lib().idb_load_stats(_ptr(counts), counts.numel(), _ptr(out), _stream(stream))
+    _check("idb_load_stats", st)

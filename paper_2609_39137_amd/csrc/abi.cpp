@@ -1,0 +1,274 @@
+// C ABI of the ID Balancing router step (declared in include/idb.h): argument
+// checks, tiling choice and kernel launches.  Every check runs before any HIP
+// call, so an invalid call enqueues nothing and touches no output.
+#include "idb.h"
+
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+
+#include "internal.h"
+
+namespace {
+
+thread_local char g_last_error[256] = "";
+
+idb_status fail(idb_status s, const char* fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_last_error, sizeof g_last_error, fmt, ap);
+    va_end(ap);
+    return s;
+}
+
+idb_status hip_result(hipError_t e, const char* what) {
+    if (e == hipSuccess) return IDB_OK;
+    return fail(IDB_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
+
+constexpr int64_t kMaxTokens = int64_t(1) << 26;
+constexpr int kMaxExperts = 1024;
+constexpr int kMaxSlices = 8;
+constexpr int kMaxKGpu = 32;
+
+size_t round_up(size_t n) { return (n + 255) & ~size_t(255); }
+
+// Resolve a router variant for a shape; returns IDB_OK and the tiling, or an error.
+idb_status resolve_tiling(int32_t E, idb_dtype dtype, int32_t variant, idb::RouterTiling* out) {
+    const int n = idb::router_tiling_count();
+    const int want_f32 = dtype == IDB_DTYPE_F32;
+    if (variant != 0) {
+        if (variant < 1 || variant > n) return fail(IDB_ERR_INVALID_ARG, "router variant %d out of range", variant);
+        idb::RouterTiling t = idb::router_tiling(variant - 1);
+        if (t.is_f32 != want_f32) return fail(IDB_ERR_UNSUPPORTED, "router variant %d is for another dtype", variant);
+        if (idb::router_slices(t, E) > kMaxSlices)
+            return fail(IDB_ERR_UNSUPPORTED, "router variant %d needs more than %d expert slices", variant,
+                        kMaxSlices);
+        *out = t;
+        return IDB_OK;
+    }
+    // Automatic: among the multi-wave tilings of this dtype (ids 1, 3, 4, 5),
+    // the fewest padded experts, then the widest slice.
+    bool found = false;
+    idb::RouterTiling best{};
+    long best_waste = 0;
+    for (int i = 0; i < n; ++i) {
+        idb::RouterTiling t = idb::router_tiling(i);
+        if (t.is_f32 != want_f32 || t.id == 2) continue;
+        const int ns = idb::router_slices(t, E);
+        if (ns > kMaxSlices) continue;
+        const long be = (long)t.waves * t.nblk * 32;
+        const long waste = ns * be - E;
+        if (!found || waste < best_waste || (waste == best_waste && be > (long)best.waves * best.nblk * 32)) {
+            best = t;
+            best_waste = waste;
+            found = true;
+        }
+    }
+    if (!found) return fail(IDB_ERR_UNSUPPORTED, "no router tiling for E=%d", E);
+    *out = best;
+    return IDB_OK;
+}
+
+idb_status check_router_shape(int64_t T, int32_t d, int32_t E, int32_t K, idb_dtype dtype) {
+    if (dtype != IDB_DTYPE_BF16 && dtype != IDB_DTYPE_F32) return fail(IDB_ERR_INVALID_ARG, "unknown dtype %d", dtype);
+    if (T < 1 || T > kMaxTokens) return fail(IDB_ERR_INVALID_ARG, "T=%lld out of [1, 2^26]", (long long)T);
+    if (d < 1 || d > 65536) return fail(IDB_ERR_INVALID_ARG, "d=%d out of [1, 65536]", d);
+    if (E < 1 || K < 1 || K > E) return fail(IDB_ERR_INVALID_ARG, "need 1 <= K <= E (K=%d, E=%d)", K, E);
+    if (E > kMaxExperts) return fail(IDB_ERR_UNSUPPORTED, "E=%d above %d", E, kMaxExperts);
+    if (E % 32 != 0) return fail(IDB_ERR_UNSUPPORTED, "E=%d is not a multiple of 32", E);
+    if (K > kMaxKGpu) return fail(IDB_ERR_UNSUPPORTED, "K=%d above %d", K, kMaxKGpu);
+    const int dmul = dtype == IDB_DTYPE_BF16 ? 64 : 32;
+    if (d % dmul != 0) return fail(IDB_ERR_UNSUPPORTED, "d=%d is not a multiple of %d", d, dmul);
+    return IDB_OK;
+}
+
+size_t router_ws_bytes(int64_t T, int32_t E, int32_t K, const idb::RouterTiling& t) {
+    const int ns = idb::router_slices(t, E);
+    if (ns <= 1) return 0;
+    return 3 * round_up((size_t)T * ns * K * 4);
+}
+
+struct RouterCall {
+    idb::RouterTiling tiling;
+    idb::RouterArgs args;
+};
+
+idb_status prepare_router(const void* x, const void* W_g, idb_dtype dtype, const float* bias, int64_t T, int32_t d,
+                          int32_t E, int32_t K, int32_t* expert_idx, float* gate_w, int32_t* counts,
+                          int32_t accumulate_counts, float* scores_dump, void* workspace, size_t workspace_bytes,
+                          int32_t variant, bool need_inputs, RouterCall* call) {
+    idb_status st = check_router_shape(T, d, E, K, dtype);
+    if (st != IDB_OK) return st;
+    if (need_inputs) {
+        if (!x || !W_g || !bias) return fail(IDB_ERR_INVALID_ARG, "null input pointer");
+        if (!aligned(x, 16) || !aligned(W_g, 16)) return fail(IDB_ERR_INVALID_ARG, "x and W_g must be 16-byte aligned");
+        if (!aligned(bias, 4)) return fail(IDB_ERR_INVALID_ARG, "bias must be 4-byte aligned");
+        if (scores_dump && !aligned(scores_dump, 16))
+            return fail(IDB_ERR_INVALID_ARG, "scores_dump must be 16-byte aligned");
+    }
+    if (!expert_idx || !gate_w || !counts) return fail(IDB_ERR_INVALID_ARG, "null output pointer");
+    if (!aligned(expert_idx, 4) || !aligned(gate_w, 4) || !aligned(counts, 4))
+        return fail(IDB_ERR_INVALID_ARG, "outputs must be 4-byte aligned");
+    st = resolve_tiling(E, dtype, variant, &call->tiling);
+    if (st != IDB_OK) return st;
+    const size_t need = router_ws_bytes(T, E, K, call->tiling);
+    if (need > 0) {
+        if (!workspace || workspace_bytes < need)
+            return fail(IDB_ERR_INVALID_ARG, "workspace of %zu bytes needed, %zu given", need, workspace_bytes);
+        if (!aligned(workspace, 16)) return fail(IDB_ERR_INVALID_ARG, "workspace must be 16-byte aligned");
+    }
+    idb::RouterArgs& a = call->args;
+    a.x = x;
+    a.W = W_g;
+    a.bias = bias;
+    a.T = T;
+    a.d = d;
+    a.E = E;
+    a.K = K;
+    a.idx = expert_idx;
+    a.w = gate_w;
+    a.counts = counts;
+    a.dump = scores_dump;
+    const int ns = idb::router_slices(call->tiling, E);
+    a.zero_counts = (!accumulate_counts && ns > 1) ? 1 : 0;
+    const size_t part = round_up((size_t)T * ns * K * 4);
+    char* ws = static_cast<char*>(workspace);
+    a.cand_v = need ? reinterpret_cast<float*>(ws) : nullptr;
+    a.cand_s = need ? reinterpret_cast<float*>(ws + part) : nullptr;
+    a.cand_i = need ? reinterpret_cast<int32_t*>(ws + 2 * part) : nullptr;
+    return IDB_OK;
+}
+
+idb_status enqueue_score_select(const RouterCall& c, int32_t accumulate_counts, hipStream_t stream) {
+    const int ns = idb::router_slices(c.tiling, c.args.E);
+    if (ns <= 1 && !accumulate_counts) {
+        idb_status st = hip_result(idb::launch_fill_i32(c.args.counts, 0, c.args.E, stream), "zero counts");
+        if (st != IDB_OK) return st;
+    }
+    return hip_result(idb::launch_router_score_select(c.tiling, c.args, stream), "router score/select launch");
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t idb_router_workspace_bytes(int64_t T, int32_t d, int32_t E, int32_t K, idb_dtype dtype, int32_t variant) {
+    if (check_router_shape(T, d, E, K, dtype) != IDB_OK) return 0;
+    idb::RouterTiling t;
+    if (resolve_tiling(E, dtype, variant, &t) != IDB_OK) return 0;
+    return router_ws_bytes(T, E, K, t);
+}
+
+idb_status idb_router_variant_info(int64_t T, int32_t d, int32_t E, int32_t K, idb_dtype dtype, int32_t variant,
+                                   int32_t out[5]) {
+    if (!out) return fail(IDB_ERR_INVALID_ARG, "null out");
+    idb_status st = check_router_shape(T, d, E, K, dtype);
+    if (st != IDB_OK) return st;
+    idb::RouterTiling t;
+    st = resolve_tiling(E, dtype, variant, &t);
+    if (st != IDB_OK) return st;
+    out[0] = 32 * t.tbw;
+    out[1] = idb::router_slices(t, E);
+    out[2] = t.waves;
+    out[3] = t.nblk;
+    out[4] = t.id;
+    return IDB_OK;
+}
+
+idb_status idb_router_score_select(const void* x, const void* W_g, idb_dtype dtype, const float* bias, int64_t T,
+                                   int32_t d, int32_t E, int32_t K, int32_t* expert_idx, float* gate_w,
+                                   int32_t* counts, int32_t accumulate_counts, float* scores_dump, void* workspace,
+                                   size_t workspace_bytes, int32_t variant, hipStream_t stream) {
+    RouterCall c;
+    idb_status st = prepare_router(x, W_g, dtype, bias, T, d, E, K, expert_idx, gate_w, counts, accumulate_counts,
+                                   scores_dump, workspace, workspace_bytes, variant, true, &c);
+    if (st != IDB_OK) return st;
+    return enqueue_score_select(c, accumulate_counts, stream);
+}
+
+idb_status idb_router_merge(int64_t T, int32_t d, int32_t E, int32_t K, idb_dtype dtype, int32_t* expert_idx,
+                            float* gate_w, int32_t* counts, void* workspace, size_t workspace_bytes, int32_t variant,
+                            hipStream_t stream) {
+    RouterCall c;
+    idb_status st = prepare_router(nullptr, nullptr, dtype, nullptr, T, d, E, K, expert_idx, gate_w, counts, 1,
+                                   nullptr, workspace, workspace_bytes, variant, false, &c);
+    if (st != IDB_OK) return st;
+    return hip_result(idb::launch_router_merge(c.tiling, c.args, stream), "router merge launch");
+}
+
+idb_status idb_router_forward(const void* x, const void* W_g, idb_dtype dtype, const float* bias, int64_t T,
+                              int32_t d, int32_t E, int32_t K, int32_t* expert_idx, float* gate_w, int32_t* counts,
+                              int32_t accumulate_counts, float* scores_dump, void* workspace,
+                              size_t workspace_bytes, int32_t variant, hipStream_t stream) {
+    RouterCall c;
+    idb_status st = prepare_router(x, W_g, dtype, bias, T, d, E, K, expert_idx, gate_w, counts, accumulate_counts,
+                                   scores_dump, workspace, workspace_bytes, variant, true, &c);
+    if (st != IDB_OK) return st;
+    st = enqueue_score_select(c, accumulate_counts, stream);
+    if (st != IDB_OK) return st;
+    return hip_result(idb::launch_router_merge(c.tiling, c.args, stream), "router merge launch");
+}
+
+idb_status idb_select_from_scores(const float* scores, const float* bias, int64_t T, int32_t E, int32_t K,
+                                  int32_t* expert_idx, float* gate_w, int32_t* counts, int32_t accumulate_counts,
+                                  hipStream_t stream) {
+    if (!scores || !bias || !expert_idx || !gate_w || !counts) return fail(IDB_ERR_INVALID_ARG, "null pointer");
+    if (T < 1 || T > kMaxTokens) return fail(IDB_ERR_INVALID_ARG, "T=%lld out of [1, 2^26]", (long long)T);
+    if (E < 1 || K < 1 || K > E) return fail(IDB_ERR_INVALID_ARG, "need 1 <= K <= E (K=%d, E=%d)", K, E);
+    if (E > kMaxExperts) return fail(IDB_ERR_UNSUPPORTED, "E=%d above %d", E, kMaxExperts);
+    if (K > kMaxKGpu) return fail(IDB_ERR_UNSUPPORTED, "K=%d above %d", K, kMaxKGpu);
+    if (!aligned(scores, 4) || !aligned(bias, 4) || !aligned(expert_idx, 4) || !aligned(gate_w, 4) ||
+        !aligned(counts, 4))
+        return fail(IDB_ERR_INVALID_ARG, "buffers must be 4-byte aligned");
+    if (!accumulate_counts) {
+        idb_status st = hip_result(idb::launch_fill_i32(counts, 0, E, stream), "zero counts");
+        if (st != IDB_OK) return st;
+    }
+    return hip_result(idb::launch_select_from_scores(scores, bias, T, E, K, expert_idx, gate_w, counts, stream),
+                      "select launch");
+}
+
+idb_status idb_controller_update(const int32_t* counts, const idb_controller_cfg* cfg,
+                                 const idb_controller_state* state, hipStream_t stream) {
+    if (!counts || !cfg || !state) return fail(IDB_ERR_INVALID_ARG, "null pointer");
+    if (!state->bias || !state->e_prev || !state->step || !state->status)
+        return fail(IDB_ERR_INVALID_ARG, "null state buffer");
+    if (cfg->E < 1 || cfg->E > kMaxExperts) return fail(IDB_ERR_INVALID_ARG, "E=%d out of [1, 1024]", cfg->E);
+    if (!(cfg->Ki >= 0.0f) || !(cfg->Kd >= 0.0f) || !isfinite(cfg->Ki) || !isfinite(cfg->Kd))
+        return fail(IDB_ERR_INVALID_ARG, "gains must be finite and >= 0");
+    if (cfg->integral_mode != IDB_INTEGRAL_ERROR && cfg->integral_mode != IDB_INTEGRAL_SIGN)
+        return fail(IDB_ERR_INVALID_ARG, "unknown integral mode %d", cfg->integral_mode);
+    if (cfg->center != 0 && cfg->center != 1) return fail(IDB_ERR_INVALID_ARG, "center must be 0 or 1");
+    if (!aligned(counts, 4) || !aligned(state->bias, 4) || !aligned(state->e_prev, 4) || !aligned(state->step, 8) ||
+        !aligned(state->status, 4))
+        return fail(IDB_ERR_INVALID_ARG, "misaligned buffer");
+    return hip_result(idb::launch_controller_update(counts, cfg->E, cfg->Ki, cfg->Kd,
+                                                    cfg->integral_mode == IDB_INTEGRAL_SIGN, cfg->center,
+                                                    state->bias, state->e_prev, state->step, state->status, stream),
+                      "controller launch");
+}
+
+idb_status idb_load_stats(const int32_t* counts, int32_t E, double* out_maxvio_minvio, hipStream_t stream) {
+    if (!counts || !out_maxvio_minvio) return fail(IDB_ERR_INVALID_ARG, "null pointer");
+    if (E < 1 || E > (1 << 20)) return fail(IDB_ERR_INVALID_ARG, "E=%d out of [1, 2^20]", E);
+    if (!aligned(counts, 4) || !aligned(out_maxvio_minvio, 8)) return fail(IDB_ERR_INVALID_ARG, "misaligned buffer");
+    return hip_result(idb::launch_load_stats(counts, E, out_maxvio_minvio, stream), "load stats launch");
+}
+
+const char* idb_status_string(idb_status s) {
+    switch (s) {
+        case IDB_OK: return "ok";
+        case IDB_ERR_INVALID_ARG: return "invalid argument";
+        case IDB_ERR_UNSUPPORTED: return "unsupported shape or option";
+        case IDB_ERR_EMPTY_BATCH: return "empty batch: every count is zero";
+        case IDB_ERR_HIP: return "HIP launch failure";
+        default: return "unknown status";
+    }
+}
+
+const char* idb_last_error(void) { return g_last_error; }
+
+}  // extern "C"

@@ -1,0 +1,62 @@
+// Host-side launchers of the gfx950 kernels, called by the C ABI (abi.cpp).
+// Arguments are validated by the caller; these only enqueue work.
+#pragma once
+
+#include <hip/hip_runtime_api.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace idb {
+
+hipError_t launch_controller_update(const int32_t* counts, int E, float Ki, float Kd, int sign_mode, int center,
+                                    float* bias, float* e_prev, int64_t* step, int32_t* status,
+                                    hipStream_t stream);
+hipError_t launch_load_stats(const int32_t* counts, int E, double* out, hipStream_t stream);
+
+hipError_t launch_fill_i32(int32_t* p, int32_t value, int64_t n, hipStream_t stream);
+// Selection from given scores; counts must already hold the starting values.
+hipError_t launch_select_from_scores(const float* scores, const float* bias, int64_t T, int E, int K,
+                                     int32_t* idx, float* w, int32_t* counts, hipStream_t stream);
+
+// Tilings of the fused router kernel.
+struct RouterTiling {
+    int id;       // variant id (1-based)
+    int is_f32;   // input dtype of this tiling
+    int waves;    // waves per workgroup
+    int tbw;      // 32-token blocks per wave (tokens per workgroup = 32 * tbw)
+    int nblk;     // 32-expert blocks per wave
+};
+
+// Number of known tilings and the i-th one (0-based).
+int router_tiling_count();
+RouterTiling router_tiling(int i);
+
+struct RouterArgs {
+    const void* x;
+    const void* W;
+    const float* bias;
+    int64_t T;
+    int d;
+    int E;
+    int K;
+    int32_t* idx;
+    float* w;
+    int32_t* counts;
+    int zero_counts;  // workgroup 0 of the multi-slice kernel zeroes counts
+    float* dump;
+    // multi-slice candidates in the workspace: [T][slices][K]
+    float* cand_v;
+    float* cand_s;
+    int32_t* cand_i;
+};
+
+// Slices of E covered by one workgroup column for tiling t.
+inline int router_slices(const RouterTiling& t, int E) {
+    const int be = t.waves * t.nblk * 32;
+    return (E + be - 1) / be;
+}
+
+hipError_t launch_router_score_select(const RouterTiling& t, const RouterArgs& a, hipStream_t stream);
+hipError_t launch_router_merge(const RouterTiling& t, const RouterArgs& a, hipStream_t stream);
+
+}  // namespace idb

@@ -1,0 +1,54 @@
+"""One router + controller step on device buffers, built on the C ABI binding.
+
+A :class:`RouterStep` owns the per-step outputs (expert indices, gate weights,
+counts, load statistics), the router workspace and the controller state of one
+MoE layer, all as device tensors, and issues the ABI calls of one iteration of
+Alg. 1: route the batch with the current bias, update the bias from the
+counts, and compute MaxVio/MinVio.
+"""
+from __future__ import annotations
+
+import torch
+
+from . import binding as B
+
+
+class RouterStep:
+    def __init__(self, T: int, d: int, E: int, K: int, dtype: torch.dtype = torch.bfloat16,
+                 cfg: B.ControllerCfg | None = None, variant: int = 0, device: str = "cuda"):
+        self.T, self.d, self.E, self.K, self.dtype, self.variant = T, d, E, K, dtype, variant
+        code = B.IDB_DTYPE_BF16 if dtype == torch.bfloat16 else B.IDB_DTYPE_F32
+        self.dtype_code = code
+        self.cfg = cfg or B.ControllerCfg(E)
+        self.state = B.ControllerState(E, device)
+        self.idx = torch.empty((T, K), dtype=torch.int32, device=device)
+        self.w = torch.empty((T, K), dtype=torch.float32, device=device)
+        self.counts = torch.zeros(E, dtype=torch.int32, device=device)
+        self.stats = torch.zeros(2, dtype=torch.float64, device=device)
+        nbytes = B.idb_router_workspace_bytes(T, d, E, K, code, variant)
+        self.workspace = torch.empty(max(nbytes, 16), dtype=torch.uint8, device=device)
+        self.info = B.idb_router_variant_info(T, d, E, K, code, variant)
+
+    def route(self, x, W, accumulate: bool = False, scores_dump=None, stream=None):
+        B.idb_router_forward(x, W, self.state.bias, self.K, self.idx, self.w, self.counts, accumulate, scores_dump,
+                             self.workspace, self.variant, stream)
+
+    def score_select(self, x, W, accumulate: bool = False, scores_dump=None, stream=None):
+        B.idb_router_score_select(x, W, self.state.bias, self.K, self.idx, self.w, self.counts, accumulate,
+                                  scores_dump, self.workspace, self.variant, stream)
+
+    def merge(self, stream=None):
+        B.idb_router_merge(self.T, self.d, self.E, self.K, self.dtype_code, self.idx, self.w, self.counts,
+                           self.workspace, self.variant, stream)
+
+    def update(self, stream=None):
+        B.idb_controller_update(self.counts, self.cfg, self.state, stream)
+
+    def load_stats(self, stream=None):
+        B.idb_load_stats(self.counts, self.stats, stream)
+
+    def step(self, x, W, stream=None):
+        """Route, update the bias, compute MaxVio/MinVio (all asynchronous)."""
+        self.route(x, W, stream=stream)
+        self.update(stream)
+        self.load_stats(stream)

@@ -1,0 +1,151 @@
+"""C ABI checks that need no GPU: the library loads, exports every function
+include/idb.h declares, and rejects invalid arguments before any HIP call
+(the pointers below are never dereferenced)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2609_39137_amd import binding as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+A16 = 1 << 20  # a 16-byte aligned fake device address, never dereferenced
+
+
+def header_functions():
+    text = open(os.path.join(ROOT, "include", "idb.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(idb_[a-z_]+)\s*\(", text)))
+
+
+def test_library_exports_every_header_function():
+    names = header_functions()
+    assert len(names) >= 10
+    L = B.lib()
+    for n in names:
+        assert hasattr(L, n), f"libidb.so does not export {n}"
+    assert set(names) == set(B.EXPORTED)
+
+
+def router(T=128, d=256, E=768, K=10, dtype=B.IDB_DTYPE_BF16, x=A16, W=A16, bias=A16, idx=A16, w=A16, counts=A16,
+           dump=None, ws=A16, ws_bytes=1 << 30, variant=0, fn="idb_router_forward"):
+    return getattr(B.lib(), fn)(x, W, dtype, bias, T, d, E, K, idx, w, counts, 0, dump, ws, ws_bytes, variant, None)
+
+
+@pytest.mark.parametrize("fn", ["idb_router_forward", "idb_router_score_select"])
+@pytest.mark.parametrize("kw,code", [
+    (dict(T=0), B.IDB_ERR_INVALID_ARG),
+    (dict(T=(1 << 26) + 1), B.IDB_ERR_INVALID_ARG),
+    (dict(K=0), B.IDB_ERR_INVALID_ARG),
+    (dict(K=769), B.IDB_ERR_INVALID_ARG),
+    (dict(E=0), B.IDB_ERR_INVALID_ARG),
+    (dict(d=0), B.IDB_ERR_INVALID_ARG),
+    (dict(dtype=7), B.IDB_ERR_INVALID_ARG),
+    (dict(x=None), B.IDB_ERR_INVALID_ARG),
+    (dict(W=None), B.IDB_ERR_INVALID_ARG),
+    (dict(bias=None), B.IDB_ERR_INVALID_ARG),
+    (dict(idx=None), B.IDB_ERR_INVALID_ARG),
+    (dict(counts=None), B.IDB_ERR_INVALID_ARG),
+    (dict(x=A16 + 4), B.IDB_ERR_INVALID_ARG),
+    (dict(W=A16 + 8), B.IDB_ERR_INVALID_ARG),
+    (dict(bias=A16 + 2), B.IDB_ERR_INVALID_ARG),
+    (dict(dump=A16 + 4), B.IDB_ERR_INVALID_ARG),
+    (dict(ws=None), B.IDB_ERR_INVALID_ARG),
+    (dict(ws_bytes=16), B.IDB_ERR_INVALID_ARG),
+    (dict(variant=99), B.IDB_ERR_INVALID_ARG),
+    (dict(variant=5), B.IDB_ERR_UNSUPPORTED),   # the fp32 tiling asked for bf16 input
+    (dict(E=2048), B.IDB_ERR_UNSUPPORTED),
+    (dict(E=100, K=4), B.IDB_ERR_UNSUPPORTED),
+    (dict(K=33), B.IDB_ERR_UNSUPPORTED),
+    (dict(d=96), B.IDB_ERR_UNSUPPORTED),
+    (dict(d=48, dtype=B.IDB_DTYPE_F32, variant=5), B.IDB_ERR_UNSUPPORTED),
+])
+def test_router_rejects_invalid_arguments(fn, kw, code):
+    assert router(fn=fn, **kw) == code
+    assert B.idb_last_error() != ""
+
+
+def test_merge_rejects_invalid_arguments():
+    L = B.lib()
+    assert L.idb_router_merge(0, 256, 768, 10, 0, A16, A16, A16, A16, 1 << 30, 0, None) == B.IDB_ERR_INVALID_ARG
+    assert L.idb_router_merge(128, 256, 768, 10, 0, None, A16, A16, A16, 1 << 30, 0, None) == B.IDB_ERR_INVALID_ARG
+    assert L.idb_router_merge(128, 256, 768, 10, 0, A16, A16, A16, A16, 8, 0, None) == B.IDB_ERR_INVALID_ARG
+
+
+def test_workspace_and_variant_info():
+    # 768 experts in bf16: the automatic tiling splits them into two 384-expert slices.
+    info = B.idb_router_variant_info(16384, 2048, 768, 10, B.IDB_DTYPE_BF16, 0)
+    assert info == {"tokens_per_wg": 128, "slices": 2, "waves": 4, "blocks_per_wave": 3, "variant": 1}
+    nbytes = B.idb_router_workspace_bytes(16384, 2048, 768, 10, B.IDB_DTYPE_BF16, 0)
+    assert nbytes == 3 * 16384 * 2 * 10 * 4
+    # a single-slice tiling needs no workspace
+    info2 = B.idb_router_variant_info(16384, 2048, 768, 10, B.IDB_DTYPE_BF16, 2)
+    assert info2["slices"] == 1 and info2["tokens_per_wg"] == 64
+    assert B.idb_router_workspace_bytes(16384, 2048, 768, 10, B.IDB_DTYPE_BF16, 2) == 0
+    # fp32 input, 64 experts: one 128-expert slice, half padding
+    info3 = B.idb_router_variant_info(4096, 256, 64, 4, B.IDB_DTYPE_F32, 0)
+    assert info3["slices"] == 1 and info3["variant"] == 5
+    assert B.idb_router_workspace_bytes(0, 256, 64, 4, B.IDB_DTYPE_F32, 0) == 0
+    with pytest.raises(B.IdbError):
+        B.idb_router_variant_info(128, 256, 768, 10, B.IDB_DTYPE_BF16, 5)
+
+
+@pytest.mark.parametrize("args,code", [
+    (dict(T=0), B.IDB_ERR_INVALID_ARG),
+    (dict(K=0), B.IDB_ERR_INVALID_ARG),
+    (dict(K=65, E=64), B.IDB_ERR_INVALID_ARG),
+    (dict(E=1025, K=4), B.IDB_ERR_UNSUPPORTED),
+    (dict(K=33, E=64), B.IDB_ERR_UNSUPPORTED),
+    (dict(scores=None), B.IDB_ERR_INVALID_ARG),
+    (dict(scores=A16 + 2), B.IDB_ERR_INVALID_ARG),
+    (dict(counts=None), B.IDB_ERR_INVALID_ARG),
+])
+def test_select_rejects_invalid_arguments(args, code):
+    a = dict(scores=A16, bias=A16, T=64, E=64, K=4, idx=A16, w=A16, counts=A16)
+    a.update(args)
+    st = B.lib().idb_select_from_scores(a["scores"], a["bias"], a["T"], a["E"], a["K"], a["idx"], a["w"],
+                                        a["counts"], 0, None)
+    assert st == code
+
+
+def _state(**kw):
+    s = dict(bias=A16, e_prev=A16, step=A16, status=A16)
+    s.update(kw)
+    return B.idb_controller_state(s["bias"], s["e_prev"], s["step"], s["status"])
+
+
+@pytest.mark.parametrize("cfg,state,code", [
+    (dict(E=0), {}, B.IDB_ERR_INVALID_ARG),
+    (dict(E=1025), {}, B.IDB_ERR_INVALID_ARG),
+    (dict(Ki=-1.0), {}, B.IDB_ERR_INVALID_ARG),
+    (dict(Kd=float("nan")), {}, B.IDB_ERR_INVALID_ARG),
+    (dict(Ki=float("inf")), {}, B.IDB_ERR_INVALID_ARG),
+    (dict(integral_mode=2), {}, B.IDB_ERR_INVALID_ARG),
+    (dict(center=2), {}, B.IDB_ERR_INVALID_ARG),
+    (dict(), dict(bias=None), B.IDB_ERR_INVALID_ARG),
+    (dict(), dict(step=A16 + 4), B.IDB_ERR_INVALID_ARG),
+    (dict(), dict(e_prev=A16 + 2), B.IDB_ERR_INVALID_ARG),
+])
+def test_controller_rejects_invalid_arguments(cfg, state, code):
+    c = dict(E=768, Ki=6e-3, Kd=6e-3, integral_mode=0, center=1)
+    c.update(cfg)
+    ccfg = B.idb_controller_cfg(c["E"], c["Ki"], c["Kd"], c["integral_mode"], c["center"])
+    st = B.lib().idb_controller_update(A16, ctypes.byref(ccfg), ctypes.byref(_state(**state)), None)
+    assert st == code
+
+
+def test_controller_and_stats_null_pointers():
+    L = B.lib()
+    ccfg = B.idb_controller_cfg(8, 0.1, 0.1, 0, 1)
+    assert L.idb_controller_update(None, ctypes.byref(ccfg), ctypes.byref(_state()), None) == B.IDB_ERR_INVALID_ARG
+    assert L.idb_controller_update(A16, None, ctypes.byref(_state()), None) == B.IDB_ERR_INVALID_ARG
+    assert L.idb_load_stats(None, 8, A16, None) == B.IDB_ERR_INVALID_ARG
+    assert L.idb_load_stats(A16, 0, A16, None) == B.IDB_ERR_INVALID_ARG
+    assert L.idb_load_stats(A16, 8, A16 + 4, None) == B.IDB_ERR_INVALID_ARG
+
+
+def test_status_strings():
+    for s in range(5):
+        assert B.idb_status_string(s) != "unknown status"
+    assert B.idb_status_string(42) == "unknown status"

@@ -1,0 +1,92 @@
+"""Closed loops of Alg. 1 on the GPU.
+
+* Given identical scores: each step draws fresh synthetic scores (the same
+  arrays for both sides), routes them with the current bias, updates the bias
+  from the counts and computes MaxVio/MinVio -- on the GPU through the C ABI and
+  on the CPU oracle, independently.  Every step's selection, counts, bias,
+  e_prev and statistics must be bit-identical: the whole bias trajectory is
+  pinned.
+* From hidden states (the tiny fp32 workload): the GPU loop runs its own
+  router; each step its fused selection must equal the select kernel on its
+  dumped scores, the scores must match the oracle's within rel 2e-3, and the
+  free-running oracle loop must stay close (near-tie flips are reported).
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2609_39137_amd import binding as B
+from paper_2609_39137_amd import synth
+from paper_2609_39137_amd.pipeline import RouterStep
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+
+
+@pytest.mark.parametrize("T,E,K,steps,Ki,Kd,mode,center", [
+    (2048, 768, 10, 30, 6e-3, 6e-3, 0, True),
+    (4096, 768, 5, 40, 6e-3, 6e-3, 0, True),
+    (4096, 768, 3, 40, 6e-3, 0.0, 0, True),
+    (1024, 64, 4, 30, 1e-3, 0.0, 1, False),
+    (1000, 100, 7, 25, 0.05, 0.1, 0, True),
+])
+def test_closed_loop_given_scores_is_bit_exact(T, E, K, steps, Ki, Kd, mode, center):
+    cfg = B.ControllerCfg(E, Ki, Kd, mode, center)
+    st = B.ControllerState(E, DEV)
+    ref = oracle.ControllerState(E)
+    idx = torch.empty((T, K), dtype=torch.int32, device=DEV)
+    w = torch.empty((T, K), dtype=torch.float32, device=DEV)
+    counts = torch.empty(E, dtype=torch.int32, device=DEV)
+    stats = torch.empty(2, dtype=torch.float64, device=DEV)
+    for t in range(steps):
+        s = synth.scores(T, E, "beta", seed=1000 + t)
+        # skew the load so the controller has work: a fixed per-expert tilt
+        s = np.clip(s + (np.arange(E, dtype=np.float32) / E * 0.2)[None, :], 0, 1).astype(np.float32)
+        B.idb_select_from_scores(torch.from_numpy(s).to(DEV), st.bias, K, idx, w, counts)
+        B.idb_controller_update(counts, cfg, st)
+        B.idb_load_stats(counts, stats)
+        r_idx, r_w, r_c = oracle.select(s, ref.bias, K)
+        oracle.controller(r_c, ref, Ki, Kd, mode=mode, center=center)
+        np.testing.assert_array_equal(idx.cpu().numpy(), r_idx, err_msg=f"step {t}")
+        np.testing.assert_array_equal(w.cpu().numpy().view(np.uint32), r_w.view(np.uint32))
+        np.testing.assert_array_equal(counts.cpu().numpy(), r_c)
+        np.testing.assert_array_equal(st.bias.cpu().numpy(), ref.bias, err_msg=f"bias step {t}")
+        np.testing.assert_array_equal(st.e_prev.cpu().numpy(), ref.e_prev)
+        np.testing.assert_array_equal(stats.cpu().numpy(), oracle.load_stats(r_c))
+    assert int(st.step.item()) == steps
+
+
+def test_tiny_workload_router_loop():
+    wl = synth.WORKLOADS["tiny-e64-k4"]
+    W = synth.router_weight(wl)
+    Wt = torch.from_numpy(W).to(DEV)
+    rs = RouterStep(wl.T, wl.d, wl.E, wl.K, torch.float32)
+    ref = oracle.ControllerState(wl.E)
+    dump = torch.empty((wl.T, wl.E), dtype=torch.float32, device=DEV)
+    idx2 = torch.empty_like(rs.idx)
+    w2 = torch.empty_like(rs.w)
+    c2 = torch.empty_like(rs.counts)
+    flips = 0
+    for t in range(wl.steps):
+        x = synth.hidden_states(wl, step=t)
+        bias_before = rs.state.bias.clone()
+        rs.route(torch.from_numpy(x).to(DEV), Wt, scores_dump=dump)
+        B.idb_select_from_scores(dump, bias_before, wl.K, idx2, w2, c2)
+        assert torch.equal(rs.idx, idx2) and torch.equal(rs.w, w2) and torch.equal(rs.counts, c2)
+        rs.update()
+        rs.load_stats()
+        s_ref = oracle.router_scores(x, W)
+        s = dump.cpu().numpy()
+        assert np.all(np.abs(s.astype(np.float64) - s_ref) <= 2e-3 * np.abs(s_ref.astype(np.float64)))
+        r_idx, r_w, r_c = oracle.select(s_ref, ref.bias, wl.K)
+        oracle.controller(r_c, ref, 6e-3, 6e-3)
+        flips += int((np.sort(rs.idx.cpu().numpy(), 1) != np.sort(r_idx, 1)).any(1).sum())
+        counts = rs.counts.cpu().numpy()
+        assert int(counts.sum()) == wl.T * wl.K
+        mx, mn = rs.stats.cpu().numpy()
+        assert 0 <= mx <= wl.E / wl.K - 1 and 0 <= mn <= 1
+    # free-running oracle vs GPU: only near-tie flips may differ
+    assert flips <= 0.01 * wl.T * wl.steps
+    np.testing.assert_allclose(rs.state.bias.cpu().numpy(), ref.bias, atol=5e-4)
+    print(f"tiny loop: {flips} token selections differ from the free-running oracle over {wl.steps} steps")

@@ -1,0 +1,83 @@
+"""GPU parity of the selection stage given identical fp32 scores
+(Eq. pid-routing; gate weights of Sec. 2.2; counts of Eq. pid-error):
+expert indices, gate weights and counts must be bit-identical to the oracle's
+on the same synthetic scores, including heavy ties, +-0, saturated scores,
+ragged token counts, K > 16 and expert counts that are not multiples of 4."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2609_39137_amd import binding as B
+from paper_2609_39137_amd import synth
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+
+
+def gpu_select(s, b, K, counts=None):
+    T, E = s.shape
+    st = torch.from_numpy(s).to(DEV)
+    bt = torch.from_numpy(b).to(DEV)
+    idx = torch.empty((T, K), dtype=torch.int32, device=DEV)
+    w = torch.empty((T, K), dtype=torch.float32, device=DEV)
+    acc = counts is not None
+    c = counts if acc else torch.full((E,), 12345, dtype=torch.int32, device=DEV)
+    B.idb_select_from_scores(st, bt, K, idx, w, c, accumulate=acc)
+    return idx.cpu().numpy(), w.cpu().numpy(), c.cpu().numpy()
+
+
+def check(s, b, K):
+    idx, w, c = gpu_select(s, b, K)
+    ridx, rw, rc = oracle.select(s, b, K)
+    np.testing.assert_array_equal(idx, ridx)
+    np.testing.assert_array_equal(w.view(np.uint32), rw.view(np.uint32))
+    np.testing.assert_array_equal(c, rc)
+
+
+@pytest.mark.parametrize("E", [32, 64, 100, 256, 768, 1024])
+@pytest.mark.parametrize("kind", ["beta", "grid", "edges", "saturated"])
+def test_select_matches_oracle(E, kind):
+    for T, K, bkind in ((1, 1, "zero"), (17, 3, "small"), (333, 10, "grid"), (1000, min(16, E), "large"),
+                        (257, min(17, E), "small"), (64, min(32, E), "grid")):
+        s = synth.scores(T, E, kind, seed=T + E)
+        b = synth.bias(E, bkind, seed=K)
+        check(s, b, K)
+
+
+def test_all_equal_scores_take_lowest_indices():
+    s = synth.scores(50, 768, "const", seed=0)
+    for K in (1, 10, 32):
+        check(s, np.zeros(768, np.float32), K)
+        idx, _, _ = gpu_select(s, np.zeros(768, np.float32), K)
+        assert np.all(idx == np.arange(K)[None, :])
+
+
+def test_headline_shape_full_size():
+    s = synth.scores(16384, 768, "beta", seed=1)
+    b = synth.bias(768, "small", seed=2)
+    check(s, b, 10)
+
+
+def test_counts_accumulate_over_microbatches():
+    s = synth.scores(3000, 768, "beta", seed=4)
+    b = synth.bias(768, "small", seed=5)
+    counts = torch.zeros(768, dtype=torch.int32, device=DEV)
+    for lo, hi in ((0, 1000), (1000, 1001), (1001, 3000)):
+        gpu_select(np.ascontiguousarray(s[lo:hi]), b, 5, counts=counts)
+    _, _, rc = oracle.select(s, b, 5)
+    np.testing.assert_array_equal(counts.cpu().numpy(), rc)
+
+
+def test_gate_weights_sum_to_one_and_ignore_bias():
+    s = synth.scores(2000, 768, "beta", seed=8)
+    idx0, w0, _ = gpu_select(s, np.zeros(768, np.float32), 10)
+    assert np.all(np.abs(w0.astype(np.float64).sum(1) - 1.0) <= 10 * 2.0 ** -23)
+    # shifting every bias by the same dyadic constant keeps sets and weights
+    # when the sums are exact: scores on a 2^-12 grid
+    g = (np.round(s * 4096) / 4096).astype(np.float32)
+    b = synth.bias(768, "grid", seed=9)
+    i1, w1, _ = gpu_select(g, b, 10)
+    i2, w2, _ = gpu_select(g, (b + np.float32(0.5)).astype(np.float32), 10)
+    np.testing.assert_array_equal(i1, i2)
+    np.testing.assert_array_equal(w1, w2)
