@@ -59,6 +59,11 @@ typedef enum idb_dtype {
     IDB_DTYPE_F32 = 1   /* x and W_g hold fp32 values                         */
 } idb_dtype;
 
+typedef enum idb_weight_layout {
+    IDB_WEIGHT_ROW_MAJOR = 0, /* W_g is [E][d] row-major                                  */
+    IDB_WEIGHT_PACKED = 1     /* W_g was written by idb_router_pack_weight (same byte size) */
+} idb_weight_layout;
+
 typedef enum idb_integral_mode {
     IDB_INTEGRAL_ERROR = 0, /* ID Balancing: integral step K_i * e (Eq. rapid-integral)   */
     IDB_INTEGRAL_SIGN = 1   /* DeepSeek loss-free: K_i * sign(e), sign(0) = 0 (Eq. pid-deepseek) */
@@ -88,7 +93,8 @@ typedef struct idb_controller_state {
  * Router step (Sec. 2.2; Eq. pid-routing; Eq. pid-error counts).
  *
  *   x           [T][d] hidden states, dtype as given, 16-byte aligned.
- *   W_g         [E][d] router matrix W_r, same dtype.
+ *   W_g         [E][d] router matrix W_r, same dtype, row-major or in the
+ *               packed layout of idb_router_pack_weight (weight_layout).
  *   bias        [E] fp32 expert bias b, read only (frozen within the step).
  *   T, d, E, K  tokens, hidden size, experts, experts per token.
  *               1 <= T <= 2^26; 1 <= K <= E; E <= 1024, E % 32 == 0 and
@@ -113,7 +119,8 @@ typedef struct idb_controller_state {
  * ------------------------------------------------------------------------- */
 size_t idb_router_workspace_bytes(int64_t T, int32_t d, int32_t E, int32_t K, idb_dtype dtype, int32_t variant);
 
-idb_status idb_router_forward(const void* x, const void* W_g, idb_dtype dtype, const float* bias, int64_t T,
+idb_status idb_router_forward(const void* x, const void* W_g, idb_dtype dtype, idb_weight_layout weight_layout,
+                              const float* bias, int64_t T,
                               int32_t d, int32_t E, int32_t K, int32_t* expert_idx, float* gate_w,
                               int32_t* counts, int32_t accumulate_counts, float* scores_dump, void* workspace,
                               size_t workspace_bytes, int32_t variant, hipStream_t stream);
@@ -127,13 +134,25 @@ idb_status idb_router_forward(const void* x, const void* W_g, idb_dtype dtype, c
  *   merge:        merges the slices' candidates into the final Top-K, gate
  *                 weights and counts; enqueues nothing for single-slice
  *                 tilings. */
-idb_status idb_router_score_select(const void* x, const void* W_g, idb_dtype dtype, const float* bias, int64_t T,
+idb_status idb_router_score_select(const void* x, const void* W_g, idb_dtype dtype, idb_weight_layout weight_layout,
+                                   const float* bias, int64_t T,
                                    int32_t d, int32_t E, int32_t K, int32_t* expert_idx, float* gate_w,
                                    int32_t* counts, int32_t accumulate_counts, float* scores_dump,
                                    void* workspace, size_t workspace_bytes, int32_t variant, hipStream_t stream);
 idb_status idb_router_merge(int64_t T, int32_t d, int32_t E, int32_t K, idb_dtype dtype, int32_t* expert_idx,
                             float* gate_w, int32_t* counts, void* workspace, size_t workspace_bytes,
                             int32_t variant, hipStream_t stream);
+
+/* The router matrix in the layout the MFMA A operands are read in: for every
+ * 32-expert block b, 128-byte chunk c of the rows and 16-byte unit u < 4, one
+ * contiguous 1 KB piece holds, for lane l = 32 h + m (h < 2, m < 32), bytes
+ * [c*128 + 64 h + 16 u, +16) of row 32 b + m.  A pure byte permutation of
+ * W_g; packing once per weight update lets every router call read W with
+ * fully coalesced loads.  W_packed must not overlap W_g; both 16-byte aligned.
+ * E % 32 == 0, d as for idb_router_forward. */
+size_t idb_router_packed_weight_bytes(int32_t E, int32_t d, idb_dtype dtype);
+idb_status idb_router_pack_weight(const void* W_g, idb_dtype dtype, int32_t E, int32_t d, void* W_packed,
+                                  hipStream_t stream);
 
 /* Tiling of a variant for a shape: out[0] = tokens per workgroup, out[1] =
  * expert slices, out[2] = waves per workgroup, out[3] = 32-expert blocks per

@@ -24,13 +24,15 @@ IDB_ERR_HIP = 4
 
 IDB_DTYPE_BF16 = 0
 IDB_DTYPE_F32 = 1
+IDB_WEIGHT_ROW_MAJOR = 0
+IDB_WEIGHT_PACKED = 1
 IDB_INTEGRAL_ERROR = 0
 IDB_INTEGRAL_SIGN = 1
 
 EXPORTED = (
     "idb_router_workspace_bytes", "idb_router_forward", "idb_router_score_select", "idb_router_merge",
     "idb_router_variant_info", "idb_select_from_scores", "idb_controller_update", "idb_load_stats",
-    "idb_status_string", "idb_last_error",
+    "idb_status_string", "idb_last_error", "idb_router_packed_weight_bytes", "idb_router_pack_weight",
 )
 
 
@@ -62,7 +64,7 @@ def lib() -> ctypes.CDLL:
         raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2609_39137_amd.build`")
     L = ctypes.CDLL(LIB_PATH)
     P, i64, i32, sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_size_t
-    router_args = [P, P, i32, P, i64, i32, i32, i32, P, P, P, i32, P, P, sz, i32, P]
+    router_args = [P, P, i32, i32, P, i64, i32, i32, i32, P, P, P, i32, P, P, sz, i32, P]
     L.idb_router_workspace_bytes.argtypes = [i64, i32, i32, i32, i32, i32]
     L.idb_router_workspace_bytes.restype = sz
     for name in ("idb_router_forward", "idb_router_score_select"):
@@ -70,6 +72,10 @@ def lib() -> ctypes.CDLL:
         getattr(L, name).restype = ctypes.c_int
     L.idb_router_merge.argtypes = [i64, i32, i32, i32, i32, P, P, P, P, sz, i32, P]
     L.idb_router_merge.restype = ctypes.c_int
+    L.idb_router_packed_weight_bytes.argtypes = [i32, i32, i32]
+    L.idb_router_packed_weight_bytes.restype = sz
+    L.idb_router_pack_weight.argtypes = [P, i32, i32, i32, P, P]
+    L.idb_router_pack_weight.restype = ctypes.c_int
     L.idb_router_variant_info.argtypes = [i64, i32, i32, i32, i32, i32, P]
     L.idb_router_variant_info.restype = ctypes.c_int
     L.idb_select_from_scores.argtypes = [P, P, i64, i32, i32, P, P, P, i32, P]
@@ -134,8 +140,21 @@ def idb_router_variant_info(T: int, d: int, E: int, K: int, dtype: int, variant:
     return {"tokens_per_wg": out[0], "slices": out[1], "waves": out[2], "blocks_per_wave": out[3], "variant": out[4]}
 
 
+def idb_router_packed_weight_bytes(E: int, d: int, dtype: int) -> int:
+    return int(lib().idb_router_packed_weight_bytes(E, d, dtype))
+
+
+def idb_router_pack_weight(W_g, W_packed, stream=None):
+    """Write ``W_g`` [E][d] into ``W_packed`` (same shape and dtype) in the MFMA A-operand layout."""
+    E, d = W_g.shape
+    if W_packed.shape != W_g.shape or W_packed.dtype != W_g.dtype:
+        raise ValueError("W_packed must match W_g in shape and dtype")
+    st = lib().idb_router_pack_weight(_ptr(W_g), _dtype_code(W_g), E, d, _ptr(W_packed), _stream(stream))
+    _check("idb_router_pack_weight", st)
+
+
 def _router_call(fn: str, x, W_g, bias, K, expert_idx, gate_w, counts, accumulate, scores_dump, workspace,
-                 variant, stream):
+                 variant, stream, weight_layout=IDB_WEIGHT_ROW_MAJOR):
     T, d = x.shape
     E = W_g.shape[0]
     if W_g.shape[1] != d or W_g.dtype != x.dtype or bias.shape != (E,) or bias.dtype != torch.float32:
@@ -143,23 +162,24 @@ def _router_call(fn: str, x, W_g, bias, K, expert_idx, gate_w, counts, accumulat
     if expert_idx.shape != (T, K) or gate_w.shape != (T, K) or counts.shape != (E,):
         raise ValueError("router outputs have the wrong shape")
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
-    st = getattr(lib(), fn)(_ptr(x), _ptr(W_g), _dtype_code(x), _ptr(bias), T, d, E, K, _ptr(expert_idx),
+    st = getattr(lib(), fn)(_ptr(x), _ptr(W_g), _dtype_code(x), int(weight_layout), _ptr(bias), T, d, E, K,
+                            _ptr(expert_idx),
                             _ptr(gate_w), _ptr(counts), int(bool(accumulate)), _ptr(scores_dump),
                             _ptr(workspace), ws_bytes, int(variant), _stream(stream))
     _check(fn, st)
 
 
 def idb_router_forward(x, W_g, bias, K, expert_idx, gate_w, counts, accumulate=False, scores_dump=None,
-                       workspace=None, variant=0, stream=None):
+                       workspace=None, variant=0, stream=None, weight_layout=IDB_WEIGHT_ROW_MAJOR):
     """Router step (gate contraction, sigmoid, biased Top-K, gate weights, counts) on ``stream``."""
     _router_call("idb_router_forward", x, W_g, bias, K, expert_idx, gate_w, counts, accumulate, scores_dump,
-                 workspace, variant, stream)
+                 workspace, variant, stream, weight_layout)
 
 
 def idb_router_score_select(x, W_g, bias, K, expert_idx, gate_w, counts, accumulate=False, scores_dump=None,
-                            workspace=None, variant=0, stream=None):
+                            workspace=None, variant=0, stream=None, weight_layout=IDB_WEIGHT_ROW_MAJOR):
     _router_call("idb_router_score_select", x, W_g, bias, K, expert_idx, gate_w, counts, accumulate, scores_dump,
-                 workspace, variant, stream)
+                 workspace, variant, stream, weight_layout)
 
 
 def idb_router_merge(T, d, E, K, dtype, expert_idx, gate_w, counts, workspace=None, variant=0, stream=None):

@@ -96,12 +96,15 @@ struct RouterCall {
     idb::RouterArgs args;
 };
 
-idb_status prepare_router(const void* x, const void* W_g, idb_dtype dtype, const float* bias, int64_t T, int32_t d,
+idb_status prepare_router(const void* x, const void* W_g, idb_dtype dtype, idb_weight_layout layout,
+                          const float* bias, int64_t T, int32_t d,
                           int32_t E, int32_t K, int32_t* expert_idx, float* gate_w, int32_t* counts,
                           int32_t accumulate_counts, float* scores_dump, void* workspace, size_t workspace_bytes,
                           int32_t variant, bool need_inputs, RouterCall* call) {
     idb_status st = check_router_shape(T, d, E, K, dtype);
     if (st != IDB_OK) return st;
+    if (layout != IDB_WEIGHT_ROW_MAJOR && layout != IDB_WEIGHT_PACKED)
+        return fail(IDB_ERR_INVALID_ARG, "unknown weight layout %d", layout);
     if (need_inputs) {
         if (!x || !W_g || !bias) return fail(IDB_ERR_INVALID_ARG, "null input pointer");
         if (!aligned(x, 16) || !aligned(W_g, 16)) return fail(IDB_ERR_INVALID_ARG, "x and W_g must be 16-byte aligned");
@@ -123,6 +126,7 @@ idb_status prepare_router(const void* x, const void* W_g, idb_dtype dtype, const
     idb::RouterArgs& a = call->args;
     a.x = x;
     a.W = W_g;
+    a.w_packed = layout == IDB_WEIGHT_PACKED;
     a.bias = bias;
     a.T = T;
     a.d = d;
@@ -178,12 +182,12 @@ idb_status idb_router_variant_info(int64_t T, int32_t d, int32_t E, int32_t K, i
     return IDB_OK;
 }
 
-idb_status idb_router_score_select(const void* x, const void* W_g, idb_dtype dtype, const float* bias, int64_t T,
-                                   int32_t d, int32_t E, int32_t K, int32_t* expert_idx, float* gate_w,
-                                   int32_t* counts, int32_t accumulate_counts, float* scores_dump, void* workspace,
-                                   size_t workspace_bytes, int32_t variant, hipStream_t stream) {
+idb_status idb_router_score_select(const void* x, const void* W_g, idb_dtype dtype, idb_weight_layout weight_layout,
+                                   const float* bias, int64_t T, int32_t d, int32_t E, int32_t K, int32_t* expert_idx,
+                                   float* gate_w, int32_t* counts, int32_t accumulate_counts, float* scores_dump,
+                                   void* workspace, size_t workspace_bytes, int32_t variant, hipStream_t stream) {
     RouterCall c;
-    idb_status st = prepare_router(x, W_g, dtype, bias, T, d, E, K, expert_idx, gate_w, counts, accumulate_counts,
+    idb_status st = prepare_router(x, W_g, dtype, weight_layout, bias, T, d, E, K, expert_idx, gate_w, counts, accumulate_counts,
                                    scores_dump, workspace, workspace_bytes, variant, true, &c);
     if (st != IDB_OK) return st;
     return enqueue_score_select(c, accumulate_counts, stream);
@@ -193,23 +197,42 @@ idb_status idb_router_merge(int64_t T, int32_t d, int32_t E, int32_t K, idb_dtyp
                             float* gate_w, int32_t* counts, void* workspace, size_t workspace_bytes, int32_t variant,
                             hipStream_t stream) {
     RouterCall c;
-    idb_status st = prepare_router(nullptr, nullptr, dtype, nullptr, T, d, E, K, expert_idx, gate_w, counts, 1,
+    idb_status st = prepare_router(nullptr, nullptr, dtype, IDB_WEIGHT_ROW_MAJOR, nullptr, T, d, E, K, expert_idx, gate_w, counts, 1,
                                    nullptr, workspace, workspace_bytes, variant, false, &c);
     if (st != IDB_OK) return st;
     return hip_result(idb::launch_router_merge(c.tiling, c.args, stream), "router merge launch");
 }
 
-idb_status idb_router_forward(const void* x, const void* W_g, idb_dtype dtype, const float* bias, int64_t T,
-                              int32_t d, int32_t E, int32_t K, int32_t* expert_idx, float* gate_w, int32_t* counts,
-                              int32_t accumulate_counts, float* scores_dump, void* workspace,
-                              size_t workspace_bytes, int32_t variant, hipStream_t stream) {
+idb_status idb_router_forward(const void* x, const void* W_g, idb_dtype dtype, idb_weight_layout weight_layout,
+                              const float* bias, int64_t T, int32_t d, int32_t E, int32_t K, int32_t* expert_idx,
+                              float* gate_w, int32_t* counts, int32_t accumulate_counts, float* scores_dump,
+                              void* workspace, size_t workspace_bytes, int32_t variant, hipStream_t stream) {
     RouterCall c;
-    idb_status st = prepare_router(x, W_g, dtype, bias, T, d, E, K, expert_idx, gate_w, counts, accumulate_counts,
+    idb_status st = prepare_router(x, W_g, dtype, weight_layout, bias, T, d, E, K, expert_idx, gate_w, counts, accumulate_counts,
                                    scores_dump, workspace, workspace_bytes, variant, true, &c);
     if (st != IDB_OK) return st;
     st = enqueue_score_select(c, accumulate_counts, stream);
     if (st != IDB_OK) return st;
     return hip_result(idb::launch_router_merge(c.tiling, c.args, stream), "router merge launch");
+}
+
+size_t idb_router_packed_weight_bytes(int32_t E, int32_t d, idb_dtype dtype) {
+    if (check_router_shape(1, d, E, 1, dtype) != IDB_OK) return 0;
+    return (size_t)E * d * (dtype == IDB_DTYPE_BF16 ? 2 : 4);
+}
+
+idb_status idb_router_pack_weight(const void* W_g, idb_dtype dtype, int32_t E, int32_t d, void* W_packed,
+                                  hipStream_t stream) {
+    idb_status st = check_router_shape(1, d, E, 1, dtype);
+    if (st != IDB_OK) return st;
+    if (!W_g || !W_packed) return fail(IDB_ERR_INVALID_ARG, "null pointer");
+    if (!aligned(W_g, 16) || !aligned(W_packed, 16)) return fail(IDB_ERR_INVALID_ARG, "W_g and W_packed must be 16-byte aligned");
+    const size_t bytes = (size_t)E * d * (dtype == IDB_DTYPE_BF16 ? 2 : 4);
+    const char* a0 = static_cast<const char*>(W_g);
+    const char* b0 = static_cast<const char*>(W_packed);
+    if (a0 < b0 + bytes && b0 < a0 + bytes) return fail(IDB_ERR_INVALID_ARG, "W_packed overlaps W_g");
+    const int64_t rb = (int64_t)d * (dtype == IDB_DTYPE_BF16 ? 2 : 4);
+    return hip_result(idb::launch_pack_weight(W_g, W_packed, E, rb, stream), "pack weight launch");
 }
 
 idb_status idb_select_from_scores(const float* scores, const float* bias, int64_t T, int32_t E, int32_t K,

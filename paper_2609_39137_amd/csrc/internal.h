@@ -34,6 +34,7 @@ RouterTiling router_tiling(int i);
 struct RouterArgs {
     const void* x;
     const void* W;
+    int w_packed;  // W is in the packed layout of launch_pack_weight
     const float* bias;
     int64_t T;
     int d;
@@ -58,5 +59,7 @@ inline int router_slices(const RouterTiling& t, int E) {
 
 hipError_t launch_router_score_select(const RouterTiling& t, const RouterArgs& a, hipStream_t stream);
 hipError_t launch_router_merge(const RouterTiling& t, const RouterArgs& a, hipStream_t stream);
+// Router matrix [E][d] (row_bytes per row) -> the packed A-operand layout.
+hipError_t launch_pack_weight(const void* W, void* P, int E, int64_t row_bytes, hipStream_t stream);
 
 }  // namespace idb

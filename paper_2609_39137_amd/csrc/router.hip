@@ -5,26 +5,38 @@
 //
 // Tiling.  A workgroup owns BT = 32*TBW tokens and one slice of BE =
 // WAVES*32*NBLK experts.  Each wave owns all BT tokens and its own 32*NBLK
-// experts, so the router rows it multiplies are private to it and come
-// straight from global memory into MFMA A-operand registers, while the token
-// tile is shared by the waves through a double-buffered LDS stage.  The
-// contraction runs over 128-byte chunks of each row; within a chunk, lane half
-// h of every 32-lane group consumes bytes [64h, 64h + 64) in four 16-byte
-// units, for both operands, so the k order is consistent between them.
+// experts: its router rows are private to it and go straight from global
+// memory into MFMA A-operand registers, while the token tile is shared by the
+// waves through LDS.  The contraction runs over 128-byte chunks of each row.
+// Within a chunk, lane half h of every 32-lane group consumes bytes
+// [64h, 64h + 64) in four 16-byte units, identically for both operands, so the
+// k order agrees between them.
+//
+// Token tile: staged through registers into two LDS stages of 144-byte rows
+// (128 bytes + 16 of padding, so the MFMA B-operand reads of 32 rows are free
+// of bank conflicts), loaded one chunk ahead of use.
+//
+// Router matrix: either row-major [E][d] (each A-operand load touches 32 rows)
+// or the packed layout written by idb_router_pack_weight, in which the 64
+// lanes' 16-byte A operands of one (32-expert block, chunk, unit) are one
+// contiguous 1 KB piece.
 //
 // MFMA 32x32 output layout (C = W_block * x_block^T): lane l holds token
 // (l % 32) of the block and experts 8*(r/4) + 4*(l/32) + (r%4), r < 16.  So a
 // token's BE scores are spread over 2*WAVES lanes, 16*NBLK per lane.
 //
 // Epilogue per token and slice (exact for any input):
-//   1. s = sigmoid(z), v = fl32(s + b).
-//   2. Each lane splits its values into G groups (16 group maxima per token);
+//   1. s = sigmoid(z) (computed once), v = fl32(s + b).
+//   2. Each lane splits its values into G groups, 16 group maxima per token;
 //      tau = the K-th largest group maximum <= the token's K-th largest v.
-//   3. Values >= tau go to an LDS candidate list (about K + 5 of them).
+//   3. Each lane counts its values >= tau; a prefix over the token's lanes
+//      gives every lane its write offset, and the candidates (typically about
+//      K + 5) are written to an LDS list without atomics.
 //   4. Candidate rank = number of candidates above it in the order (v desc,
-//      index asc); ranks < K form the slice's selection in rank order.
-//   5. Overflowing lists (ties, K > 16) fall back to K rounds of "best value
-//      strictly below the previous pick" over all the token's lanes.
+//      index asc); ranks < K are the slice's selection, in rank order.
+//   5. Lists that would overflow (heavy ties, K > 16) are resolved one token
+//      at a time: the token's values are gathered into an LDS row and one wave
+//      takes K rounds of wave-wide argmax.
 //   6. One slice: gate weights, outputs and an LDS histogram flushed with one
 //      atomic per non-zero bin.  Several slices: the slice's K candidates go
 //      to the workspace and router_merge_kernel combines them.
@@ -37,7 +49,7 @@ namespace idb {
 
 namespace {
 
-constexpr int kCap = 32;      // candidate list capacity per token and slice
+constexpr int kCap = 32;     // candidate list capacity per token and slice
 constexpr int kRowPad = 144;  // LDS bytes per staged token row (128 + 16 pad)
 constexpr int kMaxSlices = 8;
 
@@ -51,33 +63,36 @@ struct Cfg {
     static constexpr int G = 8 / WAVES;      // groups per lane: 2*WAVES*G = 16
     static constexpr int GS = NV / G;        // values per group
     static constexpr int TPT = NT / BT;      // threads per token in the ranking
-    static constexpr int PPT = BT * 8 / NT;  // 16-byte x pieces per thread per chunk
+    static constexpr int NLANES = 2 * WAVES;  // lanes holding one token's slice
+    static constexpr int PPT = BT * 8 / NT;  // 16-byte token-tile pieces per thread per chunk
     static constexpr int STAGE = BT * kRowPad;
     static constexpr int MAIN_LDS = 2 * STAGE;
-    static constexpr int NLANES = 2 * WAVES;  // lanes holding one token's slice
-    // epilogue LDS layout (bytes)
+    // epilogue LDS layout (bytes).  Per-token rows are padded (17, NLANES+1 and
+    // 36 words) so the 32 tokens of a wave fall on different LDS banks; the
+    // 36-word rows are also 16-byte aligned for vector reads.
+    static constexpr int GMS = 17;            // group-maximum row stride (words)
+    static constexpr int CNS = NLANES + 1;    // count row stride
+    static constexpr int LST = kCap + 4;      // candidate / selection row stride
     static constexpr int OFF_GM = 0;
-    static constexpr int OFF_TAU = OFF_GM + BT * 16 * 4;
+    static constexpr int OFF_TAU = OFF_GM + BT * GMS * 4;
     static constexpr int OFF_CNT = OFF_TAU + BT * 4;
-    static constexpr int OFF_PV = OFF_CNT + BT * 4;
-    static constexpr int OFF_PI = OFF_PV + BT * 4;
-    static constexpr int OFF_LV = OFF_PI + BT * 4;
-    static constexpr int OFF_LS = OFF_LV + BT * kCap * 4;
-    static constexpr int OFF_LI = OFF_LS + BT * kCap * 4;
-    static constexpr int OFF_SV = OFF_LI + BT * kCap * 4;
-    static constexpr int OFF_SS = OFF_SV + BT * kMaxK * 4;
-    static constexpr int OFF_SI = OFF_SS + BT * kMaxK * 4;
-    static constexpr int OFF_RV = OFF_SI + BT * kMaxK * 4;
-    static constexpr int OFF_RS = OFF_RV + BT * NLANES * 4;
-    static constexpr int OFF_RI = OFF_RS + BT * NLANES * 4;
-    static constexpr int OFF_HIST = OFF_RI + BT * NLANES * 4;
-    static constexpr int OFF_FLAG = OFF_HIST + 1024 * 4;
-    static constexpr int OFF_BIAS = OFF_FLAG + 16;
-    static constexpr int EPI_LDS = OFF_BIAS + BE * 4;
+    static constexpr int OFF_LV = ((OFF_CNT + BT * CNS * 4) + 15) / 16 * 16;
+    static constexpr int OFF_LS = OFF_LV + BT * LST * 4;
+    static constexpr int OFF_LI = OFF_LS + BT * LST * 4;
+    static constexpr int OFF_SV = OFF_LI + BT * LST * 4;
+    static constexpr int OFF_SS = OFF_SV + BT * LST * 4;
+    static constexpr int OFF_SI = OFF_SS + BT * LST * 4;
+    static constexpr int OFF_OVF = OFF_SI + BT * LST * 4;
+    static constexpr int OFF_ROWV = OFF_OVF + 16 * 4;
+    static constexpr int OFF_ROWS = OFF_ROWV + BE * 4;
+    static constexpr int OFF_HIST = OFF_ROWS + BE * 4;
+    static constexpr int EPI_LDS = OFF_HIST + 1024 * 4;
     static constexpr int LDS = MAIN_LDS > EPI_LDS ? MAIN_LDS : EPI_LDS;
     static_assert(BT <= NT, "one thread per token in the threshold step");
     static_assert(NV % G == 0, "groups must split a lane's values evenly");
-    static_assert(PPT * NT == BT * 8, "x pieces must split evenly");
+    static_assert(PPT * NT == BT * 8, "token-tile pieces must split evenly over threads");
+    static_assert(BT <= 16 * 32, "overflow bitmask size");
+    static_assert(BE % 64 == 0, "overflow gather row is read 64 lanes at a time");
 };
 
 // One 16-byte unit of both operands: bf16 -> one 32x32x16 MFMA; fp32 -> four
@@ -99,7 +114,11 @@ __device__ __forceinline__ floatx16 mfma_unit(uint4 a, uint4 b, floatx16 c) {
     }
 }
 
-template <bool F32, int WAVES, int TBW, int NBLK>
+__device__ __forceinline__ float comp4(const float4& f, int i) {
+    return i == 0 ? f.x : (i == 1 ? f.y : (i == 2 ? f.z : f.w));
+}
+
+template <bool F32, bool PACKED, int WAVES, int TBW, int NBLK>
 __global__ __launch_bounds__(WAVES * 64) void router_score_select_kernel(RouterArgs a, int NS) {
     using C = Cfg<F32, WAVES, TBW, NBLK>;
     __shared__ __attribute__((aligned(16))) unsigned char smem[C::LDS];
@@ -112,7 +131,7 @@ __global__ __launch_bounds__(WAVES * 64) void router_score_select_kernel(RouterA
 
     // XCD-aware block order: consecutive blocks land on different XCDs, so
     // remap to give each XCD a contiguous run of (tile, slice) pairs; the
-    // slices of one token tile then share their x rows in that XCD's L2.
+    // slices of one token tile then share their token rows in that XCD's L2.
     const int nb = gridDim.x;
     int L = blockIdx.x;
     if ((nb & 7) == 0) L = (blockIdx.x & 7) * (nb >> 3) + (blockIdx.x >> 3);
@@ -131,25 +150,33 @@ __global__ __launch_bounds__(WAVES * 64) void router_score_select_kernel(RouterA
         for (int e = tid; e < E; e += C::NT) a.counts[e] = 0;
 
     // ---------------------------------------------------------------- contraction
+    // A operands (router rows): byte strides of a chunk and of a unit.
+    constexpr int WU = PACKED ? 1024 : 16;
+    constexpr int64_t WCH = PACKED ? 4096 : 128;
     const char* wrow[NBLK];
 #pragma unroll
     for (int nbk = 0; nbk < NBLK; ++nbk) {
-        int e = e_wave0 + nbk * 32 + l32;
-        e = e < E ? e : E - 1;  // rows past E are loaded from a valid row and masked later
-        wrow[nbk] = reinterpret_cast<const char*>(a.W) + (int64_t)e * RB + 64 * h;
+        int blk = (e_wave0 + nbk * 32) / 32;
+        blk = blk < E / 32 ? blk : E / 32 - 1;  // padding blocks read a valid block; masked later
+        if constexpr (PACKED)
+            wrow[nbk] = reinterpret_cast<const char*>(a.W) + (int64_t)blk * NCH * 4096 + lane * 16;
+        else
+            wrow[nbk] = reinterpret_cast<const char*>(a.W) + (int64_t)(blk * 32 + l32) * RB + 64 * h;
     }
+    // Token-tile pieces: thread piece p = tid + NT*q covers row p/8, bytes
+    // 16*(p%8) of the chunk.  Rows past T re-read row T-1 (never output).
     const char* xsrc[C::PPT];
     int xdst[C::PPT];
-    bool xok[C::PPT];
 #pragma unroll
     for (int q = 0; q < C::PPT; ++q) {
         const int p = tid + C::NT * q;
         const int row = p >> 3, c16 = p & 7;
-        const int64_t tok = tok0 + row;
-        xok[q] = tok < T;
-        xsrc[q] = reinterpret_cast<const char*>(a.x) + (xok[q] ? tok : 0) * RB + c16 * 16;
+        int64_t tok = tok0 + row;
+        tok = tok < T ? tok : T - 1;
+        xsrc[q] = reinterpret_cast<const char*>(a.x) + tok * RB + c16 * 16;
         xdst[q] = row * kRowPad + c16 * 16;
     }
+    const int boff = l32 * kRowPad + 64 * h;
 
     floatx16 acc[TBW][NBLK];
 #pragma unroll
@@ -159,33 +186,34 @@ __global__ __launch_bounds__(WAVES * 64) void router_score_select_kernel(RouterA
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[tb][nbk][r] = 0.0f;
 
-    // W operands: one register set, refilled unit by unit.  Right after the
-    // MFMAs of unit u of chunk c are issued, the same registers start loading
-    // unit u of chunk c+1, which gives each load a whole chunk of MFMA work to
-    // arrive.
+    // Software pipeline.  W operands: one register set refilled unit by unit
+    // (right after the MFMAs of unit u of chunk c, the same registers start
+    // loading unit u of chunk c+1).  Token tile: loaded into staging registers
+    // at the top of chunk c for chunk c+1, stored into the idle LDS stage at
+    // the end of chunk c.  Vector-memory loads complete in order, and in this
+    // issue order each wait the compiler inserts covers only the data about
+    // to be used.
     uint4 w[NBLK][4], xr[C::PPT];
-
     auto load_x = [&](int c) {
 #pragma unroll
-        for (int q = 0; q < C::PPT; ++q) xr[q] = xok[q] ? ld16(xsrc[q] + c * 128) : make_uint4(0, 0, 0, 0);
+        for (int q = 0; q < C::PPT; ++q) xr[q] = ld16(xsrc[q] + c * 128);
     };
     auto store_x = [&](int stage) {
 #pragma unroll
-        for (int q = 0; q < C::PPT; ++q)
-            *reinterpret_cast<uint4*>(smem + stage * C::STAGE + xdst[q]) = xr[q];
+        for (int q = 0; q < C::PPT; ++q) *reinterpret_cast<uint4*>(smem + stage * C::STAGE + xdst[q]) = xr[q];
     };
 
     load_x(0);
 #pragma unroll
     for (int nbk = 0; nbk < NBLK; ++nbk)
 #pragma unroll
-        for (int u = 0; u < 4; ++u) w[nbk][u] = ld16(wrow[nbk] + 16 * u);
+        for (int u = 0; u < 4; ++u) w[nbk][u] = ld16(wrow[nbk] + WU * u);
     store_x(0);
     __syncthreads();
     for (int c = 0; c < NCH; ++c) {
         const bool more = c + 1 < NCH;
         if (more) load_x(c + 1);
-        const unsigned char* st = smem + (c & 1) * C::STAGE + l32 * kRowPad + 64 * h;
+        const unsigned char* st = smem + (c & 1) * C::STAGE + boff;
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
             uint4 bx[TBW];
@@ -197,7 +225,7 @@ __global__ __launch_bounds__(WAVES * 64) void router_score_select_kernel(RouterA
                 for (int nbk = 0; nbk < NBLK; ++nbk) acc[tb][nbk] = mfma_unit<F32>(w[nbk][u], bx[tb], acc[tb][nbk]);
             if (more) {
 #pragma unroll
-                for (int nbk = 0; nbk < NBLK; ++nbk) w[nbk][u] = ld16(wrow[nbk] + (c + 1) * 128 + 16 * u);
+                for (int nbk = 0; nbk < NBLK; ++nbk) w[nbk][u] = ld16(wrow[nbk] + (c + 1) * WCH + WU * u);
             }
         }
         if (more) store_x((c + 1) & 1);
@@ -208,41 +236,43 @@ __global__ __launch_bounds__(WAVES * 64) void router_score_select_kernel(RouterA
     float* gm = reinterpret_cast<float*>(smem + C::OFF_GM);
     float* tau_s = reinterpret_cast<float*>(smem + C::OFF_TAU);
     int* cnt = reinterpret_cast<int*>(smem + C::OFF_CNT);
-    float* pvs = reinterpret_cast<float*>(smem + C::OFF_PV);
-    int* pis = reinterpret_cast<int*>(smem + C::OFF_PI);
     float* lv = reinterpret_cast<float*>(smem + C::OFF_LV);
     float* ls = reinterpret_cast<float*>(smem + C::OFF_LS);
     int* li = reinterpret_cast<int*>(smem + C::OFF_LI);
     float* sv = reinterpret_cast<float*>(smem + C::OFF_SV);
     float* ss = reinterpret_cast<float*>(smem + C::OFF_SS);
     int* si = reinterpret_cast<int*>(smem + C::OFF_SI);
-    float* rv = reinterpret_cast<float*>(smem + C::OFF_RV);
-    float* rs = reinterpret_cast<float*>(smem + C::OFF_RS);
-    int* ri = reinterpret_cast<int*>(smem + C::OFF_RI);
+    unsigned* ovf = reinterpret_cast<unsigned*>(smem + C::OFF_OVF);
+    float* rowv = reinterpret_cast<float*>(smem + C::OFF_ROWV);
+    float* rows = reinterpret_cast<float*>(smem + C::OFF_ROWS);
     int* hist = reinterpret_cast<int*>(smem + C::OFF_HIST);
-    int* flag = reinterpret_cast<int*>(smem + C::OFF_FLAG);
-    float* bias_s = reinterpret_cast<float*>(smem + C::OFF_BIAS);
 
     // Expert of accumulator (nbk, r): ebase + 32 nbk + 8 (r/4) + (r%4).  E is a
     // multiple of 32, so a whole 32-expert block is either real or padding.
     const int ebase = e_wave0 + 4 * h;
     auto blk_real = [&](int nbk) { return e_wave0 + nbk * 32 < E; };
-    // The slice's bias, staged once; lane reads 4 consecutive experts at a time.
-    for (int j = tid; j < C::BE; j += C::NT) {
-        const int e = slice * C::BE + j;
-        bias_s[j] = e < E ? a.bias[e] : 0.0f;
-    }
-    for (int e = tid; e < 1024; e += C::NT) hist[e] = 0;
-    if (tid == 0) flag[0] = 0;
-    auto bias4 = [&](int nbk, int r4) {
-        return *reinterpret_cast<const float4*>(bias_s + wave * C::WE + nbk * 32 + 8 * r4 + 4 * h);
-    };
-    auto comp = [](const float4& f, int i) { return i == 0 ? f.x : (i == 1 ? f.y : (i == 2 ? f.z : f.w)); };
+    const int slot = wave * 2 + h;  // this lane's position among the token's lanes
 
-    // 1. scores s = sigmoid(z).  The accumulators keep z; every step below
-    // recomputes s from it with the same instructions, so the values the
-    // selection compares and the optional debug dump are identical.
-    auto score = [&](int tb, int nbk, int r) { return sigmoid_fast(acc[tb][nbk][r]); };
+    // this lane's bias values, four consecutive experts per (nbk, r/4)
+    float4 b4[NBLK][4];
+#pragma unroll
+    for (int nbk = 0; nbk < NBLK; ++nbk)
+#pragma unroll
+        for (int r4 = 0; r4 < 4; ++r4) {
+            const int e = ebase + nbk * 32 + 8 * r4;
+            b4[nbk][r4] = blk_real(nbk) ? make_float4(a.bias[e], a.bias[e + 1], a.bias[e + 2], a.bias[e + 3])
+                                        : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+    for (int e = tid; e < 1024; e += C::NT) hist[e] = 0;
+    if (tid < 16) ovf[tid] = 0;
+
+    // 1. scores, once (and the optional debug dump of exactly these values)
+#pragma unroll
+    for (int tb = 0; tb < TBW; ++tb)
+#pragma unroll
+        for (int nbk = 0; nbk < NBLK; ++nbk)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[tb][nbk][r] = sigmoid_fast(acc[tb][nbk][r]);
     if (a.dump) {
 #pragma unroll
         for (int tb = 0; tb < TBW; ++tb) {
@@ -254,39 +284,30 @@ __global__ __launch_bounds__(WAVES * 64) void router_score_select_kernel(RouterA
 #pragma unroll
                         for (int r4 = 0; r4 < 4; ++r4)
                             *reinterpret_cast<float4*>(a.dump + tok * E + ebase + nbk * 32 + 8 * r4) =
-                                make_float4(score(tb, nbk, 4 * r4), score(tb, nbk, 4 * r4 + 1),
-                                            score(tb, nbk, 4 * r4 + 2), score(tb, nbk, 4 * r4 + 3));
+                                make_float4(acc[tb][nbk][4 * r4], acc[tb][nbk][4 * r4 + 1], acc[tb][nbk][4 * r4 + 2],
+                                            acc[tb][nbk][4 * r4 + 3]);
                     }
             }
         }
     }
-    __syncthreads();
 
     // 2. group maxima of v = s + b
-    {
-        float gmx[TBW][C::G];
 #pragma unroll
-        for (int tb = 0; tb < TBW; ++tb)
+    for (int tb = 0; tb < TBW; ++tb) {
+        float gmx[C::G];
 #pragma unroll
-            for (int g = 0; g < C::G; ++g) gmx[tb][g] = -INFINITY;
+        for (int g = 0; g < C::G; ++g) gmx[g] = -INFINITY;
 #pragma unroll
         for (int nbk = 0; nbk < NBLK; ++nbk) {
             if (!blk_real(nbk)) continue;
-            float4 b4[4];
 #pragma unroll
-            for (int r4 = 0; r4 < 4; ++r4) b4[r4] = bias4(nbk, r4);
-#pragma unroll
-            for (int tb = 0; tb < TBW; ++tb)
-#pragma unroll
-                for (int r = 0; r < 16; ++r) {
-                    const int g = (nbk * 16 + r) / C::GS;
-                    gmx[tb][g] = fmaxf(gmx[tb][g], score(tb, nbk, r) + comp(b4[r >> 2], r & 3));
-                }
+            for (int r = 0; r < 16; ++r) {
+                const int g = (nbk * 16 + r) / C::GS;
+                gmx[g] = fmaxf(gmx[g], acc[tb][nbk][r] + comp4(b4[nbk][r >> 2], r & 3));
+            }
         }
 #pragma unroll
-        for (int tb = 0; tb < TBW; ++tb)
-#pragma unroll
-            for (int g = 0; g < C::G; ++g) gm[(tb * 32 + l32) * 16 + (wave * 2 + h) * C::G + g] = gmx[tb][g];
+        for (int g = 0; g < C::G; ++g) gm[(tb * 32 + l32) * C::GMS + slot * C::G + g] = gmx[g];
     }
     __syncthreads();
 
@@ -294,7 +315,7 @@ __global__ __launch_bounds__(WAVES * 64) void router_score_select_kernel(RouterA
     if (tid < C::BT) {
         float g16[16];
 #pragma unroll
-        for (int i = 0; i < 16; ++i) g16[i] = gm[tid * 16 + i];
+        for (int i = 0; i < 16; ++i) g16[i] = gm[tid * C::GMS + i];
         sort16_ascending(g16);
         float tau = -INFINITY;
         if (K <= 16) {
@@ -303,128 +324,165 @@ __global__ __launch_bounds__(WAVES * 64) void router_score_select_kernel(RouterA
                 if (i == 16 - K) tau = g16[i];
         }
         tau_s[tid] = tau;
-        cnt[tid] = 0;
     }
     __syncthreads();
 
-    // 4. candidates v >= tau
-    {
-        float taus[TBW];
-        bool live[TBW];
+    // 4. candidates v >= tau: count, prefix over the token's lanes, write
+    float taus[TBW];
 #pragma unroll
-        for (int tb = 0; tb < TBW; ++tb) {
-            taus[tb] = tau_s[tb * 32 + l32];
-            live[tb] = tok0 + tb * 32 + l32 < T;
-        }
+    for (int tb = 0; tb < TBW; ++tb) {
+        const int tl = tb * 32 + l32;
+        taus[tb] = tau_s[tl];
+        int n = 0;
 #pragma unroll
         for (int nbk = 0; nbk < NBLK; ++nbk) {
             if (!blk_real(nbk)) continue;
-            float4 b4[4];
 #pragma unroll
-            for (int r4 = 0; r4 < 4; ++r4) b4[r4] = bias4(nbk, r4);
+            for (int r = 0; r < 16; ++r) n += (acc[tb][nbk][r] + comp4(b4[nbk][r >> 2], r & 3) >= taus[tb]) ? 1 : 0;
+        }
+        cnt[tl * C::CNS + slot] = n;
+    }
+    __syncthreads();
 #pragma unroll
-            for (int tb = 0; tb < TBW; ++tb) {
-                const int tl = tb * 32 + l32;
+    for (int tb = 0; tb < TBW; ++tb) {
+        const int tl = tb * 32 + l32;
+        int off = 0, total = 0;
 #pragma unroll
-                for (int r = 0; r < 16; ++r) {
-                    const float s = score(tb, nbk, r);
-                    const float v = s + comp(b4[r >> 2], r & 3);
-                    if (live[tb] && v >= taus[tb]) {
-                        const int p = atomicAdd(&cnt[tl], 1);
-                        if (p < kCap) {
-                            lv[tl * kCap + p] = v;
-                            ls[tl * kCap + p] = s;
-                            li[tl * kCap + p] = ebase + nbk * 32 + 8 * (r >> 2) + (r & 3);
-                        }
-                    }
+        for (int o = 0; o < C::NLANES; ++o) {
+            const int n = cnt[tl * C::CNS + o];
+            off += (o < slot) ? n : 0;
+            total += n;
+        }
+        if (total > kCap) {
+            if (slot == 0) atomicOr(&ovf[tl >> 5], 1u << (tl & 31));
+            continue;
+        }
+        if (tok0 + tl >= T) continue;
+        const float tau = taus[tb];
+#pragma unroll
+        for (int nbk = 0; nbk < NBLK; ++nbk) {
+            if (!blk_real(nbk)) continue;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const float s = acc[tb][nbk][r];
+                const float v = s + comp4(b4[nbk][r >> 2], r & 3);
+                if (v >= tau) {
+                    lv[tl * C::LST + off] = v;
+                    ls[tl * C::LST + off] = s;
+                    li[tl * C::LST + off] = ebase + nbk * 32 + 8 * (r >> 2) + (r & 3);
+                    ++off;
                 }
             }
         }
     }
     __syncthreads();
 
-    // 5. rank the candidates of every token whose list did not overflow
+    // 5. rank the candidates of every token whose list did not overflow.  The
+    // token's threads hold its whole list in registers (entries past n read
+    // as (-inf, INT_MAX), which rank below everything) and count, for each of
+    // their candidates, the entries that rank above it.
     {
         const int tl = tid / C::TPT, q = tid % C::TPT;
-        const int n = cnt[tl];
-        if (n > kCap) {
-            flag[0] = 1;
-        } else {
+        int n = 0;
+#pragma unroll
+        for (int o = 0; o < C::NLANES; ++o) n += cnt[tl * C::CNS + o];
+        if (n <= kCap) {
+            float cv[kCap];
+            int ci[kCap];
+#pragma unroll
+            for (int o4 = 0; o4 < kCap / 4; ++o4) {
+                const float4 v4 = *reinterpret_cast<const float4*>(lv + tl * C::LST + 4 * o4);
+                const int4 i4 = *reinterpret_cast<const int4*>(li + tl * C::LST + 4 * o4);
+                cv[4 * o4] = v4.x; cv[4 * o4 + 1] = v4.y; cv[4 * o4 + 2] = v4.z; cv[4 * o4 + 3] = v4.w;
+                ci[4 * o4] = i4.x; ci[4 * o4 + 1] = i4.y; ci[4 * o4 + 2] = i4.z; ci[4 * o4 + 3] = i4.w;
+            }
+#pragma unroll
+            for (int o = 0; o < kCap; ++o)
+                if (o >= n) {
+                    cv[o] = -INFINITY;
+                    ci[o] = 0x7fffffff;
+                }
             for (int c = q; c < n; c += C::TPT) {
-                const float vc = lv[tl * kCap + c];
-                const int ic = li[tl * kCap + c];
+                const float vc = lv[tl * C::LST + c];
+                const int ic = li[tl * C::LST + c];
                 int rank = 0;
-                for (int o = 0; o < n; ++o) rank += ranks_above(lv[tl * kCap + o], li[tl * kCap + o], vc, ic) ? 1 : 0;
+#pragma unroll
+                for (int o = 0; o < kCap; ++o) rank += ranks_above(cv[o], ci[o], vc, ic) ? 1 : 0;
                 if (rank < K) {
-                    sv[tl * kMaxK + rank] = vc;
-                    ss[tl * kMaxK + rank] = ls[tl * kCap + c];
-                    si[tl * kMaxK + rank] = ic;
+                    sv[tl * C::LST + rank] = vc;
+                    ss[tl * C::LST + rank] = ls[tl * C::LST + c];
+                    si[tl * C::LST + rank] = ic;
                 }
             }
+        }
+    }
+
+    // 6. overflowing tokens, one at a time: gather the token's slice into an
+    // LDS row, then wave 0 takes K rounds of wave-wide argmax over it.
+    for (int word = 0; word < C::BT / 32; ++word) {
+        unsigned bits = ovf[word];  // uniform: written before the last barrier
+        while (bits) {
+            const int tl = word * 32 + __builtin_ctz(bits);
+            bits &= bits - 1;
+            const int tb = tl >> 5;
+            if ((tl & 31) == l32) {
+#pragma unroll
+                for (int tbb = 0; tbb < TBW; ++tbb) {
+                    if (tbb != tb) continue;
+#pragma unroll
+                    for (int nbk = 0; nbk < NBLK; ++nbk)
+#pragma unroll
+                        for (int r = 0; r < 16; ++r) {
+                            const int p = wave * C::WE + nbk * 32 + 8 * (r >> 2) + 4 * h + (r & 3);
+                            const float s = acc[tbb][nbk][r];
+                            rows[p] = s;
+                            rowv[p] = blk_real(nbk) ? s + comp4(b4[nbk][r >> 2], r & 3) : -INFINITY;
+                        }
+                }
+            }
+            __syncthreads();
+            if (wave == 0) {
+                unsigned taken = 0;
+                for (int r = 0; r < K; ++r) {
+                    float bv = -INFINITY, bs = 0.0f;
+                    int bi = 0x7fffffff, bq = -1;
+#pragma unroll
+                    for (int q = 0; q < C::BE / 64; ++q) {
+                        const int p = lane + 64 * q;
+                        const float v = rowv[p];
+                        const int e = slice * C::BE + p;
+                        if (!((taken >> q) & 1u) && v != -INFINITY && ranks_above(v, e, bv, bi)) {
+                            bv = v;
+                            bs = rows[p];
+                            bi = e;
+                            bq = q;
+                        }
+                    }
+                    float wv = bv, ws = bs;
+                    int wi = bi;
+#pragma unroll
+                    for (int off = 32; off >= 1; off >>= 1) {
+                        const float ov = __shfl_xor(wv, off);
+                        const float os = __shfl_xor(ws, off);
+                        const int oi = __shfl_xor(wi, off);
+                        if (ranks_above(ov, oi, wv, wi)) {
+                            wv = ov;
+                            ws = os;
+                            wi = oi;
+                        }
+                    }
+                    if (bi == wi && bq >= 0) taken |= 1u << bq;
+                    if (lane == 0) {
+                        sv[tl * C::LST + r] = wv;
+                        ss[tl * C::LST + r] = ws;
+                        si[tl * C::LST + r] = wi;
+                    }
+                }
+            }
+            __syncthreads();
         }
     }
     __syncthreads();
-
-    // 6. exact fallback for overflowing tokens: K rounds of "best value
-    // strictly below the previous pick", reduced over the token's lanes.
-    if (flag[0]) {
-        if (tid < C::BT) {
-            pvs[tid] = INFINITY;
-            pis[tid] = -1;
-        }
-        __syncthreads();
-        for (int r = 0; r < K; ++r) {
-#pragma unroll
-            for (int tb = 0; tb < TBW; ++tb) {
-                const int tl = tb * 32 + l32;
-                if (cnt[tl] > kCap) {
-                    const float pv = pvs[tl];
-                    const int pi = pis[tl];
-                    float bv = -INFINITY, bs = 0.0f;
-                    int bi = 0x7fffffff;
-#pragma unroll
-                    for (int nbk = 0; nbk < NBLK; ++nbk) {
-                        if (!blk_real(nbk)) continue;
-#pragma unroll
-                        for (int rr = 0; rr < 16; ++rr) {
-                            const float s = score(tb, nbk, rr);
-                            const float v = s + bias_s[wave * C::WE + nbk * 32 + 8 * (rr >> 2) + 4 * h + (rr & 3)];
-                            const int e = ebase + nbk * 32 + 8 * (rr >> 2) + (rr & 3);
-                            const bool below = (pi < 0) || ranks_above(pv, pi, v, e);
-                            if (below && ranks_above(v, e, bv, bi)) {
-                                bv = v;
-                                bs = s;
-                                bi = e;
-                            }
-                        }
-                    }
-                    const int o = tl * C::NLANES + wave * 2 + h;
-                    rv[o] = bv;
-                    rs[o] = bs;
-                    ri[o] = bi;
-                }
-            }
-            __syncthreads();
-            if (tid < C::BT && cnt[tid] > kCap) {
-                float bv = -INFINITY, bs = 0.0f;
-                int bi = 0x7fffffff;
-                for (int o = 0; o < C::NLANES; ++o) {
-                    const int k = tid * C::NLANES + o;
-                    if (ranks_above(rv[k], ri[k], bv, bi)) {
-                        bv = rv[k];
-                        bs = rs[k];
-                        bi = ri[k];
-                    }
-                }
-                sv[tid * kMaxK + r] = bv;
-                ss[tid * kMaxK + r] = bs;
-                si[tid * kMaxK + r] = bi;
-                pvs[tid] = bv;
-                pis[tid] = bi;
-            }
-            __syncthreads();
-        }
-    }
 
     // 7. outputs
     {
@@ -434,15 +492,21 @@ __global__ __launch_bounds__(WAVES * 64) void router_score_select_kernel(RouterA
             if (NS > 1) {
                 const int64_t base = (tok * NS + slice) * K;
                 for (int r = q; r < K; r += C::TPT) {
-                    a.cand_v[base + r] = sv[tl * kMaxK + r];
-                    a.cand_s[base + r] = ss[tl * kMaxK + r];
-                    a.cand_i[base + r] = si[tl * kMaxK + r];
+                    a.cand_v[base + r] = sv[tl * C::LST + r];
+                    a.cand_s[base + r] = ss[tl * C::LST + r];
+                    a.cand_i[base + r] = si[tl * C::LST + r];
                 }
             } else {
+                // gate weights: den is the fp32 sum of the selected unbiased
+                // scores in rank order
+                float den = 0.0f;
+#pragma unroll
+                for (int r = 0; r < kMaxK; ++r)
+                    if (r < K) den = den + ss[tl * C::LST + r];
                 for (int r = q; r < K; r += C::TPT) {
-                    const int e = si[tl * kMaxK + r];
+                    const int e = si[tl * C::LST + r];
                     a.idx[tok * K + r] = e;
-                    a.w[tok * K + r] = gate_weight(ss + tl * kMaxK, K, r);
+                    a.w[tok * K + r] = (den == 0.0f) ? 1.0f / (float)K : ss[tl * C::LST + r] / den;
                     if ((unsigned)e < (unsigned)E) atomicAdd(&hist[e], 1);
                 }
             }
@@ -456,69 +520,112 @@ __global__ __launch_bounds__(WAVES * 64) void router_score_select_kernel(RouterA
 }
 
 // Merge the slices' rank-ordered candidate lists into the final Top-K, compute
-// the gate weights and count the assignments.  One thread per token.
+// the gate weights and count the assignments.  The workgroup copies its
+// tokens' candidates into LDS with coalesced loads, then each thread merges
+// one token.
 constexpr int kMergeThreads = 256;
 
-__global__ __launch_bounds__(kMergeThreads) void router_merge_kernel(RouterArgs a, int NS) {
-    __shared__ int hist[1024];
-    const int tid = threadIdx.x;
+__global__ __launch_bounds__(kMergeThreads) void router_merge_kernel(RouterArgs a, int NS, int tokens_per_wg) {
+    extern __shared__ __attribute__((aligned(16))) unsigned char dyn[];
+    int* hist = reinterpret_cast<int*>(dyn);
     const int E = a.E, K = a.K;
+    const int per_tok = NS * K;
+    float* cv = reinterpret_cast<float*>(dyn + 4096);
+    float* cs = cv + tokens_per_wg * per_tok;
+    int* ci = reinterpret_cast<int*>(cs + tokens_per_wg * per_tok);
+    const int tid = threadIdx.x;
     for (int e = tid; e < E; e += kMergeThreads) hist[e] = 0;
-    __syncthreads();
-    for (int64_t tok = (int64_t)blockIdx.x * kMergeThreads + tid; tok < a.T;
-         tok += (int64_t)gridDim.x * kMergeThreads) {
-        const int64_t base = tok * NS * K;
-        int head[kMaxSlices];
+    for (int64_t tok_base = (int64_t)blockIdx.x * tokens_per_wg; tok_base < a.T;
+         tok_base += (int64_t)gridDim.x * tokens_per_wg) {
+        const int ntok = (int)((a.T - tok_base) < tokens_per_wg ? (a.T - tok_base) : tokens_per_wg);
+        const int64_t g0 = tok_base * per_tok;
+        __syncthreads();
+        for (int i = tid; i < ntok * per_tok; i += kMergeThreads) {
+            cv[i] = a.cand_v[g0 + i];
+            cs[i] = a.cand_s[g0 + i];
+            ci[i] = a.cand_i[g0 + i];
+        }
+        __syncthreads();
+        for (int t = tid; t < ntok; t += kMergeThreads) {
+            const int base = t * per_tok;
+            int head[kMaxSlices];
 #pragma unroll
-        for (int s = 0; s < kMaxSlices; ++s) head[s] = 0;
-        float sel_s[kMaxK];
+            for (int s = 0; s < kMaxSlices; ++s) head[s] = 0;
+            float sel_s[kMaxK];
+            const int64_t tok = tok_base + t;
 #pragma unroll
-        for (int r = 0; r < kMaxK; ++r) {
-            if (r < K) {
-                float bv = -INFINITY, bs = 0.0f;
-                int bi = 0x7fffffff, bsl = 0;
+            for (int r = 0; r < kMaxK; ++r) {
+                if (r < K) {
+                    float bv = -INFINITY, bs = 0.0f;
+                    int bi = 0x7fffffff, bsl = 0;
 #pragma unroll
-                for (int s = 0; s < kMaxSlices; ++s) {
-                    if (s < NS && head[s] < K) {
-                        const int64_t o = base + (int64_t)s * K + head[s];
-                        const float v = a.cand_v[o];
-                        const int i = a.cand_i[o];
-                        if (ranks_above(v, i, bv, bi)) {
-                            bv = v;
-                            bi = i;
-                            bs = a.cand_s[o];
-                            bsl = s;
+                    for (int s = 0; s < kMaxSlices; ++s) {
+                        if (s < NS && head[s] < K) {
+                            const int o = base + s * K + head[s];
+                            if (ranks_above(cv[o], ci[o], bv, bi)) {
+                                bv = cv[o];
+                                bi = ci[o];
+                                bs = cs[o];
+                                bsl = s;
+                            }
                         }
                     }
+#pragma unroll
+                    for (int s = 0; s < kMaxSlices; ++s) head[s] += (s == bsl) ? 1 : 0;
+                    sel_s[r] = bs;
+                    a.idx[tok * K + r] = bi;
+                    if ((unsigned)bi < (unsigned)E) atomicAdd(&hist[bi], 1);
                 }
-#pragma unroll
-                for (int s = 0; s < kMaxSlices; ++s) head[s] += (s == bsl) ? 1 : 0;
-                sel_s[r] = bs;
-                a.idx[tok * K + r] = bi;
-                if ((unsigned)bi < (unsigned)E) atomicAdd(&hist[bi], 1);
             }
+            float den = 0.0f;
+#pragma unroll
+            for (int r = 0; r < kMaxK; ++r)
+                if (r < K) den = den + sel_s[r];
+#pragma unroll
+            for (int r = 0; r < kMaxK; ++r)
+                if (r < K) a.w[tok * K + r] = (den == 0.0f) ? 1.0f / (float)K : sel_s[r] / den;
         }
-        float den = 0.0f;
-#pragma unroll
-        for (int r = 0; r < kMaxK; ++r)
-            if (r < K) den = den + sel_s[r];
-#pragma unroll
-        for (int r = 0; r < kMaxK; ++r)
-            if (r < K) a.w[tok * K + r] = (den == 0.0f) ? 1.0f / (float)K : sel_s[r] / den;
     }
     __syncthreads();
     for (int e = tid; e < E; e += kMergeThreads)
         if (hist[e] != 0) atomicAdd(&a.counts[e], hist[e]);
 }
 
-template <bool F32, int WAVES, int TBW, int NBLK>
+// Router matrix [E][d] -> packed layout: for 32-expert block b, chunk c
+// (128 bytes of each row), unit u (16 bytes), lane l = 32h + m, the 16 bytes
+// at ((b*NCH + c)*4 + u)*1024 + 16 l are row 32b + m, bytes c*128 + 64h + 16u.
+__global__ void pack_weight_kernel(const char* __restrict__ W, char* __restrict__ P, int64_t RB, int64_t pieces) {
+    const int64_t nch = RB / 128;
+    for (int64_t o = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; o < pieces;
+         o += (int64_t)gridDim.x * blockDim.x) {
+        const int l = (int)(o & 63), u = (int)((o >> 6) & 3);
+        const int64_t c = (o >> 8) % nch, b = (o >> 8) / nch;
+        const int m = l & 31, hh = l >> 5;
+        const int64_t src = (b * 32 + m) * RB + c * 128 + 64 * hh + 16 * u;
+        *reinterpret_cast<uint4*>(P + o * 16) = *reinterpret_cast<const uint4*>(W + src);
+    }
+}
+
+template <bool F32, bool PACKED, int WAVES, int TBW, int NBLK>
 hipError_t launch_tiling(const RouterArgs& a, int NS, hipStream_t stream) {
     using C = Cfg<F32, WAVES, TBW, NBLK>;
     const int64_t tiles = (a.T + C::BT - 1) / C::BT;
     const int64_t blocks = tiles * NS;
-    hipLaunchKernelGGL((router_score_select_kernel<F32, WAVES, TBW, NBLK>), dim3((unsigned)blocks), dim3(C::NT), 0,
-                       stream, a, NS);
+    hipLaunchKernelGGL((router_score_select_kernel<F32, PACKED, WAVES, TBW, NBLK>), dim3((unsigned)blocks),
+                       dim3(C::NT), 0, stream, a, NS);
     return hipGetLastError();
+}
+
+template <bool PACKED>
+hipError_t launch_layout(const RouterTiling& t, const RouterArgs& a, int NS, hipStream_t stream) {
+    switch (t.id) {
+        case 1: return launch_tiling<false, PACKED, 4, 4, 3>(a, NS, stream);
+        case 2: return launch_tiling<false, PACKED, 8, 2, 3>(a, NS, stream);
+        case 3: return launch_tiling<false, PACKED, 4, 4, 2>(a, NS, stream);
+        case 4: return launch_tiling<false, PACKED, 4, 4, 1>(a, NS, stream);
+        case 5: return launch_tiling<true, PACKED, 4, 4, 1>(a, NS, stream);
+        default: return hipErrorInvalidValue;
+    }
 }
 
 const RouterTiling kTilings[] = {
@@ -536,22 +643,29 @@ RouterTiling router_tiling(int i) { return kTilings[i]; }
 
 hipError_t launch_router_score_select(const RouterTiling& t, const RouterArgs& a, hipStream_t stream) {
     const int NS = router_slices(t, a.E);
-    switch (t.id) {
-        case 1: return launch_tiling<false, 4, 4, 3>(a, NS, stream);
-        case 2: return launch_tiling<false, 8, 2, 3>(a, NS, stream);
-        case 3: return launch_tiling<false, 4, 4, 2>(a, NS, stream);
-        case 4: return launch_tiling<false, 4, 4, 1>(a, NS, stream);
-        case 5: return launch_tiling<true, 4, 4, 1>(a, NS, stream);
-        default: return hipErrorInvalidValue;
-    }
+    return a.w_packed ? launch_layout<true>(t, a, NS, stream) : launch_layout<false>(t, a, NS, stream);
 }
 
 hipError_t launch_router_merge(const RouterTiling& t, const RouterArgs& a, hipStream_t stream) {
     const int NS = router_slices(t, a.E);
     if (NS <= 1) return hipSuccess;
-    int64_t blocks = (a.T + kMergeThreads - 1) / kMergeThreads;
-    if (blocks > 64) blocks = 64;
-    hipLaunchKernelGGL(router_merge_kernel, dim3((unsigned)blocks), dim3(kMergeThreads), 0, stream, a, NS);
+    const int per_tok_bytes = NS * a.K * 12;
+    int tpw = 49152 / per_tok_bytes;
+    tpw = tpw > 256 ? 256 : tpw;
+    tpw = tpw < 1 ? 1 : tpw;
+    int64_t blocks = (a.T + tpw - 1) / tpw;
+    if (blocks > 1024) blocks = 1024;
+    const size_t lds = 4096 + (size_t)tpw * per_tok_bytes;
+    hipLaunchKernelGGL(router_merge_kernel, dim3((unsigned)blocks), dim3(kMergeThreads), lds, stream, a, NS, tpw);
+    return hipGetLastError();
+}
+
+hipError_t launch_pack_weight(const void* W, void* P, int E, int64_t row_bytes, hipStream_t stream) {
+    const int64_t pieces = (int64_t)E * row_bytes / 16;
+    int64_t blocks = (pieces + 255) / 256;
+    if (blocks > 4096) blocks = 4096;
+    hipLaunchKernelGGL(pack_weight_kernel, dim3((unsigned)blocks), dim3(256), 0, stream,
+                       reinterpret_cast<const char*>(W), reinterpret_cast<char*>(P), row_bytes, pieces);
     return hipGetLastError();
 }
 

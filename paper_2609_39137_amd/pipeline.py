@@ -28,14 +28,29 @@ class RouterStep:
         nbytes = B.idb_router_workspace_bytes(T, d, E, K, code, variant)
         self.workspace = torch.empty(max(nbytes, 16), dtype=torch.uint8, device=device)
         self.info = B.idb_router_variant_info(T, d, E, K, code, variant)
+        self.W_packed = None
 
-    def route(self, x, W, accumulate: bool = False, scores_dump=None, stream=None):
-        B.idb_router_forward(x, W, self.state.bias, self.K, self.idx, self.w, self.counts, accumulate, scores_dump,
-                             self.workspace, self.variant, stream)
+    def pack(self, W, stream=None):
+        """Pack the router matrix once per weight update; later calls read the packed copy."""
+        self.W_packed = torch.empty_like(W)
+        B.idb_router_pack_weight(W, self.W_packed, stream)
+        return self.W_packed
 
-    def score_select(self, x, W, accumulate: bool = False, scores_dump=None, stream=None):
-        B.idb_router_score_select(x, W, self.state.bias, self.K, self.idx, self.w, self.counts, accumulate,
-                                  scores_dump, self.workspace, self.variant, stream)
+    def _weights(self, W):
+        if W is None:
+            return self.W_packed, B.IDB_WEIGHT_PACKED
+        return W, B.IDB_WEIGHT_ROW_MAJOR
+
+    def route(self, x, W=None, accumulate: bool = False, scores_dump=None, stream=None):
+        """Route with row-major ``W``, or with the packed copy from :meth:`pack` when ``W`` is None."""
+        Wt, layout = self._weights(W)
+        B.idb_router_forward(x, Wt, self.state.bias, self.K, self.idx, self.w, self.counts, accumulate, scores_dump,
+                             self.workspace, self.variant, stream, layout)
+
+    def score_select(self, x, W=None, accumulate: bool = False, scores_dump=None, stream=None):
+        Wt, layout = self._weights(W)
+        B.idb_router_score_select(x, Wt, self.state.bias, self.K, self.idx, self.w, self.counts, accumulate,
+                                  scores_dump, self.workspace, self.variant, stream, layout)
 
     def merge(self, stream=None):
         B.idb_router_merge(self.T, self.d, self.E, self.K, self.dtype_code, self.idx, self.w, self.counts,
@@ -47,7 +62,7 @@ class RouterStep:
     def load_stats(self, stream=None):
         B.idb_load_stats(self.counts, self.stats, stream)
 
-    def step(self, x, W, stream=None):
+    def step(self, x, W=None, stream=None):
         """Route, update the bias, compute MaxVio/MinVio (all asynchronous)."""
         self.route(x, W, stream=stream)
         self.update(stream)

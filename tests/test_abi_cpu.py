@@ -29,8 +29,9 @@ def test_library_exports_every_header_function():
 
 
 def router(T=128, d=256, E=768, K=10, dtype=B.IDB_DTYPE_BF16, x=A16, W=A16, bias=A16, idx=A16, w=A16, counts=A16,
-           dump=None, ws=A16, ws_bytes=1 << 30, variant=0, fn="idb_router_forward"):
-    return getattr(B.lib(), fn)(x, W, dtype, bias, T, d, E, K, idx, w, counts, 0, dump, ws, ws_bytes, variant, None)
+           dump=None, ws=A16, ws_bytes=1 << 30, variant=0, fn="idb_router_forward", layout=0):
+    return getattr(B.lib(), fn)(x, W, dtype, layout, bias, T, d, E, K, idx, w, counts, 0, dump, ws, ws_bytes, variant,
+                                None)
 
 
 @pytest.mark.parametrize("fn", ["idb_router_forward", "idb_router_score_select"])
@@ -54,6 +55,7 @@ def router(T=128, d=256, E=768, K=10, dtype=B.IDB_DTYPE_BF16, x=A16, W=A16, bias
     (dict(ws=None), B.IDB_ERR_INVALID_ARG),
     (dict(ws_bytes=16), B.IDB_ERR_INVALID_ARG),
     (dict(variant=99), B.IDB_ERR_INVALID_ARG),
+    (dict(layout=2), B.IDB_ERR_INVALID_ARG),
     (dict(variant=5), B.IDB_ERR_UNSUPPORTED),   # the fp32 tiling asked for bf16 input
     (dict(E=2048), B.IDB_ERR_UNSUPPORTED),
     (dict(E=100, K=4), B.IDB_ERR_UNSUPPORTED),
@@ -64,6 +66,19 @@ def router(T=128, d=256, E=768, K=10, dtype=B.IDB_DTYPE_BF16, x=A16, W=A16, bias
 def test_router_rejects_invalid_arguments(fn, kw, code):
     assert router(fn=fn, **kw) == code
     assert B.idb_last_error() != ""
+
+
+def test_pack_weight_rejects_invalid_arguments():
+    L = B.lib()
+    assert L.idb_router_pack_weight(None, 0, 768, 2048, A16, None) == B.IDB_ERR_INVALID_ARG
+    assert L.idb_router_pack_weight(A16, 0, 768, 2048, None, None) == B.IDB_ERR_INVALID_ARG
+    assert L.idb_router_pack_weight(A16, 0, 768, 2048, A16 + 4096, None) == B.IDB_ERR_INVALID_ARG  # overlap
+    assert L.idb_router_pack_weight(A16 + 8, 0, 768, 2048, A16 + (1 << 26), None) == B.IDB_ERR_INVALID_ARG
+    assert L.idb_router_pack_weight(A16, 0, 100, 2048, A16 + (1 << 26), None) == B.IDB_ERR_UNSUPPORTED
+    assert L.idb_router_pack_weight(A16, 0, 768, 96, A16 + (1 << 26), None) == B.IDB_ERR_UNSUPPORTED
+    assert B.idb_router_packed_weight_bytes(768, 2048, B.IDB_DTYPE_BF16) == 768 * 2048 * 2
+    assert B.idb_router_packed_weight_bytes(64, 256, B.IDB_DTYPE_F32) == 64 * 256 * 4
+    assert B.idb_router_packed_weight_bytes(100, 256, B.IDB_DTYPE_F32) == 0
 
 
 def test_merge_rejects_invalid_arguments():

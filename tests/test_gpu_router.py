@@ -236,3 +236,36 @@ def test_workload_full_size_sampled_rows(name):
         si, sw, sc = gpu_select(s, b, wl.K)
         np.testing.assert_array_equal(idx, si)
         np.testing.assert_array_equal(c, sc)
+
+
+@pytest.mark.parametrize("T,d,E,K,dtype,variant", [
+    (517, 512, 768, 10, "bf16", 1), (517, 512, 768, 10, "bf16", 2), (300, 256, 768, 5, "bf16", 3),
+    (129, 128, 800, 10, "bf16", 4), (1000, 256, 64, 4, "f32", 5), (64, 2048, 256, 8, "bf16", 0),
+])
+def test_packed_weight_layout_is_bit_identical(T, d, E, K, dtype, variant):
+    x, W = synth.normal_router_inputs(T, d, E, seed=11, dtype=dtype, w_std=0.05)
+    b = synth.bias(E, "small", seed=12)
+    ref = run_router(x, W, b, K, variant=variant)
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    rs = RouterStep(T, d, E, K, tdt, variant=variant)
+    rs.state.bias.copy_(torch.from_numpy(b))
+    Wp = rs.pack(to_dev(W))
+    assert not torch.equal(Wp.view(-1), to_dev(W).view(-1)) or E * d <= 64 * 32
+    dump = torch.empty((T, E), dtype=torch.float32, device=DEV)
+    rs.route(to_dev(x), None, scores_dump=dump)
+    np.testing.assert_array_equal(rs.idx.cpu().numpy(), ref[0])
+    np.testing.assert_array_equal(rs.w.cpu().numpy(), ref[1])
+    np.testing.assert_array_equal(rs.counts.cpu().numpy(), ref[2])
+    np.testing.assert_array_equal(dump.cpu().numpy(), ref[3])
+
+
+def test_pack_weight_is_the_documented_permutation():
+    E, d = 96, 256
+    _, W = synth.normal_router_inputs(1, d, E, seed=13, dtype="bf16")
+    Wt = to_dev(W)
+    P = torch.empty_like(Wt)
+    B.idb_router_pack_weight(Wt, P)
+    nch = d // 64  # 128-byte chunks of a bf16 row
+    want = W.view(np.uint16).reshape(E // 32, 32, nch, 2, 4, 8).transpose(0, 2, 4, 3, 1, 5).reshape(E, d)
+    got = P.cpu().view(torch.int16).numpy().view(np.uint16)
+    np.testing.assert_array_equal(got, want)
