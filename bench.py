@@ -1,12 +1,19 @@
 """Benchmark of the ID Balancing router + controller step on one MI355X.
 
-One step = the whole hot path over one batch: fused gate contraction +
-sigmoid + biased Top-K + gate weights + load counts (idb_router_forward),
-the ID controller update (idb_controller_update) and MaxVio/MinVio
-(idb_load_stats).  Inputs are synthetic, seeded, resident in HBM before the
-timed region; the hidden-state batch rotates over several distinct buffers so
-it is not served from the 256 MB Infinity Cache.  Each step is one HIP graph
-replay (the graph holds exactly the ABI calls of one step).
+One step = the whole hot path over one batch: repacking the router matrix
+into the MFMA operand layout (a training step changes it after every
+optimizer update), the fused gate contraction + sigmoid + biased Top-K + gate
+weights + load counts (idb_router_forward), the ID controller update
+(idb_controller_update) and MaxVio/MinVio (idb_load_stats).  Inputs are
+synthetic, seeded, resident in HBM before the timed region; the hidden-state
+batch rotates over several distinct buffers so it is not served from the
+256 MB Infinity Cache.  Steps are issued as HIP graph replays, each graph
+holding the ABI calls of several consecutive steps (one per input buffer), so
+exactly ``--steps`` steps run in the timed region.
+
+``--pmc-pass`` instead runs a short eager sequence for hardware-counter
+collection: one device-to-device copy of known size (the calibration for the
+HBM byte counters) followed by a few launches of the fused router kernel.
 
 Prints one JSON line: routed tokens/s for the step, with the dominant
 kernel's roofline and the CPU oracle timed on a bounded sample of the same
@@ -15,7 +22,6 @@ workload.
 from __future__ import annotations
 
 import argparse
-import hashlib
 import json
 import math
 import os
@@ -35,16 +41,10 @@ def log(msg: str) -> None:
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-def router_source_hash() -> str:
-    h = hashlib.sha256()
-    for f in ("router.hip", "common.h"):
-        with open(os.path.join(ROOT, "paper_2609_39137_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
-    return h.hexdigest()[:16]
-
-
 def load_traffic(workload: str, variant_id: int):
-    """HBM bytes per launch of the dominant kernel from a committed PMC summary, or None if stale/absent."""
+    """HBM bytes per launch of the dominant kernel from a committed counter summary, or None if stale/absent."""
+    from paper_2609_39137_amd.profsum import router_source_hash
+
     path = os.path.join(PROFILES, f"router_score_select_{workload}_pmc.json")
     if not os.path.exists(path):
         return None
@@ -56,27 +56,36 @@ def load_traffic(workload: str, variant_id: int):
 
 
 def cpu_baseline(wl, W, target_s: float):
-    """Time the CPU oracle (router + controller + stats) on a bounded sample of the workload."""
+    """Time the CPU oracle (router + controller + stats) on a bounded sample of the workload.
+
+    The sample is a prefix of batch 0's tokens, grown until one oracle step
+    takes about a second, then that step is repeated (the controller state
+    carries over, as in training) until about ``target_s`` seconds of CPU
+    work have been timed."""
     import oracle
     from paper_2609_39137_amd import synth
 
     threads = oracle.num_threads()
-    n = 64
-    x = synth.hidden_states(wl, step=0, rows=np.arange(n))
+    n = 256
+    while True:
+        x = synth.hidden_states(wl, step=0, rows=np.arange(n))
+        t = oracle.step_seconds(x, W, wl.K, 6e-3, 6e-3, oracle.ControllerState(wl.E))
+        if t >= 0.5 or n >= wl.T:
+            break
+        n = min(wl.T, n * 4)
+    reps = max(1, int(round(target_s / max(t, 1e-6))))
     st = oracle.ControllerState(wl.E)
-    t = oracle.step_seconds(x, W, wl.K, 6e-3, 6e-3, st)
-    n = int(min(wl.T, max(n, n * target_s / max(t, 1e-6))))
-    n = max(64, (n // 64) * 64)
-    x = synth.hidden_states(wl, step=0, rows=np.arange(n))
-    st = oracle.ControllerState(wl.E)
-    t = oracle.step_seconds(x, W, wl.K, 6e-3, 6e-3, st)
+    total = 0.0
+    for _ in range(reps):
+        total += oracle.step_seconds(x, W, wl.K, 6e-3, 6e-3, st)
     return {
-        "value": n / t,
+        "value": n * reps / total,
         "unit": "routed tokens/s",
         "cores": threads,
         "kind": "oracle",
-        "sample": f"first {n} of the {wl.T} tokens of step 0 ({wl.name}), one router step + ID update + "
-                  f"MaxVio/MinVio, {t:.2f} s wall on {threads} OpenMP threads",
+        "sample": f"{reps} oracle steps (router + ID update + MaxVio/MinVio, controller state carried over) on the "
+                  f"first {n} of the {wl.T} tokens of batch 0 of {wl.name}: {total:.2f} s wall on {threads} "
+                  f"OpenMP threads",
     }
 
 
@@ -89,8 +98,11 @@ def main() -> int:
     ap.add_argument("--variant", type=int, default=0, help="router tiling (0 = automatic)")
     ap.add_argument("--buffers", type=int, default=0, help="distinct hidden-state buffers to rotate (0 = auto)")
     ap.add_argument("--eager", action="store_true", help="launch the ABI calls directly instead of graph replays")
+    ap.add_argument("--pmc-pass", action="store_true",
+                    help="eager copy calibration + a few router launches, for rocprofv3 counter passes")
+    ap.add_argument("--copy-mib", type=int, default=512, help="size of the calibration copy of --pmc-pass")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-seconds", type=float, default=3.0, help="wall-clock target of the CPU oracle sample")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0, help="wall-clock target of the CPU oracle sample")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -132,46 +144,67 @@ def main() -> int:
     stream = torch.cuda.Stream()  # default priority
     torch.cuda.synchronize()
 
+    def one_step(i):
+        rs.pack(W, stream=stream)
+        rs.step(xs[i % nbuf], None, stream=stream)
+
     # eager warm-up (also validates every call)
     with torch.cuda.stream(stream):
         for i in range(2):
-            rs.step(xs[i % nbuf], W)
+            one_step(i)
     torch.cuda.synchronize()
 
-    step_graphs, k1_graphs = [], []
-    if not args.eager:
-        with torch.cuda.stream(stream):
-            for i in range(nbuf):
-                g = torch.cuda.CUDAGraph()
-                with torch.cuda.graph(g, stream=stream):
-                    rs.step(xs[i], W)
-                step_graphs.append(g)
-            for i in range(nbuf):
-                g = torch.cuda.CUDAGraph()
-                with torch.cuda.graph(g, stream=stream):
-                    rs.score_select(xs[i], W)
-                k1_graphs.append(g)
+    if args.pmc_pass:
+        n_copy = args.copy_mib * 2**20
+        src = torch.empty(n_copy, dtype=torch.uint8, device=dev).fill_(1)
+        dst = torch.empty_like(src)
         torch.cuda.synchronize()
+        with torch.cuda.stream(stream):
+            dst.copy_(src)
+            for i in range(3):
+                rs.score_select(xs[i % nbuf], None, stream=stream)
+        torch.cuda.synchronize()
+        print(json.dumps({"pmc_pass": True, "copy_bytes": n_copy, "workload": wl.name,
+                          "variant": rs.info["variant"], "router_launches": 3}), flush=True)
+        return 0
 
-    def run_steps(n, start=0):
-        for k in range(start, start + n):
-            if args.eager:
-                rs.step(xs[k % nbuf], W, stream=stream)
-            else:
-                step_graphs[k % nbuf].replay()
+    def capture(fn, n):
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.stream(stream):
+            with torch.cuda.graph(g, stream=stream):
+                for i in range(n):
+                    fn(i)
+        return g
 
-    with torch.cuda.stream(stream):
-        run_steps(args.warmup)
+    graphs = {}
+
+    def run_steps(n):
+        """Issue exactly n steps: full replays of the nbuf-step graph, then a graph of the remainder."""
+        if args.eager:
+            with torch.cuda.stream(stream):
+                for i in range(n):
+                    one_step(i)
+            return
+        full, rem = divmod(n, nbuf)
+        for part in ([nbuf] if full else []) + ([rem] if rem else []):
+            if part not in graphs:
+                graphs[part] = capture(one_step, part)
+        with torch.cuda.stream(stream):
+            for _ in range(full):
+                graphs[nbuf].replay()
+            if rem:
+                graphs[rem].replay()
+
+    run_steps(args.warmup)
     torch.cuda.synchronize()
     log(f"warm-up of {args.warmup} steps done")
 
     ev0 = torch.cuda.Event(enable_timing=True)
     ev1 = torch.cuda.Event(enable_timing=True)
-    with torch.cuda.stream(stream):
-        torch.cuda.synchronize()
-        ev0.record(stream)
-        run_steps(args.steps, args.warmup)
-        ev1.record(stream)
+    torch.cuda.synchronize()
+    ev0.record(stream)
+    run_steps(args.steps)
+    ev1.record(stream)
     torch.cuda.synchronize()
     ms_total = ev0.elapsed_time(ev1)
     ms_step = ms_total / args.steps
@@ -183,19 +216,23 @@ def main() -> int:
     assert int(rs.state.status.item()) == 0
     stats = rs.stats.cpu().tolist()
 
-    # live timing of the dominant kernel (score/select) on the same stream
-    n_k1 = max(args.steps, 50)
+    # live timing of the dominant kernel: back-to-back launches of the fused
+    # router kernel alone, on the stream the steps run on, between HIP events
+    per = nbuf * max(1, 16 // nbuf)
+    k1_graph = capture(lambda i: rs.score_select(xs[i % nbuf], None, stream=stream), per)
+    n_rep = max(1, -(-max(args.steps, 64) // per))
     with torch.cuda.stream(stream):
-        for k in range(5):
-            (k1_graphs[k % nbuf].replay() if k1_graphs else rs.score_select(xs[k % nbuf], W, stream=stream))
-        torch.cuda.synchronize()
-        ev0.record(stream)
-        for k in range(n_k1):
-            (k1_graphs[k % nbuf].replay() if k1_graphs else rs.score_select(xs[k % nbuf], W, stream=stream))
-        ev1.record(stream)
+        for _ in range(2):
+            k1_graph.replay()
     torch.cuda.synchronize()
-    k1_ms = ev0.elapsed_time(ev1) / n_k1
-    log(f"score/select kernel: {k1_ms * 1000:.2f} us/launch")
+    ev0.record(stream)
+    with torch.cuda.stream(stream):
+        for _ in range(n_rep):
+            k1_graph.replay()
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    k1_ms = ev0.elapsed_time(ev1) / (n_rep * per)
+    log(f"fused router kernel: {k1_ms * 1000:.2f} us/launch over {n_rep * per} launches")
 
     flops = wl.flops
     peak = PEAK_BF16_TFLOPS if wl.dtype == "bf16" else PEAK_F32_TFLOPS
@@ -209,6 +246,7 @@ def main() -> int:
         "traffic": load_traffic(wl.name, rs.info["variant"]),
         "kernel": "router_score_select_kernel",
         "kernel_us": round(k1_ms * 1000, 2),
+        "flops_per_launch": flops,
     }
     value = wl.T / (ms_step * 1e-3)
     out = {
@@ -226,7 +264,9 @@ def main() -> int:
         "data": "synthetic",
         "config": {"workload": wl.name, "T": wl.T, "d": wl.d, "E": wl.E, "K": wl.K, "global_batch": wl.T,
                    "parallelism": "single GPU", "variant": rs.info["variant"],
-                   "launch": "eager" if args.eager else "hip-graph per step", "input_buffers": nbuf},
+                   "launch": "eager" if args.eager else f"hip-graph of {nbuf} steps", "input_buffers": nbuf,
+                   "weight": "bf16 row-major, repacked every step" if wl.dtype == "bf16" else
+                             "fp32 row-major, repacked every step"},
         "roofline": roofline,
         "last_step": {"maxvio": stats[0], "minvio": stats[1]},
     }

@@ -31,8 +31,12 @@ class RouterStep:
         self.W_packed = None
 
     def pack(self, W, stream=None):
-        """Pack the router matrix once per weight update; later calls read the packed copy."""
-        self.W_packed = torch.empty_like(W)
+        """Pack the router matrix (once per weight update); later calls with ``W=None`` read the packed copy.
+
+        The packed buffer is allocated on the first call and reused after, so
+        the call can be captured in a graph."""
+        if self.W_packed is None or self.W_packed.shape != W.shape or self.W_packed.dtype != W.dtype:
+            self.W_packed = torch.empty_like(W)
         B.idb_router_pack_weight(W, self.W_packed, stream)
         return self.W_packed
 
