@@ -161,6 +161,8 @@ def _router_call(fn: str, x, W_g, bias, K, expert_idx, gate_w, counts, accumulat
         raise ValueError("router operands disagree in shape or dtype")
     if expert_idx.shape != (T, K) or gate_w.shape != (T, K) or counts.shape != (E,):
         raise ValueError("router outputs have the wrong shape")
+    if scores_dump is not None and (scores_dump.dtype != torch.float32 or scores_dump.numel() != T * E):
+        raise ValueError("scores_dump must be a float32 tensor of T*E elements")
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     st = getattr(lib(), fn)(_ptr(x), _ptr(W_g), _dtype_code(x), int(weight_layout), _ptr(bias), T, d, E, K,
                             _ptr(expert_idx),

@@ -26,6 +26,10 @@ FLAGS = [
     "-ffp-contract=off",
     # no packed fp32 instructions
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # MFMA accumulators in VGPRs (the A operands then sit in AGPRs).  The
+    # default heuristic keeps them in AGPRs and copies all of them through
+    # VGPRs on every iteration of the contraction loop.
+    "-mllvm", "-amdgpu-mfma-vgpr-form=1",
     "-I", os.path.join(ROOT, "include"), "-I", CSRC,
 ]
 

@@ -25,6 +25,17 @@ __device__ __forceinline__ bool ranks_above(float va, int ia, float vb, int ib) 
     return (va > vb) || (va == vb && ia < ib);
 }
 
+// The same order as one unsigned 64-bit key: key(a) > key(b) exactly when
+// ranks_above(a, b).  High word: the float's bits mapped to an unsigned order
+// (after -0 -> +0, so equal values get equal words); low word: ~index, so the
+// lower index wins ties.  Key 0 ranks below every finite or infinite value and
+// serves as "no entry".
+__device__ __forceinline__ unsigned long long rank_key(float v, int idx) {
+    const unsigned u = __float_as_uint(v + 0.0f);  // -0 + +0 = +0
+    const unsigned o = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+    return ((unsigned long long)o << 32) | (unsigned)(~(unsigned)idx);
+}
+
 // Score activation s = sigmoid(z) = 1 / (1 + 2^(-z log2 e)) with the hardware
 // exp2 and reciprocal (each about 1 ulp).  Saturates to exactly 0 and 1.
 __device__ __forceinline__ float sigmoid_fast(float z) {

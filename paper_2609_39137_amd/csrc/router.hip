@@ -25,19 +25,21 @@
 // (l % 32) of the block and experts 8*(r/4) + 4*(l/32) + (r%4), r < 16.  So a
 // token's BE scores are spread over 2*WAVES lanes, 16*NBLK per lane.
 //
-// Epilogue per token and slice (exact for any input):
-//   1. s = sigmoid(z) (computed once), v = fl32(s + b).
-//   2. Each lane splits its values into G groups, 16 group maxima per token;
-//      tau = the K-th largest group maximum <= the token's K-th largest v.
-//   3. Each lane counts its values >= tau; a prefix over the token's lanes
-//      gives every lane its write offset, and the candidates (typically about
-//      K + 5) are written to an LDS list without atomics.
-//   4. Candidate rank = number of candidates above it in the order (v desc,
-//      index asc); ranks < K are the slice's selection, in rank order.
-//   5. Lists that would overflow (heavy ties, K > 16) are resolved one token
-//      at a time: the token's values are gathered into an LDS row and one wave
-//      takes K rounds of wave-wide argmax.
-//   6. One slice: gate weights, outputs and an LDS histogram flushed with one
+// Epilogue (exact for any input).  The scores of PB token blocks at a time
+// are written token-major into LDS (the contraction's staging area is free by
+// then); TPT adjacent threads then own one token, VPT contiguous experts each.
+//   A. s = sigmoid(z) into the LDS score matrix (padding experts: -inf).
+//   B. v = fl32(s + b) into registers; 16 group maxima per token.
+//   C. tau = the K-th largest group maximum, <= the token's K-th largest v;
+//      each thread marks its values >= tau in a bitmask and counts them.
+//   D. A prefix over the token's threads gives write offsets; the candidates
+//      (typically about K + 5) go to an LDS list as 64-bit rank keys.
+//   E. Candidate rank = number of list keys above it; ranks < K are the
+//      slice's selection, in rank order.
+//   F. Tokens whose list would overflow (heavy ties, K > 16) are resolved by
+//      one wave each: K rounds of "best key strictly below the previous pick"
+//      over the token's LDS score row.
+//   G. One slice: gate weights, outputs and an LDS histogram flushed with one
 //      atomic per non-zero bin.  Several slices: the slice's K candidates go
 //      to the workspace and router_merge_kernel combines them.
 #include "common.h"
@@ -53,46 +55,48 @@ constexpr int kCap = 32;     // candidate list capacity per token and slice
 constexpr int kRowPad = 144;  // LDS bytes per staged token row (128 + 16 pad)
 constexpr int kMaxSlices = 8;
 
+constexpr int kScoreLds = 100000;  // LDS budget of the epilogue's score matrix
+
 template <bool F32, int WAVES, int TBW, int NBLK>
 struct Cfg {
     static constexpr int NT = WAVES * 64;
     static constexpr int BT = 32 * TBW;
     static constexpr int WE = 32 * NBLK;
     static constexpr int BE = WAVES * WE;
-    static constexpr int NV = 16 * NBLK;     // values per lane per token
-    static constexpr int G = 8 / WAVES;      // groups per lane: 2*WAVES*G = 16
-    static constexpr int GS = NV / G;        // values per group
-    static constexpr int TPT = NT / BT;      // threads per token in the ranking
-    static constexpr int NLANES = 2 * WAVES;  // lanes holding one token's slice
     static constexpr int PPT = BT * 8 / NT;  // 16-byte token-tile pieces per thread per chunk
     static constexpr int STAGE = BT * kRowPad;
     static constexpr int MAIN_LDS = 2 * STAGE;
-    // epilogue LDS layout (bytes).  Per-token rows are padded (17, NLANES+1 and
-    // 36 words) so the 32 tokens of a wave fall on different LDS banks; the
-    // 36-word rows are also 16-byte aligned for vector reads.
-    static constexpr int GMS = 17;            // group-maximum row stride (words)
-    static constexpr int CNS = NLANES + 1;    // count row stride
-    static constexpr int LST = kCap + 4;      // candidate / selection row stride
-    static constexpr int OFF_GM = 0;
-    static constexpr int OFF_TAU = OFF_GM + BT * GMS * 4;
-    static constexpr int OFF_CNT = OFF_TAU + BT * 4;
-    static constexpr int OFF_LV = ((OFF_CNT + BT * CNS * 4) + 15) / 16 * 16;
-    static constexpr int OFF_LS = OFF_LV + BT * LST * 4;
-    static constexpr int OFF_LI = OFF_LS + BT * LST * 4;
-    static constexpr int OFF_SV = OFF_LI + BT * LST * 4;
-    static constexpr int OFF_SS = OFF_SV + BT * LST * 4;
-    static constexpr int OFF_SI = OFF_SS + BT * LST * 4;
-    static constexpr int OFF_OVF = OFF_SI + BT * LST * 4;
-    static constexpr int OFF_ROWV = OFF_OVF + 16 * 4;
-    static constexpr int OFF_ROWS = OFF_ROWV + BE * 4;
-    static constexpr int OFF_HIST = OFF_ROWS + BE * 4;
+    // epilogue: PB token blocks (TPP tokens) per pass, TPT threads per token
+    static constexpr int RS = BE + 4;  // score row stride in floats (odd number of 16-byte units)
+    static constexpr int PB = (TBW % 4 == 0 && 128 * RS * 4 <= kScoreLds) ? 4
+                              : ((TBW % 2 == 0 && 64 * RS * 4 <= kScoreLds) ? 2 : 1);
+    static constexpr int TPP = 32 * PB;
+    static constexpr int NPASS = TBW / PB;
+    static constexpr int TPT = NT / TPP;
+    static constexpr int VPT = BE / TPT;  // slice columns per thread
+    static constexpr int GPT = 16 / TPT;  // group maxima per thread
+    static constexpr int GSZ = VPT / GPT;
+    static constexpr int MW = (VPT + 31) / 32;  // candidate mask words
+    static constexpr int GMS = 20;              // group-maximum row stride (words, 16-byte aligned)
+    static constexpr int CNS = TPT + 1;         // count row stride
+    static constexpr int LKS = kCap + 2;        // candidate-key row stride (8-byte keys)
+    static constexpr int LSS = kMaxK + 4;       // selection row stride
+    static constexpr int OFF_SC = 0;
+    static constexpr int OFF_BIAS = OFF_SC + TPP * RS * 4;
+    static constexpr int OFF_GM = OFF_BIAS + BE * 4;
+    static constexpr int OFF_CNT = OFF_GM + TPP * GMS * 4;
+    static constexpr int OFF_LK = (OFF_CNT + TPP * CNS * 4 + 15) / 16 * 16;
+    static constexpr int OFF_SI = OFF_LK + TPP * LKS * 8;
+    static constexpr int OFF_SS = OFF_SI + TPP * LSS * 4;
+    static constexpr int OFF_OVF = OFF_SS + TPP * LSS * 4;
+    static constexpr int OFF_HIST = OFF_OVF + 16 * 4;
     static constexpr int EPI_LDS = OFF_HIST + 1024 * 4;
     static constexpr int LDS = MAIN_LDS > EPI_LDS ? MAIN_LDS : EPI_LDS;
-    static_assert(BT <= NT, "one thread per token in the threshold step");
-    static_assert(NV % G == 0, "groups must split a lane's values evenly");
     static_assert(PPT * NT == BT * 8, "token-tile pieces must split evenly over threads");
-    static_assert(BT <= 16 * 32, "overflow bitmask size");
-    static_assert(BE % 64 == 0, "overflow gather row is read 64 lanes at a time");
+    static_assert(TPT * TPP == NT && TPT <= 16 && 16 % TPT == 0, "a token's threads share one wave");
+    static_assert(VPT * TPT == BE && VPT % 4 == 0 && GSZ * GPT == VPT, "columns split evenly");
+    static_assert(TPP <= 16 * 32, "overflow bitmask size");
+    static_assert(LDS <= 160 * 1024, "LDS of one workgroup");
 };
 
 // One 16-byte unit of both operands: bf16 -> one 32x32x16 MFMA; fp32 -> four
@@ -112,10 +116,6 @@ __device__ __forceinline__ floatx16 mfma_unit(uint4 a, uint4 b, floatx16 c) {
     } else {
         return __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a), as_bf16x8(b), c, 0, 0, 0);
     }
-}
-
-__device__ __forceinline__ float comp4(const float4& f, int i) {
-    return i == 0 ? f.x : (i == 1 ? f.y : (i == 2 ? f.z : f.w));
 }
 
 template <bool F32, bool PACKED, int WAVES, int TBW, int NBLK>
@@ -186,404 +186,367 @@ __global__ __launch_bounds__(WAVES * 64) void router_score_select_kernel(RouterA
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[tb][nbk][r] = 0.0f;
 
-    // Software pipeline.  W operands: one register set refilled unit by unit
-    // (right after the MFMAs of unit u of chunk c, the same registers start
-    // loading unit u of chunk c+1).  Token tile: loaded into staging registers
-    // at the top of chunk c for chunk c+1, stored into the idle LDS stage at
-    // the end of chunk c.  Vector-memory loads complete in order, and in this
-    // issue order each wait the compiler inserts covers only the data about
-    // to be used.
-    uint4 w[NBLK][4], xr[C::PPT];
-    auto load_x = [&](int c) {
+    // Software pipeline, two chunks deep for both operands.  W operands: two
+    // register sets; right after the MFMAs of unit u of chunk c, set c&1
+    // starts loading unit u of chunk c+2.  Token tile: two sets of staging
+    // registers; the top of chunk c loads chunk c+2 into the set that held
+    // chunk c, and the end of chunk c stores chunk c+1 (loaded a whole chunk
+    // earlier) into the idle LDS stage.  Every fetch thus has about two
+    // chunks of MFMA work to arrive.  Vector-memory loads complete in order,
+    // and in this issue order each wait the compiler inserts covers only the
+    // data about to be used.
+    uint4 w[2][NBLK][4], xr[2][C::PPT];
+    auto load_x = [&](int c, int j) {
 #pragma unroll
-        for (int q = 0; q < C::PPT; ++q) xr[q] = ld16(xsrc[q] + c * 128);
+        for (int q = 0; q < C::PPT; ++q) xr[j][q] = ld16(xsrc[q] + c * 128);
     };
-    auto store_x = [&](int stage) {
+    auto store_x = [&](int stage, int j) {
 #pragma unroll
-        for (int q = 0; q < C::PPT; ++q) *reinterpret_cast<uint4*>(smem + stage * C::STAGE + xdst[q]) = xr[q];
+        for (int q = 0; q < C::PPT; ++q) *reinterpret_cast<uint4*>(smem + stage * C::STAGE + xdst[q]) = xr[j][q];
     };
-
-    load_x(0);
-#pragma unroll
-    for (int nbk = 0; nbk < NBLK; ++nbk)
-#pragma unroll
-        for (int u = 0; u < 4; ++u) w[nbk][u] = ld16(wrow[nbk] + WU * u);
-    store_x(0);
-    __syncthreads();
-    for (int c = 0; c < NCH; ++c) {
-        const bool more = c + 1 < NCH;
-        if (more) load_x(c + 1);
-        const unsigned char* st = smem + (c & 1) * C::STAGE + boff;
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            uint4 bx[TBW];
-#pragma unroll
-            for (int tb = 0; tb < TBW; ++tb) bx[tb] = *reinterpret_cast<const uint4*>(st + tb * 32 * kRowPad + 16 * u);
-#pragma unroll
-            for (int tb = 0; tb < TBW; ++tb)
-#pragma unroll
-                for (int nbk = 0; nbk < NBLK; ++nbk) acc[tb][nbk] = mfma_unit<F32>(w[nbk][u], bx[tb], acc[tb][nbk]);
-            if (more) {
-#pragma unroll
-                for (int nbk = 0; nbk < NBLK; ++nbk) w[nbk][u] = ld16(wrow[nbk] + (c + 1) * WCH + WU * u);
-            }
-        }
-        if (more) store_x((c + 1) & 1);
-        __syncthreads();
-    }
-
-    // ---------------------------------------------------------------- epilogue
-    float* gm = reinterpret_cast<float*>(smem + C::OFF_GM);
-    float* tau_s = reinterpret_cast<float*>(smem + C::OFF_TAU);
-    int* cnt = reinterpret_cast<int*>(smem + C::OFF_CNT);
-    float* lv = reinterpret_cast<float*>(smem + C::OFF_LV);
-    float* ls = reinterpret_cast<float*>(smem + C::OFF_LS);
-    int* li = reinterpret_cast<int*>(smem + C::OFF_LI);
-    float* sv = reinterpret_cast<float*>(smem + C::OFF_SV);
-    float* ss = reinterpret_cast<float*>(smem + C::OFF_SS);
-    int* si = reinterpret_cast<int*>(smem + C::OFF_SI);
-    unsigned* ovf = reinterpret_cast<unsigned*>(smem + C::OFF_OVF);
-    float* rowv = reinterpret_cast<float*>(smem + C::OFF_ROWV);
-    float* rows = reinterpret_cast<float*>(smem + C::OFF_ROWS);
-    int* hist = reinterpret_cast<int*>(smem + C::OFF_HIST);
-
-    // Expert of accumulator (nbk, r): ebase + 32 nbk + 8 (r/4) + (r%4).  E is a
-    // multiple of 32, so a whole 32-expert block is either real or padding.
-    const int ebase = e_wave0 + 4 * h;
-    auto blk_real = [&](int nbk) { return e_wave0 + nbk * 32 < E; };
-    const int slot = wave * 2 + h;  // this lane's position among the token's lanes
-
-    // this lane's bias values, four consecutive experts per (nbk, r/4)
-    float4 b4[NBLK][4];
-#pragma unroll
-    for (int nbk = 0; nbk < NBLK; ++nbk)
-#pragma unroll
-        for (int r4 = 0; r4 < 4; ++r4) {
-            const int e = ebase + nbk * 32 + 8 * r4;
-            b4[nbk][r4] = blk_real(nbk) ? make_float4(a.bias[e], a.bias[e + 1], a.bias[e + 2], a.bias[e + 3])
-                                        : make_float4(0.f, 0.f, 0.f, 0.f);
-        }
-    for (int e = tid; e < 1024; e += C::NT) hist[e] = 0;
-    if (tid < 16) ovf[tid] = 0;
-
-    // 1. scores, once (and the optional debug dump of exactly these values)
-#pragma unroll
-    for (int tb = 0; tb < TBW; ++tb)
+    auto load_w = [&](int c, int j) {
 #pragma unroll
         for (int nbk = 0; nbk < NBLK; ++nbk)
 #pragma unroll
-            for (int r = 0; r < 16; ++r) acc[tb][nbk][r] = sigmoid_fast(acc[tb][nbk][r]);
-    if (a.dump) {
+            for (int u = 0; u < 4; ++u) w[j][nbk][u] = ld16(wrow[nbk] + c * WCH + WU * u);
+    };
+
+    load_x(0, 0);
+    load_w(0, 0);
+    if (NCH > 1) {
+        load_x(1, 1);
+        load_w(1, 1);
+    }
+    store_x(0, 0);
+    __syncthreads();
+    for (int c0 = 0; c0 < NCH; c0 += 2) {
 #pragma unroll
-        for (int tb = 0; tb < TBW; ++tb) {
-            const int64_t tok = tok0 + tb * 32 + l32;
-            if (tok < T) {
+        for (int j = 0; j < 2; ++j) {
+            const int c = c0 + j;
+            if (c < NCH) {
+                const bool more2 = c + 2 < NCH;
+                if (more2) load_x(c + 2, j);
+                const unsigned char* st = smem + j * C::STAGE + boff;
 #pragma unroll
-                for (int nbk = 0; nbk < NBLK; ++nbk)
-                    if (blk_real(nbk)) {
+                for (int u = 0; u < 4; ++u) {
+                    uint4 bx[TBW];
 #pragma unroll
-                        for (int r4 = 0; r4 < 4; ++r4)
-                            *reinterpret_cast<float4*>(a.dump + tok * E + ebase + nbk * 32 + 8 * r4) =
-                                make_float4(acc[tb][nbk][4 * r4], acc[tb][nbk][4 * r4 + 1], acc[tb][nbk][4 * r4 + 2],
-                                            acc[tb][nbk][4 * r4 + 3]);
+                    for (int tb = 0; tb < TBW; ++tb)
+                        bx[tb] = *reinterpret_cast<const uint4*>(st + tb * 32 * kRowPad + 16 * u);
+#pragma unroll
+                    for (int tb = 0; tb < TBW; ++tb)
+#pragma unroll
+                        for (int nbk = 0; nbk < NBLK; ++nbk)
+                            acc[tb][nbk] = mfma_unit<F32>(w[j][nbk][u], bx[tb], acc[tb][nbk]);
+                    if (more2) {
+#pragma unroll
+                        for (int nbk = 0; nbk < NBLK; ++nbk)
+                            w[j][nbk][u] = ld16(wrow[nbk] + (c + 2) * WCH + WU * u);
                     }
+                }
+                if (c + 1 < NCH) store_x(1 - j, 1 - j);
+                __syncthreads();
             }
         }
     }
 
-    // 2. group maxima of v = s + b
+    // ---------------------------------------------------------------- epilogue
+    float* sc = reinterpret_cast<float*>(smem + C::OFF_SC);
+    float* bias_s = reinterpret_cast<float*>(smem + C::OFF_BIAS);
+    float* gm = reinterpret_cast<float*>(smem + C::OFF_GM);
+    int* cnt = reinterpret_cast<int*>(smem + C::OFF_CNT);
+    unsigned long long* lk = reinterpret_cast<unsigned long long*>(smem + C::OFF_LK);
+    int* si = reinterpret_cast<int*>(smem + C::OFF_SI);
+    float* ss = reinterpret_cast<float*>(smem + C::OFF_SS);
+    unsigned* ovf = reinterpret_cast<unsigned*>(smem + C::OFF_OVF);
+    int* hist = reinterpret_cast<int*>(smem + C::OFF_HIST);
+
+    // The contraction ended with a barrier, so its staging area is free.
+    const int sbase = slice * C::BE;  // first expert of the slice
+    for (int c = tid; c < C::BE; c += C::NT) bias_s[c] = (sbase + c < E) ? a.bias[sbase + c] : 0.0f;
+    for (int e = tid; e < 1024; e += C::NT) hist[e] = 0;
+
+    // Slice column of accumulator (nbk, r): ccol + 32 nbk + 8 (r/4) + (r%4).
+    // E is a multiple of 32, so a whole 32-expert block is real or padding.
+    const int ccol = wave * C::WE + 4 * h;
+    const int tl = tid / C::TPT, q = tid % C::TPT;  // token of the pass and part, in steps B-G
+    const int c0 = q * C::VPT;                       // this thread's first slice column
+    unsigned valid[C::MW];                           // columns that are real experts
+    {
+        const int nreal = E - sbase - c0;  // may be <= 0 or >= VPT
 #pragma unroll
-    for (int tb = 0; tb < TBW; ++tb) {
-        float gmx[C::G];
+        for (int w = 0; w < C::MW; ++w) {
+            const int b = nreal - 32 * w;
+            valid[w] = b >= 32 ? ~0u : (b <= 0 ? 0u : ((1u << b) - 1u));
+        }
+    }
+
 #pragma unroll
-        for (int g = 0; g < C::G; ++g) gmx[g] = -INFINITY;
+    for (int pass = 0; pass < C::NPASS; ++pass) {
+        // A. scores of the pass's token blocks into the LDS score matrix
 #pragma unroll
-        for (int nbk = 0; nbk < NBLK; ++nbk) {
-            if (!blk_real(nbk)) continue;
+        for (int pb = 0; pb < C::PB; ++pb) {
+            const int tb = pass * C::PB + pb;
+            const int row = pb * 32 + l32;
+            const int64_t tok = tok0 + tb * 32 + l32;
 #pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const int g = (nbk * 16 + r) / C::GS;
-                gmx[g] = fmaxf(gmx[g], acc[tb][nbk][r] + comp4(b4[nbk][r >> 2], r & 3));
+            for (int nbk = 0; nbk < NBLK; ++nbk) {
+                const bool real = sbase + ccol - 4 * h + nbk * 32 < E;
+#pragma unroll
+                for (int r4 = 0; r4 < 4; ++r4) {
+                    float4 s4;
+                    s4.x = real ? sigmoid_fast(acc[tb][nbk][4 * r4 + 0]) : -INFINITY;
+                    s4.y = real ? sigmoid_fast(acc[tb][nbk][4 * r4 + 1]) : -INFINITY;
+                    s4.z = real ? sigmoid_fast(acc[tb][nbk][4 * r4 + 2]) : -INFINITY;
+                    s4.w = real ? sigmoid_fast(acc[tb][nbk][4 * r4 + 3]) : -INFINITY;
+                    const int col = ccol + nbk * 32 + 8 * r4;
+                    *reinterpret_cast<float4*>(sc + row * C::RS + col) = s4;
+                    if (a.dump && real && tok < T)
+                        *reinterpret_cast<float4*>(a.dump + tok * E + sbase + col) = s4;
+                }
             }
         }
-#pragma unroll
-        for (int g = 0; g < C::G; ++g) gm[(tb * 32 + l32) * C::GMS + slot * C::G + g] = gmx[g];
-    }
-    __syncthreads();
+        if (tid < 16) ovf[tid] = 0;
+        __syncthreads();
 
-    // 3. per-token threshold
-    if (tid < C::BT) {
-        float g16[16];
+        // B. biased values of this thread's columns; group maxima
+        float v[C::VPT];
 #pragma unroll
-        for (int i = 0; i < 16; ++i) g16[i] = gm[tid * C::GMS + i];
-        sort16_ascending(g16);
+        for (int j4 = 0; j4 < C::VPT / 4; ++j4) {
+            const float4 s4 = *reinterpret_cast<const float4*>(sc + tl * C::RS + c0 + 4 * j4);
+            const float4 b4 = *reinterpret_cast<const float4*>(bias_s + c0 + 4 * j4);
+            v[4 * j4 + 0] = s4.x + b4.x;
+            v[4 * j4 + 1] = s4.y + b4.y;
+            v[4 * j4 + 2] = s4.z + b4.z;
+            v[4 * j4 + 3] = s4.w + b4.w;
+        }
+#pragma unroll
+        for (int g = 0; g < C::GPT; ++g) {
+            float m = -INFINITY;
+#pragma unroll
+            for (int j = 0; j < C::GSZ; ++j) m = fmaxf(m, v[g * C::GSZ + j]);
+            gm[tl * C::GMS + q * C::GPT + g] = m;
+        }
+        __syncthreads();
+
+        // C. threshold; candidate masks and counts
         float tau = -INFINITY;
-        if (K <= 16) {
+        {
+            float g16[16];
 #pragma unroll
-            for (int i = 0; i < 16; ++i)
-                if (i == 16 - K) tau = g16[i];
+            for (int i4 = 0; i4 < 4; ++i4) {
+                const float4 t4 = *reinterpret_cast<const float4*>(gm + tl * C::GMS + 4 * i4);
+                g16[4 * i4 + 0] = t4.x;
+                g16[4 * i4 + 1] = t4.y;
+                g16[4 * i4 + 2] = t4.z;
+                g16[4 * i4 + 3] = t4.w;
+            }
+            sort16_ascending(g16);
+            if (K <= 16) {
+#pragma unroll
+                for (int i = 0; i < 16; ++i)
+                    if (i == 16 - K) tau = g16[i];
+            }
         }
-        tau_s[tid] = tau;
-    }
-    __syncthreads();
+        // Bit j: v_j >= tau, read off the sign of v_j - tau (a difference of
+        // two finite floats is +0 only when they are equal, and -inf - tau is
+        // negative); padding columns are masked out, which also covers the
+        // NaN of -inf - -inf when tau = -inf.
+        unsigned msk[C::MW];
+#pragma unroll
+        for (int w = 0; w < C::MW; ++w) msk[w] = 0u;
+#pragma unroll
+        for (int j = 0; j < C::VPT; ++j)
+            msk[j / 32] |= ((__float_as_uint(v[j] - tau) >> 31) ^ 1u) << (j % 32);
+        int own = 0;
+#pragma unroll
+        for (int w = 0; w < C::MW; ++w) {
+            msk[w] &= valid[w];
+            own += __builtin_popcount(msk[w]);
+        }
+        cnt[tl * C::CNS + q] = own;
+        __syncthreads();
 
-    // 4. candidates v >= tau: count, prefix over the token's lanes, write
-    float taus[TBW];
+        // D. write offsets; candidate keys into the token's list
+        int off = 0, n = 0;
 #pragma unroll
-    for (int tb = 0; tb < TBW; ++tb) {
-        const int tl = tb * 32 + l32;
-        taus[tb] = tau_s[tl];
-        int n = 0;
-#pragma unroll
-        for (int nbk = 0; nbk < NBLK; ++nbk) {
-            if (!blk_real(nbk)) continue;
-#pragma unroll
-            for (int r = 0; r < 16; ++r) n += (acc[tb][nbk][r] + comp4(b4[nbk][r >> 2], r & 3) >= taus[tb]) ? 1 : 0;
+        for (int o = 0; o < C::TPT; ++o) {
+            const int m = cnt[tl * C::CNS + o];
+            off += (o < q) ? m : 0;
+            n += m;
         }
-        cnt[tl * C::CNS + slot] = n;
-    }
-    __syncthreads();
+        const bool listed = n <= kCap;
+        if (!listed) {
+            if (q == 0) atomicOr(&ovf[tl >> 5], 1u << (tl & 31));
+        } else {
 #pragma unroll
-    for (int tb = 0; tb < TBW; ++tb) {
-        const int tl = tb * 32 + l32;
-        int off = 0, total = 0;
-#pragma unroll
-        for (int o = 0; o < C::NLANES; ++o) {
-            const int n = cnt[tl * C::CNS + o];
-            off += (o < slot) ? n : 0;
-            total += n;
-        }
-        if (total > kCap) {
-            if (slot == 0) atomicOr(&ovf[tl >> 5], 1u << (tl & 31));
-            continue;
-        }
-        if (tok0 + tl >= T) continue;
-        const float tau = taus[tb];
-#pragma unroll
-        for (int nbk = 0; nbk < NBLK; ++nbk) {
-            if (!blk_real(nbk)) continue;
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const float s = acc[tb][nbk][r];
-                const float v = s + comp4(b4[nbk][r >> 2], r & 3);
-                if (v >= tau) {
-                    lv[tl * C::LST + off] = v;
-                    ls[tl * C::LST + off] = s;
-                    li[tl * C::LST + off] = ebase + nbk * 32 + 8 * (r >> 2) + (r & 3);
+            for (int w = 0; w < C::MW; ++w) {
+                unsigned m = msk[w];
+                while (m) {
+                    const int col = c0 + w * 32 + __builtin_ctz(m);
+                    m &= m - 1u;
+                    lk[tl * C::LKS + off] = rank_key(sc[tl * C::RS + col] + bias_s[col], sbase + col);
                     ++off;
                 }
             }
         }
-    }
-    __syncthreads();
+        __syncthreads();
 
-    // 5. rank the candidates of every token whose list did not overflow.  The
-    // token's threads hold its whole list in registers (entries past n read
-    // as (-inf, INT_MAX), which rank below everything) and count, for each of
-    // their candidates, the entries that rank above it.
-    {
-        const int tl = tid / C::TPT, q = tid % C::TPT;
-        int n = 0;
+        // E. ranks of the listed candidates (entries past n count as key 0)
+        if (listed) {
+            unsigned long long key[kCap];
 #pragma unroll
-        for (int o = 0; o < C::NLANES; ++o) n += cnt[tl * C::CNS + o];
-        if (n <= kCap) {
-            float cv[kCap];
-            int ci[kCap];
-#pragma unroll
-            for (int o4 = 0; o4 < kCap / 4; ++o4) {
-                const float4 v4 = *reinterpret_cast<const float4*>(lv + tl * C::LST + 4 * o4);
-                const int4 i4 = *reinterpret_cast<const int4*>(li + tl * C::LST + 4 * o4);
-                cv[4 * o4] = v4.x; cv[4 * o4 + 1] = v4.y; cv[4 * o4 + 2] = v4.z; cv[4 * o4 + 3] = v4.w;
-                ci[4 * o4] = i4.x; ci[4 * o4 + 1] = i4.y; ci[4 * o4 + 2] = i4.z; ci[4 * o4 + 3] = i4.w;
+            for (int o2 = 0; o2 < kCap / 2; ++o2) {
+                const ulonglong2 k2 = *reinterpret_cast<const ulonglong2*>(lk + tl * C::LKS + 2 * o2);
+                key[2 * o2] = k2.x;
+                key[2 * o2 + 1] = k2.y;
             }
 #pragma unroll
             for (int o = 0; o < kCap; ++o)
-                if (o >= n) {
-                    cv[o] = -INFINITY;
-                    ci[o] = 0x7fffffff;
-                }
+                if (o >= n) key[o] = 0ull;
             for (int c = q; c < n; c += C::TPT) {
-                const float vc = lv[tl * C::LST + c];
-                const int ic = li[tl * C::LST + c];
+                const unsigned long long mine = lk[tl * C::LKS + c];
                 int rank = 0;
 #pragma unroll
-                for (int o = 0; o < kCap; ++o) rank += ranks_above(cv[o], ci[o], vc, ic) ? 1 : 0;
+                for (int o = 0; o < kCap; ++o) rank += (key[o] > mine) ? 1 : 0;
                 if (rank < K) {
-                    sv[tl * C::LST + rank] = vc;
-                    ss[tl * C::LST + rank] = ls[tl * C::LST + c];
-                    si[tl * C::LST + rank] = ic;
+                    const int e = (int)~(unsigned)mine;
+                    si[tl * C::LSS + rank] = e;
+                    ss[tl * C::LSS + rank] = sc[tl * C::RS + (e - sbase)];
                 }
             }
         }
-    }
 
-    // 6. overflowing tokens, one at a time: gather the token's slice into an
-    // LDS row, then wave 0 takes K rounds of wave-wide argmax over it.
-    for (int word = 0; word < C::BT / 32; ++word) {
-        unsigned bits = ovf[word];  // uniform: written before the last barrier
-        while (bits) {
-            const int tl = word * 32 + __builtin_ctz(bits);
-            bits &= bits - 1;
-            const int tb = tl >> 5;
-            if ((tl & 31) == l32) {
-#pragma unroll
-                for (int tbb = 0; tbb < TBW; ++tbb) {
-                    if (tbb != tb) continue;
-#pragma unroll
-                    for (int nbk = 0; nbk < NBLK; ++nbk)
-#pragma unroll
-                        for (int r = 0; r < 16; ++r) {
-                            const int p = wave * C::WE + nbk * 32 + 8 * (r >> 2) + 4 * h + (r & 3);
-                            const float s = acc[tbb][nbk][r];
-                            rows[p] = s;
-                            rowv[p] = blk_real(nbk) ? s + comp4(b4[nbk][r >> 2], r & 3) : -INFINITY;
+        // F. overflowing tokens, one wave each (the bitmask is uniform: it was
+        // complete at the last barrier)
+        {
+            int k = 0;
+            for (int word = 0; word < C::TPP / 32; ++word) {
+                unsigned bits = ovf[word];
+                while (bits) {
+                    const int t = word * 32 + __builtin_ctz(bits);
+                    bits &= bits - 1u;
+                    if ((k++ % WAVES) != wave) continue;
+                    unsigned long long prev = ~0ull;
+                    for (int r = 0; r < K; ++r) {
+                        unsigned long long best = 0ull;
+                        for (int c = lane; c < C::BE; c += 64) {
+                            if (sbase + c < E) {
+                                const unsigned long long kk = rank_key(sc[t * C::RS + c] + bias_s[c], sbase + c);
+                                if (kk < prev && kk > best) best = kk;
+                            }
                         }
-                }
-            }
-            __syncthreads();
-            if (wave == 0) {
-                unsigned taken = 0;
-                for (int r = 0; r < K; ++r) {
-                    float bv = -INFINITY, bs = 0.0f;
-                    int bi = 0x7fffffff, bq = -1;
 #pragma unroll
-                    for (int q = 0; q < C::BE / 64; ++q) {
-                        const int p = lane + 64 * q;
-                        const float v = rowv[p];
-                        const int e = slice * C::BE + p;
-                        if (!((taken >> q) & 1u) && v != -INFINITY && ranks_above(v, e, bv, bi)) {
-                            bv = v;
-                            bs = rows[p];
-                            bi = e;
-                            bq = q;
+                        for (int o = 32; o >= 1; o >>= 1) {
+                            const unsigned lo = __shfl_xor((unsigned)best, o);
+                            const unsigned hi = __shfl_xor((unsigned)(best >> 32), o);
+                            const unsigned long long other = ((unsigned long long)hi << 32) | lo;
+                            best = other > best ? other : best;
+                        }
+                        prev = best;
+                        if (lane == 0) {
+                            const int e = (int)~(unsigned)best;
+                            si[t * C::LSS + r] = e;
+                            ss[t * C::LSS + r] = sc[t * C::RS + (e - sbase)];
                         }
                     }
-                    float wv = bv, ws = bs;
-                    int wi = bi;
-#pragma unroll
-                    for (int off = 32; off >= 1; off >>= 1) {
-                        const float ov = __shfl_xor(wv, off);
-                        const float os = __shfl_xor(ws, off);
-                        const int oi = __shfl_xor(wi, off);
-                        if (ranks_above(ov, oi, wv, wi)) {
-                            wv = ov;
-                            ws = os;
-                            wi = oi;
-                        }
-                    }
-                    if (bi == wi && bq >= 0) taken |= 1u << bq;
-                    if (lane == 0) {
-                        sv[tl * C::LST + r] = wv;
-                        ss[tl * C::LST + r] = ws;
-                        si[tl * C::LST + r] = wi;
-                    }
-                }
-            }
-            __syncthreads();
-        }
-    }
-    __syncthreads();
-
-    // 7. outputs
-    {
-        const int tl = tid / C::TPT, q = tid % C::TPT;
-        const int64_t tok = tok0 + tl;
-        if (tok < T) {
-            if (NS > 1) {
-                const int64_t base = (tok * NS + slice) * K;
-                for (int r = q; r < K; r += C::TPT) {
-                    a.cand_v[base + r] = sv[tl * C::LST + r];
-                    a.cand_s[base + r] = ss[tl * C::LST + r];
-                    a.cand_i[base + r] = si[tl * C::LST + r];
-                }
-            } else {
-                // gate weights: den is the fp32 sum of the selected unbiased
-                // scores in rank order
-                float den = 0.0f;
-#pragma unroll
-                for (int r = 0; r < kMaxK; ++r)
-                    if (r < K) den = den + ss[tl * C::LST + r];
-                for (int r = q; r < K; r += C::TPT) {
-                    const int e = si[tl * C::LST + r];
-                    a.idx[tok * K + r] = e;
-                    a.w[tok * K + r] = (den == 0.0f) ? 1.0f / (float)K : ss[tl * C::LST + r] / den;
-                    if ((unsigned)e < (unsigned)E) atomicAdd(&hist[e], 1);
                 }
             }
         }
-    }
-    if (NS == 1) {
         __syncthreads();
+
+        // G. outputs of the pass's tokens
+        {
+            const int64_t tok = tok0 + pass * C::TPP + tl;
+            if (tok < T) {
+                if (NS > 1) {
+                    const int64_t base = (tok * NS + slice) * K;
+                    for (int r = q; r < K; r += C::TPT) {
+                        const int e = si[tl * C::LSS + r];
+                        const float s = ss[tl * C::LSS + r];
+                        a.cand_v[base + r] = s + bias_s[e - sbase];
+                        a.cand_s[base + r] = s;
+                        a.cand_i[base + r] = e;
+                    }
+                } else {
+                    // gate weights: den is the fp32 sum of the selected
+                    // unbiased scores in rank order
+                    float den = 0.0f;
+#pragma unroll
+                    for (int r = 0; r < kMaxK; ++r)
+                        if (r < K) den = den + ss[tl * C::LSS + r];
+                    for (int r = q; r < K; r += C::TPT) {
+                        const int e = si[tl * C::LSS + r];
+                        a.idx[tok * K + r] = e;
+                        a.w[tok * K + r] = (den == 0.0f) ? 1.0f / (float)K : ss[tl * C::LSS + r] / den;
+                        atomicAdd(&hist[e], 1);
+                    }
+                }
+            }
+        }
+        __syncthreads();
+    }
+    if (NS == 1)
         for (int e = tid; e < E; e += C::NT)
             if (hist[e] != 0) atomicAdd(&a.counts[e], hist[e]);
-    }
 }
 
 // Merge the slices' rank-ordered candidate lists into the final Top-K, compute
-// the gate weights and count the assignments.  The workgroup copies its
-// tokens' candidates into LDS with coalesced loads, then each thread merges
-// one token.
+// the gate weights and count the assignments.  One thread per candidate: its
+// final rank is its position in its own slice's list plus the number of the
+// other slices' candidates that rank above it (keys are distinct: every
+// candidate is a different expert).  A workgroup takes groups of
+// kMergeThreads / (NS*K) tokens in a grid-stride loop and flushes one LDS
+// histogram at the end.
 constexpr int kMergeThreads = 256;
+constexpr int kMergeBlocks = 512;
 
-__global__ __launch_bounds__(kMergeThreads) void router_merge_kernel(RouterArgs a, int NS, int tokens_per_wg) {
-    extern __shared__ __attribute__((aligned(16))) unsigned char dyn[];
-    int* hist = reinterpret_cast<int*>(dyn);
+__global__ __launch_bounds__(kMergeThreads) void router_merge_kernel(RouterArgs a, int NS) {
+    __shared__ int hist[1024];
+    __shared__ unsigned long long key[kMergeThreads];
+    __shared__ float sel[kMergeThreads];  // selected scores, [token of the group][rank]
     const int E = a.E, K = a.K;
-    const int per_tok = NS * K;
-    float* cv = reinterpret_cast<float*>(dyn + 4096);
-    float* cs = cv + tokens_per_wg * per_tok;
-    int* ci = reinterpret_cast<int*>(cs + tokens_per_wg * per_tok);
+    const int per_tok = NS * K;  // <= kMaxSlices * kMaxK = kMergeThreads
+    const int tpg = kMergeThreads / per_tok;
     const int tid = threadIdx.x;
+    const int tt = tid / per_tok, pos = tid - tt * per_tok;
+    const int sl = pos / K, r = pos - sl * K;
     for (int e = tid; e < E; e += kMergeThreads) hist[e] = 0;
-    for (int64_t tok_base = (int64_t)blockIdx.x * tokens_per_wg; tok_base < a.T;
-         tok_base += (int64_t)gridDim.x * tokens_per_wg) {
-        const int ntok = (int)((a.T - tok_base) < tokens_per_wg ? (a.T - tok_base) : tokens_per_wg);
-        const int64_t g0 = tok_base * per_tok;
+    const int64_t groups = (a.T + tpg - 1) / tpg;
+    for (int64_t g = blockIdx.x; g < groups; g += gridDim.x) {
+        const int64_t tok = g * tpg + tt;
+        const bool act = tt < tpg && tok < a.T;
+        float s = 0.0f;
+        int e = 0;
+        unsigned long long k = 0ull;
+        if (act) {
+            const int64_t gi = tok * per_tok + pos;
+            s = a.cand_s[gi];
+            e = a.cand_i[gi];
+            k = rank_key(a.cand_v[gi], e);
+        }
+        __syncthreads();  // the previous group is done with key[] and sel[]
+        key[tid] = k;
         __syncthreads();
-        for (int i = tid; i < ntok * per_tok; i += kMergeThreads) {
-            cv[i] = a.cand_v[g0 + i];
-            cs[i] = a.cand_s[g0 + i];
-            ci[i] = a.cand_i[g0 + i];
+        int rank = r;
+        if (act) {
+            for (int o = 0; o < NS; ++o) {
+                if (o == sl) continue;
+                const int b = tt * per_tok + o * K;
+                for (int j = 0; j < K; ++j) rank += (key[b + j] > k) ? 1 : 0;
+            }
+            if (rank < K) {
+                sel[tt * K + rank] = s;
+                a.idx[tok * K + rank] = e;
+                atomicAdd(&hist[e], 1);
+            }
         }
         __syncthreads();
-        for (int t = tid; t < ntok; t += kMergeThreads) {
-            const int base = t * per_tok;
-            int head[kMaxSlices];
-#pragma unroll
-            for (int s = 0; s < kMaxSlices; ++s) head[s] = 0;
-            float sel_s[kMaxK];
-            const int64_t tok = tok_base + t;
-#pragma unroll
-            for (int r = 0; r < kMaxK; ++r) {
-                if (r < K) {
-                    float bv = -INFINITY, bs = 0.0f;
-                    int bi = 0x7fffffff, bsl = 0;
-#pragma unroll
-                    for (int s = 0; s < kMaxSlices; ++s) {
-                        if (s < NS && head[s] < K) {
-                            const int o = base + s * K + head[s];
-                            if (ranks_above(cv[o], ci[o], bv, bi)) {
-                                bv = cv[o];
-                                bi = ci[o];
-                                bs = cs[o];
-                                bsl = s;
-                            }
-                        }
-                    }
-#pragma unroll
-                    for (int s = 0; s < kMaxSlices; ++s) head[s] += (s == bsl) ? 1 : 0;
-                    sel_s[r] = bs;
-                    a.idx[tok * K + r] = bi;
-                    if ((unsigned)bi < (unsigned)E) atomicAdd(&hist[bi], 1);
-                }
-            }
+        if (act && rank < K) {
+            // den: fp32 sum of the selected unbiased scores in rank order
             float den = 0.0f;
-#pragma unroll
-            for (int r = 0; r < kMaxK; ++r)
-                if (r < K) den = den + sel_s[r];
-#pragma unroll
-            for (int r = 0; r < kMaxK; ++r)
-                if (r < K) a.w[tok * K + r] = (den == 0.0f) ? 1.0f / (float)K : sel_s[r] / den;
+            for (int j = 0; j < K; ++j) den = den + sel[tt * K + j];
+            a.w[tok * K + rank] = (den == 0.0f) ? 1.0f / (float)K : s / den;
         }
     }
     __syncthreads();
@@ -649,14 +612,10 @@ hipError_t launch_router_score_select(const RouterTiling& t, const RouterArgs& a
 hipError_t launch_router_merge(const RouterTiling& t, const RouterArgs& a, hipStream_t stream) {
     const int NS = router_slices(t, a.E);
     if (NS <= 1) return hipSuccess;
-    const int per_tok_bytes = NS * a.K * 12;
-    int tpw = 49152 / per_tok_bytes;
-    tpw = tpw > 256 ? 256 : tpw;
-    tpw = tpw < 1 ? 1 : tpw;
-    int64_t blocks = (a.T + tpw - 1) / tpw;
-    if (blocks > 1024) blocks = 1024;
-    const size_t lds = 4096 + (size_t)tpw * per_tok_bytes;
-    hipLaunchKernelGGL(router_merge_kernel, dim3((unsigned)blocks), dim3(kMergeThreads), lds, stream, a, NS, tpw);
+    const int tpg = kMergeThreads / (NS * a.K);
+    int64_t groups = (a.T + tpg - 1) / tpg;
+    if (groups > kMergeBlocks) groups = kMergeBlocks;
+    hipLaunchKernelGGL(router_merge_kernel, dim3((unsigned)groups), dim3(kMergeThreads), 0, stream, a, NS);
     return hipGetLastError();
 }
 

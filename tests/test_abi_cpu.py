@@ -164,3 +164,17 @@ def test_status_strings():
     for s in range(5):
         assert B.idb_status_string(s) != "unknown status"
     assert B.idb_status_string(42) == "unknown status"
+
+
+def test_binding_rejects_short_score_dump():
+    # host-side check before any pointer is taken: the dump must hold T*E floats
+    import torch
+    T, d, E, K = 64, 256, 64, 4
+    x = torch.zeros((T, d), dtype=torch.bfloat16)
+    W = torch.zeros((E, d), dtype=torch.bfloat16)
+    b = torch.zeros(E, dtype=torch.float32)
+    idx = torch.zeros((T, K), dtype=torch.int32)
+    w = torch.zeros((T, K), dtype=torch.float32)
+    c = torch.zeros(E, dtype=torch.int32)
+    with pytest.raises(ValueError, match="scores_dump"):
+        B.idb_router_forward(x, W, b, K, idx, w, c, scores_dump=torch.zeros(T * E // 2, dtype=torch.float32))

@@ -187,6 +187,22 @@ def test_edge_shapes(T, E, K):
     check_against_oracle(x, W, b, K, idx, w, c, s, max_uncertain=0.02)
 
 
+@pytest.mark.parametrize("E,K,variant", [(1024, 32, 4), (1024, 17, 3), (800, 10, 4), (768, 16, 1), (768, 32, 1)])
+def test_many_slices_and_large_k(E, K, variant):
+    # up to 8 expert slices merged, K above the threshold path's 16 (every
+    # list takes the per-token fallback), and E not a multiple of the slice
+    T, d = 300, 256
+    x, W = synth.normal_router_inputs(T, d, E, seed=E + K, w_std=0.05)
+    b = synth.bias(E, "small", seed=K)
+    idx, w, c, s = run_router(x, W, b, K, variant=variant)
+    check_invariants(idx, w, c, T, E, K)
+    si, sw, sc = gpu_select(s, b, K)
+    np.testing.assert_array_equal(idx, si)
+    np.testing.assert_array_equal(w.view(np.uint32), sw.view(np.uint32))
+    np.testing.assert_array_equal(c, sc)
+    check_against_oracle(x, W, b, K, idx, w, c, s, max_uncertain=0.02)
+
+
 def test_tied_scores_fall_back_exactly():
     # identical tokens and a zero router matrix: every score is 0.5, every
     # token picks experts 0..K-1 (all candidate lists overflow).
