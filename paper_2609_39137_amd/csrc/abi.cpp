@@ -49,14 +49,14 @@ idb_status resolve_tiling(int32_t E, idb_dtype dtype, int32_t variant, idb::Rout
         *out = t;
         return IDB_OK;
     }
-    // Automatic: among the multi-wave tilings of this dtype (ids 1, 3, 4, 5),
-    // the fewest padded experts, then the widest slice.
+    // Automatic: among the tilings of this dtype, the fewest padded experts,
+    // then the widest slice (fewer slices to merge).
     bool found = false;
     idb::RouterTiling best{};
     long best_waste = 0;
     for (int i = 0; i < n; ++i) {
         idb::RouterTiling t = idb::router_tiling(i);
-        if (t.is_f32 != want_f32 || t.id == 2) continue;
+        if (t.is_f32 != want_f32) continue;
         const int ns = idb::router_slices(t, E);
         if (ns > kMaxSlices) continue;
         const long be = (long)t.waves * t.nblk * 32;
@@ -75,6 +75,8 @@ idb_status resolve_tiling(int32_t E, idb_dtype dtype, int32_t variant, idb::Rout
 idb_status check_router_shape(int64_t T, int32_t d, int32_t E, int32_t K, idb_dtype dtype) {
     if (dtype != IDB_DTYPE_BF16 && dtype != IDB_DTYPE_F32) return fail(IDB_ERR_INVALID_ARG, "unknown dtype %d", dtype);
     if (T < 1 || T > kMaxTokens) return fail(IDB_ERR_INVALID_ARG, "T=%lld out of [1, 2^26]", (long long)T);
+    // d <= 65536 and E <= 1024 keep every operand byte offset of the fused
+    // kernel (at most E * d * 4 = 2^28) inside its 32-bit buffer addressing.
     if (d < 1 || d > 65536) return fail(IDB_ERR_INVALID_ARG, "d=%d out of [1, 65536]", d);
     if (E < 1 || K < 1 || K > E) return fail(IDB_ERR_INVALID_ARG, "need 1 <= K <= E (K=%d, E=%d)", K, E);
     if (E > kMaxExperts) return fail(IDB_ERR_UNSUPPORTED, "E=%d above %d", E, kMaxExperts);

@@ -62,17 +62,20 @@ __device__ __forceinline__ float row16_sorted_ascending_at(float x, int r) {
     return __shfl(x, r, 16);
 }
 
-// Sort 16 register values ascending in place (fixed bitonic network).
-__device__ __forceinline__ void sort16_ascending(float (&a)[16]) {
+// Sort N (a power of two) register values ascending in place (fixed bitonic
+// network).
+template <int N>
+__device__ __forceinline__ void sort_ascending(float (&a)[N]) {
+    static_assert((N & (N - 1)) == 0, "bitonic network needs a power of two");
 #pragma unroll
-    for (int k = 2; k <= 16; k <<= 1) {
+    for (int k = 2; k <= N; k <<= 1) {
 #pragma unroll
         for (int j = k >> 1; j > 0; j >>= 1) {
 #pragma unroll
-            for (int i = 0; i < 16; ++i) {
-                int l = i ^ j;
+            for (int i = 0; i < N; ++i) {
+                const int l = i ^ j;
                 if (l > i) {
-                    float lo = fminf(a[i], a[l]), hi = fmaxf(a[i], a[l]);
+                    const float lo = fminf(a[i], a[l]), hi = fmaxf(a[i], a[l]);
                     if ((i & k) == 0) {
                         a[i] = lo;
                         a[l] = hi;
@@ -87,6 +90,16 @@ __device__ __forceinline__ void sort16_ascending(float (&a)[16]) {
 }
 
 __device__ __forceinline__ uint4 ld16(const void* p) { return *reinterpret_cast<const uint4*>(p); }
+
+// Raw buffer resource over [base, base + bytes) (bytes < 2^32) and a 16-byte
+// load at per-lane offset voff plus scalar offset soff.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, int64_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, (int)bytes, 0x00020000);
+}
+__device__ __forceinline__ uint4 bload16(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
+    const auto v = __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0);
+    return make_uint4(v[0], v[1], v[2], v[3]);
+}
 
 __device__ __forceinline__ bf16x8 as_bf16x8(uint4 u) { return __builtin_bit_cast(bf16x8, u); }
 

@@ -29,14 +29,14 @@
 // are written token-major into LDS (the contraction's staging area is free by
 // then); TPT adjacent threads then own one token, VPT contiguous experts each.
 //   A. s = sigmoid(z) into the LDS score matrix (padding experts: -inf).
-//   B. v = fl32(s + b) into registers; 16 group maxima per token.
+//   B. v = fl32(s + b) into registers; 32 group maxima per token.
 //   C. tau = the K-th largest group maximum, <= the token's K-th largest v;
 //      each thread marks its values >= tau in a bitmask and counts them.
 //   D. A prefix over the token's threads gives write offsets; the candidates
 //      (typically about K + 5) go to an LDS list as 64-bit rank keys.
 //   E. Candidate rank = number of list keys above it; ranks < K are the
 //      slice's selection, in rank order.
-//   F. Tokens whose list would overflow (heavy ties, K > 16) are resolved by
+//   F. Tokens whose list would overflow (heavy ties, large K) are resolved by
 //      one wave each: K rounds of "best key strictly below the previous pick"
 //      over the token's LDS score row.
 //   G. One slice: gate weights, outputs and an LDS histogram flushed with one
@@ -73,11 +73,15 @@ struct Cfg {
     static constexpr int TPP = 32 * PB;
     static constexpr int NPASS = TBW / PB;
     static constexpr int TPT = NT / TPP;
-    static constexpr int VPT = BE / TPT;  // slice columns per thread
-    static constexpr int GPT = 16 / TPT;  // group maxima per thread
+    static constexpr int VPT = BE / TPT;  // slice columns per thread: every TPT-th 16-column block
+    static constexpr int NBL = VPT / 16;  // 16-column blocks per thread
+    static constexpr int NG = 32;         // group maxima per token
+    static constexpr int GPT = NG / TPT;  // group maxima per thread
     static constexpr int GSZ = VPT / GPT;
     static constexpr int MW = (VPT + 31) / 32;  // candidate mask words
-    static constexpr int GMS = 20;              // group-maximum row stride (words, 16-byte aligned)
+    static constexpr int NCI = (kCap + TPT - 1) / TPT;  // list entries ranked per thread
+    static constexpr int NBIAS = (BE + NT - 1) / NT;    // bias values staged per thread
+    static constexpr int GMS = NG + 4;          // group-maximum row stride (words, 16-byte aligned)
     static constexpr int CNS = TPT + 1;         // count row stride
     static constexpr int LKS = kCap + 2;        // candidate-key row stride (8-byte keys)
     static constexpr int LSS = kMaxK + 4;       // selection row stride
@@ -87,14 +91,13 @@ struct Cfg {
     static constexpr int OFF_CNT = OFF_GM + TPP * GMS * 4;
     static constexpr int OFF_LK = (OFF_CNT + TPP * CNS * 4 + 15) / 16 * 16;
     static constexpr int OFF_SI = OFF_LK + TPP * LKS * 8;
-    static constexpr int OFF_SS = OFF_SI + TPP * LSS * 4;
-    static constexpr int OFF_OVF = OFF_SS + TPP * LSS * 4;
+    static constexpr int OFF_OVF = OFF_SI + TPP * LSS * 4;
     static constexpr int OFF_HIST = OFF_OVF + 16 * 4;
     static constexpr int EPI_LDS = OFF_HIST + 1024 * 4;
     static constexpr int LDS = MAIN_LDS > EPI_LDS ? MAIN_LDS : EPI_LDS;
     static_assert(PPT * NT == BT * 8, "token-tile pieces must split evenly over threads");
     static_assert(TPT * TPP == NT && TPT <= 16 && 16 % TPT == 0, "a token's threads share one wave");
-    static_assert(VPT * TPT == BE && VPT % 4 == 0 && GSZ * GPT == VPT, "columns split evenly");
+    static_assert(VPT * TPT == BE && VPT % 16 == 0 && GSZ * GPT == VPT && GPT * TPT == NG, "columns split evenly");
     static_assert(TPP <= 16 * 32, "overflow bitmask size");
     static_assert(LDS <= 160 * 1024, "LDS of one workgroup");
 };
@@ -125,7 +128,7 @@ __global__ __launch_bounds__(WAVES * 64) void router_score_select_kernel(RouterA
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int wave = tid >> 6;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: keep it scalar
     const int h = lane >> 5;
     const int l32 = lane & 31;
 
@@ -149,31 +152,49 @@ __global__ __launch_bounds__(WAVES * 64) void router_score_select_kernel(RouterA
     if (a.zero_counts && blockIdx.x == 0)
         for (int e = tid; e < E; e += C::NT) a.counts[e] = 0;
 
+    // The slice's bias, fetched now (it arrives during the contraction) and
+    // moved to LDS by the epilogue.
+    const int sbase = slice * C::BE;  // first expert of the slice
+    float breg[C::NBIAS];
+#pragma unroll
+    for (int i = 0; i < C::NBIAS; ++i) {
+        const int c = tid + C::NT * i;
+        breg[i] = (c < C::BE && sbase + c < E) ? a.bias[sbase + c] : 0.0f;
+    }
+
     // ---------------------------------------------------------------- contraction
-    // A operands (router rows): byte strides of a chunk and of a unit.
+    // Operands are fetched with buffer loads: a scalar resource per operand
+    // and a 32-bit per-lane offset, with the chunk and block advance in the
+    // scalar offset, so the unrolled loads need no 64-bit address registers.
+    // Every load stays inside its resource by construction (the scalar offset
+    // is not range-checked).
+    //
+    // A operands (router rows): the per-lane offset and, per block, the
+    // block's scalar offset; a chunk adds WCH bytes, a unit WU.
     constexpr int WU = PACKED ? 1024 : 16;
-    constexpr int64_t WCH = PACKED ? 4096 : 128;
-    const char* wrow[NBLK];
+    constexpr int WCH = PACKED ? 4096 : 128;
+    const __amdgpu_buffer_rsrc_t wres = make_rsrc(a.W, (int64_t)E * RB);
+    const int wvoff = PACKED ? lane * 16 : l32 * (int)RB + 64 * h;
+    int wsoff[NBLK];
 #pragma unroll
     for (int nbk = 0; nbk < NBLK; ++nbk) {
         int blk = (e_wave0 + nbk * 32) / 32;
         blk = blk < E / 32 ? blk : E / 32 - 1;  // padding blocks read a valid block; masked later
-        if constexpr (PACKED)
-            wrow[nbk] = reinterpret_cast<const char*>(a.W) + (int64_t)blk * NCH * 4096 + lane * 16;
-        else
-            wrow[nbk] = reinterpret_cast<const char*>(a.W) + (int64_t)(blk * 32 + l32) * RB + 64 * h;
+        wsoff[nbk] = PACKED ? blk * NCH * 4096 : blk * 32 * (int)RB;
     }
     // Token-tile pieces: thread piece p = tid + NT*q covers row p/8, bytes
     // 16*(p%8) of the chunk.  Rows past T re-read row T-1 (never output).
-    const char* xsrc[C::PPT];
+    const int nrows = (int)((T - tok0) < C::BT ? (T - tok0) : C::BT);
+    const __amdgpu_buffer_rsrc_t xres =
+        make_rsrc(reinterpret_cast<const char*>(a.x) + tok0 * RB, (int64_t)nrows * RB);
+    int xvoff[C::PPT];
     int xdst[C::PPT];
 #pragma unroll
     for (int q = 0; q < C::PPT; ++q) {
         const int p = tid + C::NT * q;
         const int row = p >> 3, c16 = p & 7;
-        int64_t tok = tok0 + row;
-        tok = tok < T ? tok : T - 1;
-        xsrc[q] = reinterpret_cast<const char*>(a.x) + tok * RB + c16 * 16;
+        const int rowc = row < nrows ? row : nrows - 1;
+        xvoff[q] = rowc * (int)RB + c16 * 16;
         xdst[q] = row * kRowPad + c16 * 16;
     }
     const int boff = l32 * kRowPad + 64 * h;
@@ -192,13 +213,17 @@ __global__ __launch_bounds__(WAVES * 64) void router_score_select_kernel(RouterA
     // registers; the top of chunk c loads chunk c+2 into the set that held
     // chunk c, and the end of chunk c stores chunk c+1 (loaded a whole chunk
     // earlier) into the idle LDS stage.  Every fetch thus has about two
-    // chunks of MFMA work to arrive.  Vector-memory loads complete in order,
-    // and in this issue order each wait the compiler inserts covers only the
-    // data about to be used.
+    // chunks of MFMA work to arrive.
+    //
+    // The loop body is branch-free so that the compiler's vector-memory wait
+    // counts stay exact (loads complete in order; a conditional load would
+    // make every later wait drain the queue): prefetch targets are clamped
+    // to the last chunk (a cached re-read at the end), the last store goes to
+    // a stage that is never read, and an odd last chunk is peeled.
     uint4 w[2][NBLK][4], xr[2][C::PPT];
     auto load_x = [&](int c, int j) {
 #pragma unroll
-        for (int q = 0; q < C::PPT; ++q) xr[j][q] = ld16(xsrc[q] + c * 128);
+        for (int q = 0; q < C::PPT; ++q) xr[j][q] = bload16(xres, xvoff[q], c * 128);
     };
     auto store_x = [&](int stage, int j) {
 #pragma unroll
@@ -208,46 +233,49 @@ __global__ __launch_bounds__(WAVES * 64) void router_score_select_kernel(RouterA
 #pragma unroll
         for (int nbk = 0; nbk < NBLK; ++nbk)
 #pragma unroll
-            for (int u = 0; u < 4; ++u) w[j][nbk][u] = ld16(wrow[nbk] + c * WCH + WU * u);
+            for (int u = 0; u < 4; ++u) w[j][nbk][u] = bload16(wres, wvoff + WU * u, wsoff[nbk] + c * WCH);
+    };
+    // MFMAs of one chunk from LDS stage / W set j; with prefetch, each W unit
+    // is refilled from chunk cn right after its MFMAs.
+    auto compute = [&](int j, bool prefetch, int cn) {
+        const unsigned char* st = smem + j * C::STAGE + boff;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            uint4 bx[TBW];
+#pragma unroll
+            for (int tb = 0; tb < TBW; ++tb) bx[tb] = *reinterpret_cast<const uint4*>(st + tb * 32 * kRowPad + 16 * u);
+#pragma unroll
+            for (int tb = 0; tb < TBW; ++tb)
+#pragma unroll
+                for (int nbk = 0; nbk < NBLK; ++nbk) acc[tb][nbk] = mfma_unit<F32>(w[j][nbk][u], bx[tb], acc[tb][nbk]);
+            if (prefetch) {
+#pragma unroll
+                for (int nbk = 0; nbk < NBLK; ++nbk) w[j][nbk][u] = bload16(wres, wvoff + WU * u, wsoff[nbk] + cn * WCH);
+            }
+        }
     };
 
+    const int last = NCH - 1;
     load_x(0, 0);
     load_w(0, 0);
-    if (NCH > 1) {
-        load_x(1, 1);
-        load_w(1, 1);
-    }
+    load_x(last < 1 ? last : 1, 1);
+    load_w(last < 1 ? last : 1, 1);
     store_x(0, 0);
     __syncthreads();
-    for (int c0 = 0; c0 < NCH; c0 += 2) {
+    for (int c0 = 0; c0 + 1 < NCH; c0 += 2) {
 #pragma unroll
         for (int j = 0; j < 2; ++j) {
             const int c = c0 + j;
-            if (c < NCH) {
-                const bool more2 = c + 2 < NCH;
-                if (more2) load_x(c + 2, j);
-                const unsigned char* st = smem + j * C::STAGE + boff;
-#pragma unroll
-                for (int u = 0; u < 4; ++u) {
-                    uint4 bx[TBW];
-#pragma unroll
-                    for (int tb = 0; tb < TBW; ++tb)
-                        bx[tb] = *reinterpret_cast<const uint4*>(st + tb * 32 * kRowPad + 16 * u);
-#pragma unroll
-                    for (int tb = 0; tb < TBW; ++tb)
-#pragma unroll
-                        for (int nbk = 0; nbk < NBLK; ++nbk)
-                            acc[tb][nbk] = mfma_unit<F32>(w[j][nbk][u], bx[tb], acc[tb][nbk]);
-                    if (more2) {
-#pragma unroll
-                        for (int nbk = 0; nbk < NBLK; ++nbk)
-                            w[j][nbk][u] = ld16(wrow[nbk] + (c + 2) * WCH + WU * u);
-                    }
-                }
-                if (c + 1 < NCH) store_x(1 - j, 1 - j);
-                __syncthreads();
-            }
+            const int cn = c + 2 < last ? c + 2 : last;
+            load_x(cn, j);
+            compute(j, true, cn);
+            store_x(1 - j, 1 - j);
+            __syncthreads();
         }
+    }
+    if (NCH & 1) {
+        compute(0, false, 0);
+        __syncthreads();
     }
 
     // ---------------------------------------------------------------- epilogue
@@ -257,27 +285,32 @@ __global__ __launch_bounds__(WAVES * 64) void router_score_select_kernel(RouterA
     int* cnt = reinterpret_cast<int*>(smem + C::OFF_CNT);
     unsigned long long* lk = reinterpret_cast<unsigned long long*>(smem + C::OFF_LK);
     int* si = reinterpret_cast<int*>(smem + C::OFF_SI);
-    float* ss = reinterpret_cast<float*>(smem + C::OFF_SS);
     unsigned* ovf = reinterpret_cast<unsigned*>(smem + C::OFF_OVF);
     int* hist = reinterpret_cast<int*>(smem + C::OFF_HIST);
 
     // The contraction ended with a barrier, so its staging area is free.
-    const int sbase = slice * C::BE;  // first expert of the slice
-    for (int c = tid; c < C::BE; c += C::NT) bias_s[c] = (sbase + c < E) ? a.bias[sbase + c] : 0.0f;
+#pragma unroll
+    for (int i = 0; i < C::NBIAS; ++i) {
+        const int c = tid + C::NT * i;
+        if (c < C::BE) bias_s[c] = breg[i];
+    }
     for (int e = tid; e < 1024; e += C::NT) hist[e] = 0;
 
     // Slice column of accumulator (nbk, r): ccol + 32 nbk + 8 (r/4) + (r%4).
     // E is a multiple of 32, so a whole 32-expert block is real or padding.
     const int ccol = wave * C::WE + 4 * h;
     const int tl = tid / C::TPT, q = tid % C::TPT;  // token of the pass and part, in steps B-G
-    const int c0 = q * C::VPT;                       // this thread's first slice column
-    unsigned valid[C::MW];                           // columns that are real experts
+    // This thread's value j sits in slice column col(j) = 16 (q + TPT (j/16)) + j%16.
+    auto col_of = [&](int j) { return 16 * (q + C::TPT * (j >> 4)) + (j & 15); };
+    unsigned valid[C::MW];  // bit j: column j is a real expert
     {
-        const int nreal = E - sbase - c0;  // may be <= 0 or >= VPT
 #pragma unroll
-        for (int w = 0; w < C::MW; ++w) {
-            const int b = nreal - 32 * w;
-            valid[w] = b >= 32 ? ~0u : (b <= 0 ? 0u : ((1u << b) - 1u));
+        for (int w = 0; w < C::MW; ++w) valid[w] = 0u;
+#pragma unroll
+        for (int m = 0; m < C::NBL; ++m) {
+            const int nreal = E - sbase - 16 * (q + C::TPT * m);  // may be <= 0 or >= 16
+            const unsigned bits = nreal >= 16 ? 0xffffu : (nreal <= 0 ? 0u : ((1u << nreal) - 1u));
+            valid[m >> 1] |= bits << (16 * (m & 1));
         }
     }
 
@@ -312,41 +345,54 @@ __global__ __launch_bounds__(WAVES * 64) void router_score_select_kernel(RouterA
         // B. biased values of this thread's columns; group maxima
         float v[C::VPT];
 #pragma unroll
-        for (int j4 = 0; j4 < C::VPT / 4; ++j4) {
-            const float4 s4 = *reinterpret_cast<const float4*>(sc + tl * C::RS + c0 + 4 * j4);
-            const float4 b4 = *reinterpret_cast<const float4*>(bias_s + c0 + 4 * j4);
-            v[4 * j4 + 0] = s4.x + b4.x;
-            v[4 * j4 + 1] = s4.y + b4.y;
-            v[4 * j4 + 2] = s4.z + b4.z;
-            v[4 * j4 + 3] = s4.w + b4.w;
-        }
+        for (int m = 0; m < C::NBL; ++m)
+#pragma unroll
+            for (int i4 = 0; i4 < 4; ++i4) {
+                const int col = 16 * (q + C::TPT * m) + 4 * i4;
+                const float4 s4 = *reinterpret_cast<const float4*>(sc + tl * C::RS + col);
+                const float4 b4 = *reinterpret_cast<const float4*>(bias_s + col);
+                const int j = 16 * m + 4 * i4;
+                v[j + 0] = s4.x + b4.x;
+                v[j + 1] = s4.y + b4.y;
+                v[j + 2] = s4.z + b4.z;
+                v[j + 3] = s4.w + b4.w;
+            }
+        float own[C::GPT];
 #pragma unroll
         for (int g = 0; g < C::GPT; ++g) {
-            float m = -INFINITY;
+            float mx = -INFINITY;
 #pragma unroll
-            for (int j = 0; j < C::GSZ; ++j) m = fmaxf(m, v[g * C::GSZ + j]);
-            gm[tl * C::GMS + q * C::GPT + g] = m;
+            for (int j = 0; j < C::GSZ; ++j) mx = fmaxf(mx, v[g * C::GSZ + j]);
+            own[g] = mx;
+            gm[tl * C::GMS + q * C::GPT + g] = mx;
         }
         __syncthreads();
 
         // C. threshold; candidate masks and counts
+        // tau = the K-th largest of the token's 32 group maxima, i.e. the
+        // largest maximum m with #{maxima >= m} >= K (K <= 32): each thread
+        // tests its own maxima against all 32, a max over the token's lanes
+        // combines them.
         float tau = -INFINITY;
         {
-            float g16[16];
+            float g[C::NG];
 #pragma unroll
-            for (int i4 = 0; i4 < 4; ++i4) {
+            for (int i4 = 0; i4 < C::NG / 4; ++i4) {
                 const float4 t4 = *reinterpret_cast<const float4*>(gm + tl * C::GMS + 4 * i4);
-                g16[4 * i4 + 0] = t4.x;
-                g16[4 * i4 + 1] = t4.y;
-                g16[4 * i4 + 2] = t4.z;
-                g16[4 * i4 + 3] = t4.w;
+                g[4 * i4 + 0] = t4.x;
+                g[4 * i4 + 1] = t4.y;
+                g[4 * i4 + 2] = t4.z;
+                g[4 * i4 + 3] = t4.w;
             }
-            sort16_ascending(g16);
-            if (K <= 16) {
 #pragma unroll
-                for (int i = 0; i < 16; ++i)
-                    if (i == 16 - K) tau = g16[i];
+            for (int i = 0; i < C::GPT; ++i) {
+                int ge = 0;
+#pragma unroll
+                for (int j = 0; j < C::NG; ++j) ge += (g[j] >= own[i]) ? 1 : 0;
+                if (ge >= K) tau = fmaxf(tau, own[i]);
             }
+#pragma unroll
+            for (int o = 1; o < C::TPT; o <<= 1) tau = fmaxf(tau, __shfl_xor(tau, o));
         }
         // Bit j: v_j >= tau, read off the sign of v_j - tau (a difference of
         // two finite floats is +0 only when they are equal, and -inf - tau is
@@ -358,13 +404,13 @@ __global__ __launch_bounds__(WAVES * 64) void router_score_select_kernel(RouterA
 #pragma unroll
         for (int j = 0; j < C::VPT; ++j)
             msk[j / 32] |= ((__float_as_uint(v[j] - tau) >> 31) ^ 1u) << (j % 32);
-        int own = 0;
+        int mine_n = 0;
 #pragma unroll
         for (int w = 0; w < C::MW; ++w) {
             msk[w] &= valid[w];
-            own += __builtin_popcount(msk[w]);
+            mine_n += __builtin_popcount(msk[w]);
         }
-        cnt[tl * C::CNS + q] = own;
+        cnt[tl * C::CNS + q] = mine_n;
         __syncthreads();
 
         // D. write offsets; candidate keys into the token's list
@@ -383,7 +429,7 @@ __global__ __launch_bounds__(WAVES * 64) void router_score_select_kernel(RouterA
             for (int w = 0; w < C::MW; ++w) {
                 unsigned m = msk[w];
                 while (m) {
-                    const int col = c0 + w * 32 + __builtin_ctz(m);
+                    const int col = col_of(w * 32 + __builtin_ctz(m));
                     m &= m - 1u;
                     lk[tl * C::LKS + off] = rank_key(sc[tl * C::RS + col] + bias_s[col], sbase + col);
                     ++off;
@@ -392,29 +438,25 @@ __global__ __launch_bounds__(WAVES * 64) void router_score_select_kernel(RouterA
         }
         __syncthreads();
 
-        // E. ranks of the listed candidates (entries past n count as key 0)
+        // E. ranks of the listed candidates: thread q ranks entries q, q+TPT, ...
+        // against the n list keys, reading each list key once.
         if (listed) {
-            unsigned long long key[kCap];
+            unsigned long long mine[C::NCI];
+            int rank[C::NCI];
 #pragma unroll
-            for (int o2 = 0; o2 < kCap / 2; ++o2) {
-                const ulonglong2 k2 = *reinterpret_cast<const ulonglong2*>(lk + tl * C::LKS + 2 * o2);
-                key[2 * o2] = k2.x;
-                key[2 * o2 + 1] = k2.y;
+            for (int i = 0; i < C::NCI; ++i) {
+                const int c = q + C::TPT * i;
+                mine[i] = c < n ? lk[tl * C::LKS + c] : ~0ull;  // ~0: beyond the list, never written
+                rank[i] = 0;
+            }
+            for (int o = 0; o < n; ++o) {
+                const unsigned long long ko = lk[tl * C::LKS + o];
+#pragma unroll
+                for (int i = 0; i < C::NCI; ++i) rank[i] += (ko > mine[i]) ? 1 : 0;
             }
 #pragma unroll
-            for (int o = 0; o < kCap; ++o)
-                if (o >= n) key[o] = 0ull;
-            for (int c = q; c < n; c += C::TPT) {
-                const unsigned long long mine = lk[tl * C::LKS + c];
-                int rank = 0;
-#pragma unroll
-                for (int o = 0; o < kCap; ++o) rank += (key[o] > mine) ? 1 : 0;
-                if (rank < K) {
-                    const int e = (int)~(unsigned)mine;
-                    si[tl * C::LSS + rank] = e;
-                    ss[tl * C::LSS + rank] = sc[tl * C::RS + (e - sbase)];
-                }
-            }
+            for (int i = 0; i < C::NCI; ++i)
+                if (q + C::TPT * i < n && rank[i] < K) si[tl * C::LSS + rank[i]] = (int)~(unsigned)mine[i];
         }
 
         // F. overflowing tokens, one wave each (the bitmask is uniform: it was
@@ -444,18 +486,15 @@ __global__ __launch_bounds__(WAVES * 64) void router_score_select_kernel(RouterA
                             best = other > best ? other : best;
                         }
                         prev = best;
-                        if (lane == 0) {
-                            const int e = (int)~(unsigned)best;
-                            si[t * C::LSS + r] = e;
-                            ss[t * C::LSS + r] = sc[t * C::RS + (e - sbase)];
-                        }
+                        if (lane == 0) si[t * C::LSS + r] = (int)~(unsigned)best;
                     }
                 }
             }
         }
         __syncthreads();
 
-        // G. outputs of the pass's tokens
+        // G. outputs of the pass's tokens (selected scores read back from the
+        // token's LDS score row)
         {
             const int64_t tok = tok0 + pass * C::TPP + tl;
             if (tok < T) {
@@ -463,7 +502,7 @@ __global__ __launch_bounds__(WAVES * 64) void router_score_select_kernel(RouterA
                     const int64_t base = (tok * NS + slice) * K;
                     for (int r = q; r < K; r += C::TPT) {
                         const int e = si[tl * C::LSS + r];
-                        const float s = ss[tl * C::LSS + r];
+                        const float s = sc[tl * C::RS + (e - sbase)];
                         a.cand_v[base + r] = s + bias_s[e - sbase];
                         a.cand_s[base + r] = s;
                         a.cand_i[base + r] = e;
@@ -472,13 +511,12 @@ __global__ __launch_bounds__(WAVES * 64) void router_score_select_kernel(RouterA
                     // gate weights: den is the fp32 sum of the selected
                     // unbiased scores in rank order
                     float den = 0.0f;
-#pragma unroll
-                    for (int r = 0; r < kMaxK; ++r)
-                        if (r < K) den = den + ss[tl * C::LSS + r];
+                    for (int r = 0; r < K; ++r) den = den + sc[tl * C::RS + (si[tl * C::LSS + r] - sbase)];
                     for (int r = q; r < K; r += C::TPT) {
                         const int e = si[tl * C::LSS + r];
+                        const float s = sc[tl * C::RS + (e - sbase)];
                         a.idx[tok * K + r] = e;
-                        a.w[tok * K + r] = (den == 0.0f) ? 1.0f / (float)K : ss[tl * C::LSS + r] / den;
+                        a.w[tok * K + r] = (den == 0.0f) ? 1.0f / (float)K : s / den;
                         atomicAdd(&hist[e], 1);
                     }
                 }

@@ -52,8 +52,8 @@ def router(T=128, d=256, E=768, K=10, dtype=B.IDB_DTYPE_BF16, x=A16, W=A16, bias
     (dict(W=A16 + 8), B.IDB_ERR_INVALID_ARG),
     (dict(bias=A16 + 2), B.IDB_ERR_INVALID_ARG),
     (dict(dump=A16 + 4), B.IDB_ERR_INVALID_ARG),
-    (dict(ws=None), B.IDB_ERR_INVALID_ARG),
-    (dict(ws_bytes=16), B.IDB_ERR_INVALID_ARG),
+    (dict(ws=None, variant=1), B.IDB_ERR_INVALID_ARG),  # two slices: the workspace is required
+    (dict(ws_bytes=16, variant=1), B.IDB_ERR_INVALID_ARG),
     (dict(variant=99), B.IDB_ERR_INVALID_ARG),
     (dict(layout=2), B.IDB_ERR_INVALID_ARG),
     (dict(variant=5), B.IDB_ERR_UNSUPPORTED),   # the fp32 tiling asked for bf16 input
@@ -85,19 +85,19 @@ def test_merge_rejects_invalid_arguments():
     L = B.lib()
     assert L.idb_router_merge(0, 256, 768, 10, 0, A16, A16, A16, A16, 1 << 30, 0, None) == B.IDB_ERR_INVALID_ARG
     assert L.idb_router_merge(128, 256, 768, 10, 0, None, A16, A16, A16, 1 << 30, 0, None) == B.IDB_ERR_INVALID_ARG
-    assert L.idb_router_merge(128, 256, 768, 10, 0, A16, A16, A16, A16, 8, 0, None) == B.IDB_ERR_INVALID_ARG
+    assert L.idb_router_merge(128, 256, 768, 10, 0, A16, A16, A16, A16, 8, 1, None) == B.IDB_ERR_INVALID_ARG  # two slices
 
 
 def test_workspace_and_variant_info():
-    # 768 experts in bf16: the automatic tiling splits them into two 384-expert slices.
+    # 768 experts in bf16: the automatic tiling covers them in one 768-expert
+    # slice (8 waves, 64 tokens per workgroup) and needs no workspace.
     info = B.idb_router_variant_info(16384, 2048, 768, 10, B.IDB_DTYPE_BF16, 0)
-    assert info == {"tokens_per_wg": 128, "slices": 2, "waves": 4, "blocks_per_wave": 3, "variant": 1}
-    nbytes = B.idb_router_workspace_bytes(16384, 2048, 768, 10, B.IDB_DTYPE_BF16, 0)
-    assert nbytes == 3 * 16384 * 2 * 10 * 4
-    # a single-slice tiling needs no workspace
-    info2 = B.idb_router_variant_info(16384, 2048, 768, 10, B.IDB_DTYPE_BF16, 2)
-    assert info2["slices"] == 1 and info2["tokens_per_wg"] == 64
-    assert B.idb_router_workspace_bytes(16384, 2048, 768, 10, B.IDB_DTYPE_BF16, 2) == 0
+    assert info == {"tokens_per_wg": 64, "slices": 1, "waves": 8, "blocks_per_wave": 3, "variant": 2}
+    assert B.idb_router_workspace_bytes(16384, 2048, 768, 10, B.IDB_DTYPE_BF16, 0) == 0
+    # the two-slice tiling stages the slices' candidates in the workspace
+    info1 = B.idb_router_variant_info(16384, 2048, 768, 10, B.IDB_DTYPE_BF16, 1)
+    assert info1["slices"] == 2 and info1["tokens_per_wg"] == 128
+    assert B.idb_router_workspace_bytes(16384, 2048, 768, 10, B.IDB_DTYPE_BF16, 1) == 3 * 16384 * 2 * 10 * 4
     # fp32 input, 64 experts: one 128-expert slice, half padding
     info3 = B.idb_router_variant_info(4096, 256, 64, 4, B.IDB_DTYPE_F32, 0)
     assert info3["slices"] == 1 and info3["variant"] == 5
