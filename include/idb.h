@@ -113,8 +113,11 @@ typedef struct idb_controller_state {
  *               selection used (debug / parity; the arithmetic is unchanged).
  *   workspace   device scratch of at least idb_router_workspace_bytes().
  *   variant     0 = automatic tiling; other values force a tiling (see
- *               idb_router_variant_info).  Every variant gives identical
- *               outputs.
+ *               idb_router_variant_info).  Variants 1-5 (32x32 MFMA tiles)
+ *               give identical outputs; variant 6 (16x16 tiles) accumulates
+ *               the contraction in another order, so its scores can differ
+ *               in the last fp32 bits.  Given its scores, every variant's
+ *               selection, gate weights and counts are exact.
  * The T x E score matrix is never written to memory unless scores_dump is set.
  * ------------------------------------------------------------------------- */
 size_t idb_router_workspace_bytes(int64_t T, int32_t d, int32_t E, int32_t K, idb_dtype dtype, int32_t variant);
@@ -144,19 +147,20 @@ idb_status idb_router_merge(int64_t T, int32_t d, int32_t E, int32_t K, idb_dtyp
                             int32_t variant, hipStream_t stream);
 
 /* The router matrix in the layout the MFMA A operands are read in: for every
- * 32-expert block b, 128-byte chunk c of the rows and 16-byte unit u < 4, one
- * contiguous 1 KB piece holds, for lane l = 32 h + m (h < 2, m < 32), bytes
- * [c*128 + 64 h + 16 u, +16) of row 32 b + m.  A pure byte permutation of
- * W_g; packing once per weight update lets every router call read W with
- * fully coalesced loads.  W_packed must not overlap W_g; both 16-byte aligned.
- * E % 32 == 0, d as for idb_router_forward. */
+ * 16-expert block b, 128-byte chunk c of the rows and 64-byte half s < 2 of
+ * the chunk, one contiguous 1 KB piece, at byte ((b*NCH + c)*2 + s)*1024 with
+ * NCH = row bytes / 128, holds for lane slot l < 64 the bytes
+ * [c*128 + 64 s + 16 (l/16), +16) of row 16 b + l%16.  A pure byte
+ * permutation of W_g; packing once per weight update lets every router call
+ * read W with fully coalesced loads.  W_packed must not overlap W_g; both
+ * 16-byte aligned.  E % 32 == 0, d as for idb_router_forward. */
 size_t idb_router_packed_weight_bytes(int32_t E, int32_t d, idb_dtype dtype);
 idb_status idb_router_pack_weight(const void* W_g, idb_dtype dtype, int32_t E, int32_t d, void* W_packed,
                                   hipStream_t stream);
 
 /* Tiling of a variant for a shape: out[0] = tokens per workgroup, out[1] =
- * expert slices, out[2] = waves per workgroup, out[3] = 32-expert blocks per
- * wave, out[4] = resolved variant id.  Returns IDB_ERR_UNSUPPORTED when the
+ * expert slices, out[2] = waves per workgroup, out[3] = experts per wave,
+ * out[4] = resolved variant id.  Returns IDB_ERR_UNSUPPORTED when the
  * variant cannot run the shape.  Host only, no HIP call. */
 idb_status idb_router_variant_info(int64_t T, int32_t d, int32_t E, int32_t K, idb_dtype dtype, int32_t variant,
                                    int32_t out[5]);
@@ -197,6 +201,13 @@ idb_status idb_controller_update(const int32_t* counts, const idb_controller_cfg
  * out is a device double[2].
  * ------------------------------------------------------------------------- */
 idb_status idb_load_stats(const int32_t* counts, int32_t E, double* out_maxvio_minvio, hipStream_t stream);
+
+/* One launch for both calls of an iteration's controller phase: writes
+ * MaxVio/MinVio of counts into out_maxvio_minvio (exactly as idb_load_stats)
+ * and applies the ID update (exactly as idb_controller_update), on stream.
+ * Same argument rules as the two calls; out_maxvio_minvio must not be null. */
+idb_status idb_controller_step(const int32_t* counts, const idb_controller_cfg* cfg,
+                               const idb_controller_state* state, double* out_maxvio_minvio, hipStream_t stream);
 
 /* Static description of a status code; message of the last failing call on
  * this thread (empty string if none). */

@@ -33,6 +33,7 @@ EXPORTED = (
     "idb_router_workspace_bytes", "idb_router_forward", "idb_router_score_select", "idb_router_merge",
     "idb_router_variant_info", "idb_select_from_scores", "idb_controller_update", "idb_load_stats",
     "idb_status_string", "idb_last_error", "idb_router_packed_weight_bytes", "idb_router_pack_weight",
+    "idb_controller_step",
 )
 
 
@@ -84,6 +85,9 @@ def lib() -> ctypes.CDLL:
     L.idb_controller_update.restype = ctypes.c_int
     L.idb_load_stats.argtypes = [P, i32, P, P]
     L.idb_load_stats.restype = ctypes.c_int
+    L.idb_controller_step.argtypes = [P, ctypes.POINTER(idb_controller_cfg), ctypes.POINTER(idb_controller_state), P,
+                                      P]
+    L.idb_controller_step.restype = ctypes.c_int
     L.idb_status_string.argtypes = [ctypes.c_int]
     L.idb_status_string.restype = ctypes.c_char_p
     L.idb_last_error.argtypes = []
@@ -137,7 +141,7 @@ def idb_router_workspace_bytes(T: int, d: int, E: int, K: int, dtype: int, varia
 def idb_router_variant_info(T: int, d: int, E: int, K: int, dtype: int, variant: int = 0) -> dict:
     out = (ctypes.c_int32 * 5)()
     _check("idb_router_variant_info", lib().idb_router_variant_info(T, d, E, K, dtype, variant, out))
-    return {"tokens_per_wg": out[0], "slices": out[1], "waves": out[2], "blocks_per_wave": out[3], "variant": out[4]}
+    return {"tokens_per_wg": out[0], "slices": out[1], "waves": out[2], "experts_per_wave": out[3], "variant": out[4]}
 
 
 def idb_router_packed_weight_bytes(E: int, d: int, dtype: int) -> int:
@@ -244,3 +248,13 @@ def idb_load_stats(counts, out, stream=None):
         raise ValueError("out must be a float64 tensor of 2 elements")
     st = lib().idb_load_stats(_ptr(counts), counts.numel(), _ptr(out), _stream(stream))
     _check("idb_load_stats", st)
+
+
+def idb_controller_step(counts, cfg: ControllerCfg, state: ControllerState, out, stream=None):
+    """MaxVio/MinVio of ``counts`` into ``out`` and one ID update of ``state``, in one launch."""
+    if out.dtype != torch.float64 or out.numel() != 2:
+        raise ValueError("out must be a float64 tensor of 2 elements")
+    c_cfg, c_state = cfg.c(), state.c()
+    st = lib().idb_controller_step(_ptr(counts), ctypes.byref(c_cfg), ctypes.byref(c_state), _ptr(out),
+                                   _stream(stream))
+    _check("idb_controller_step", st)

@@ -50,7 +50,7 @@ idb_status resolve_tiling(int32_t E, idb_dtype dtype, int32_t variant, idb::Rout
         return IDB_OK;
     }
     // Automatic: among the tilings of this dtype, the fewest padded experts,
-    // then the widest slice (fewer slices to merge).
+    // then the preferred one (the ranking follows measured throughput).
     bool found = false;
     idb::RouterTiling best{};
     long best_waste = 0;
@@ -59,9 +59,8 @@ idb_status resolve_tiling(int32_t E, idb_dtype dtype, int32_t variant, idb::Rout
         if (t.is_f32 != want_f32) continue;
         const int ns = idb::router_slices(t, E);
         if (ns > kMaxSlices) continue;
-        const long be = (long)t.waves * t.nblk * 32;
-        const long waste = ns * be - E;
-        if (!found || waste < best_waste || (waste == best_waste && be > (long)best.waves * best.nblk * 32)) {
+        const long waste = (long)ns * t.waves * t.we - E;
+        if (!found || waste < best_waste || (waste == best_waste && t.rank < best.rank)) {
             best = t;
             best_waste = waste;
             found = true;
@@ -90,6 +89,7 @@ idb_status check_router_shape(int64_t T, int32_t d, int32_t E, int32_t K, idb_dt
 size_t router_ws_bytes(int64_t T, int32_t E, int32_t K, const idb::RouterTiling& t) {
     const int ns = idb::router_slices(t, E);
     if (ns <= 1) return 0;
+    // candidates (value, score, index) [T][ns][K]
     return 3 * round_up((size_t)T * ns * K * 4);
 }
 
@@ -176,10 +176,10 @@ idb_status idb_router_variant_info(int64_t T, int32_t d, int32_t E, int32_t K, i
     idb::RouterTiling t;
     st = resolve_tiling(E, dtype, variant, &t);
     if (st != IDB_OK) return st;
-    out[0] = 32 * t.tbw;
+    out[0] = t.bt;
     out[1] = idb::router_slices(t, E);
     out[2] = t.waves;
-    out[3] = t.nblk;
+    out[3] = t.we;
     out[4] = t.id;
     return IDB_OK;
 }
@@ -256,8 +256,9 @@ idb_status idb_select_from_scores(const float* scores, const float* bias, int64_
                       "select launch");
 }
 
-idb_status idb_controller_update(const int32_t* counts, const idb_controller_cfg* cfg,
-                                 const idb_controller_state* state, hipStream_t stream) {
+namespace {
+idb_status controller_call(const int32_t* counts, const idb_controller_cfg* cfg, const idb_controller_state* state,
+                           double* stats, hipStream_t stream) {
     if (!counts || !cfg || !state) return fail(IDB_ERR_INVALID_ARG, "null pointer");
     if (!state->bias || !state->e_prev || !state->step || !state->status)
         return fail(IDB_ERR_INVALID_ARG, "null state buffer");
@@ -268,12 +269,25 @@ idb_status idb_controller_update(const int32_t* counts, const idb_controller_cfg
         return fail(IDB_ERR_INVALID_ARG, "unknown integral mode %d", cfg->integral_mode);
     if (cfg->center != 0 && cfg->center != 1) return fail(IDB_ERR_INVALID_ARG, "center must be 0 or 1");
     if (!aligned(counts, 4) || !aligned(state->bias, 4) || !aligned(state->e_prev, 4) || !aligned(state->step, 8) ||
-        !aligned(state->status, 4))
+        !aligned(state->status, 4) || (stats && !aligned(stats, 8)))
         return fail(IDB_ERR_INVALID_ARG, "misaligned buffer");
     return hip_result(idb::launch_controller_update(counts, cfg->E, cfg->Ki, cfg->Kd,
                                                     cfg->integral_mode == IDB_INTEGRAL_SIGN, cfg->center,
-                                                    state->bias, state->e_prev, state->step, state->status, stream),
+                                                    state->bias, state->e_prev, state->step, state->status, stats,
+                                                    stream),
                       "controller launch");
+}
+}  // namespace
+
+idb_status idb_controller_update(const int32_t* counts, const idb_controller_cfg* cfg,
+                                 const idb_controller_state* state, hipStream_t stream) {
+    return controller_call(counts, cfg, state, nullptr, stream);
+}
+
+idb_status idb_controller_step(const int32_t* counts, const idb_controller_cfg* cfg,
+                               const idb_controller_state* state, double* out_maxvio_minvio, hipStream_t stream) {
+    if (!out_maxvio_minvio) return fail(IDB_ERR_INVALID_ARG, "null statistics output");
+    return controller_call(counts, cfg, state, out_maxvio_minvio, stream);
 }
 
 idb_status idb_load_stats(const int32_t* counts, int32_t E, double* out_maxvio_minvio, hipStream_t stream) {

@@ -9,6 +9,7 @@ namespace idb {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float floatx16 __attribute__((ext_vector_type(16)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
 
 // Device status codes (same values as idb_status in include/idb.h).
 constexpr int32_t kStatusOk = 0;

@@ -8,8 +8,9 @@
 
 namespace idb {
 
+// stats: nullable device double[2]; when set, MaxVio/MinVio of counts too.
 hipError_t launch_controller_update(const int32_t* counts, int E, float Ki, float Kd, int sign_mode, int center,
-                                    float* bias, float* e_prev, int64_t* step, int32_t* status,
+                                    float* bias, float* e_prev, int64_t* step, int32_t* status, double* stats,
                                     hipStream_t stream);
 hipError_t launch_load_stats(const int32_t* counts, int E, double* out, hipStream_t stream);
 
@@ -23,8 +24,9 @@ struct RouterTiling {
     int id;       // variant id (1-based)
     int is_f32;   // input dtype of this tiling
     int waves;    // waves per workgroup
-    int tbw;      // 32-token blocks per wave (tokens per workgroup = 32 * tbw)
-    int nblk;     // 32-expert blocks per wave
+    int bt;       // tokens per workgroup
+    int we;       // experts per wave (a workgroup's slice is waves * we experts)
+    int rank;     // preference among tilings with equally few padded experts (lower first)
 };
 
 // Number of known tilings and the i-th one (0-based).
@@ -53,7 +55,7 @@ struct RouterArgs {
 
 // Slices of E covered by one workgroup column for tiling t.
 inline int router_slices(const RouterTiling& t, int E) {
-    const int be = t.waves * t.nblk * 32;
+    const int be = t.waves * t.we;
     return (E + be - 1) / be;
 }
 

@@ -3,37 +3,46 @@
 // unbiased scores and per-expert load counts (Eq. pid-error).  The T x E score
 // matrix stays in registers and LDS.
 //
-// Tiling.  A workgroup owns BT = 32*TBW tokens and one slice of BE =
-// WAVES*32*NBLK experts.  Each wave owns all BT tokens and its own 32*NBLK
-// experts: its router rows are private to it and go straight from global
-// memory into MFMA A-operand registers, while the token tile is shared by the
-// waves through LDS.  The contraction runs over 128-byte chunks of each row.
-// Within a chunk, lane half h of every 32-lane group consumes bytes
-// [64h, 64h + 64) in four 16-byte units, identically for both operands, so the
-// k order agrees between them.
+// Tiling.  A workgroup owns BT tokens and one slice of BE experts; each wave
+// owns all BT tokens and its own WE = BE / WAVES experts.  The wave's router
+// rows are private to it and go straight from global memory into MFMA
+// A-operand registers; the token tile is shared by the waves through LDS.
+// The contraction runs over 128-byte chunks of each row.  Two contraction
+// kernels share the selection epilogue:
+//   - 32x32x16 tiles (router32_kernel): WE = 32 NBLK, BT = 32 TBW; also the
+//     fp32-input path (32x32x2 MFMAs).
+//   - 16x16x32 tiles (router16_kernel): WE = 16 ET, BT = 16 TT.  With 8 waves
+//     of 48 experts x 128 tokens each wave needs only 96 accumulators, so two
+//     waves share a SIMD while every router byte is still loaded once per
+//     workgroup.
+// In both, lanes of a wave consume the same k bytes of a chunk for both
+// operands, so the k order agrees between A and B.
 //
 // Token tile: staged through registers into two LDS stages of 144-byte rows
-// (128 bytes + 16 of padding, so the MFMA B-operand reads of 32 rows are free
-// of bank conflicts), loaded one chunk ahead of use.
+// (128 bytes + 16 of padding, so the B-operand reads are free of bank
+// conflicts), loaded two chunks ahead of use.
 //
-// Router matrix: either row-major [E][d] (each A-operand load touches 32 rows)
-// or the packed layout written by idb_router_pack_weight, in which the 64
-// lanes' 16-byte A operands of one (32-expert block, chunk, unit) are one
-// contiguous 1 KB piece.
+// Router matrix: either row-major [E][d] or the packed layout written by
+// idb_router_pack_weight: for every 16-expert block b, chunk c and 64-byte
+// half s of the chunk, one contiguous 1 KB piece holds, for lane l < 64, bytes
+// [c*128 + 64 s + 16 (l/16), +16) of row 16 b + l%16 (exactly one 16x16x32
+// A operand; a 32x32x16 A operand is four 256-byte runs of it).
 //
-// MFMA 32x32 output layout (C = W_block * x_block^T): lane l holds token
-// (l % 32) of the block and experts 8*(r/4) + 4*(l/32) + (r%4), r < 16.  So a
-// token's BE scores are spread over 2*WAVES lanes, 16*NBLK per lane.
+// MFMA output layouts (C = W_tile x_tile^T): 32x32 - lane l holds token l%32
+// of the block and experts 8 (r/4) + 4 (l/32) + r%4, r < 16; 16x16 - lane l
+// holds token l%16 of the tile and experts 4 (l/16) + r, r < 4.
 //
-// Epilogue (exact for any input).  The scores of PB token blocks at a time
-// are written token-major into LDS (the contraction's staging area is free by
-// then); TPT adjacent threads then own one token, VPT contiguous experts each.
-//   A. s = sigmoid(z) into the LDS score matrix (padding experts: -inf).
+// Epilogue (exact for any input).  The scores of TPP tokens at a time are
+// written token-major into LDS (the contraction's staging area is free by
+// then); TPT adjacent threads then own one token, each every TPT-th block of
+// 16 experts (so a wave's LDS reads of the score rows hit distinct banks).
+//   A. s = sigmoid(z) into the LDS score matrix (padding experts: -inf); this
+//      step is the contraction kernel's, as it depends on the MFMA layout.
 //   B. v = fl32(s + b) into registers; 32 group maxima per token.
 //   C. tau = the K-th largest group maximum, <= the token's K-th largest v;
 //      each thread marks its values >= tau in a bitmask and counts them.
 //   D. A prefix over the token's threads gives write offsets; the candidates
-//      (typically about K + 5) go to an LDS list as 64-bit rank keys.
+//      (typically about K + 2) go to an LDS list as 64-bit rank keys.
 //   E. Candidate rank = number of list keys above it; ranks < K are the
 //      slice's selection, in rank order.
 //   F. Tokens whose list would overflow (heavy ties, large K) are resolved by
@@ -51,40 +60,36 @@ namespace idb {
 
 namespace {
 
-constexpr int kCap = 32;     // candidate list capacity per token and slice
+constexpr int kCap = 32;      // candidate list capacity per token and slice
 constexpr int kRowPad = 144;  // LDS bytes per staged token row (128 + 16 pad)
 constexpr int kMaxSlices = 8;
-
 constexpr int kScoreLds = 100000;  // LDS budget of the epilogue's score matrix
 
-template <bool F32, int WAVES, int TBW, int NBLK>
-struct Cfg {
-    static constexpr int NT = WAVES * 64;
-    static constexpr int BT = 32 * TBW;
-    static constexpr int WE = 32 * NBLK;
-    static constexpr int BE = WAVES * WE;
-    static constexpr int PPT = BT * 8 / NT;  // 16-byte token-tile pieces per thread per chunk
-    static constexpr int STAGE = BT * kRowPad;
-    static constexpr int MAIN_LDS = 2 * STAGE;
-    // epilogue: PB token blocks (TPP tokens) per pass, TPT threads per token
+// Epilogue layout for NT threads, BT tokens, BE experts per workgroup; the
+// contraction's MAIN_LDS bytes of LDS are reused.
+template <int NT_, int BT_, int BE_, int MAIN_LDS_>
+struct EpiCfg {
+    static constexpr int NT = NT_;
+    static constexpr int BT = BT_;
+    static constexpr int BE = BE_;
     static constexpr int RS = BE + 4;  // score row stride in floats (odd number of 16-byte units)
-    static constexpr int PB = (TBW % 4 == 0 && 128 * RS * 4 <= kScoreLds) ? 4
-                              : ((TBW % 2 == 0 && 64 * RS * 4 <= kScoreLds) ? 2 : 1);
-    static constexpr int TPP = 32 * PB;
-    static constexpr int NPASS = TBW / PB;
+    // tokens per pass: the largest of BT, BT/2, BT/4 whose score rows fit
+    static constexpr int TPP = (BT * RS * 4 <= kScoreLds && BT <= NT) ? BT
+                               : ((BT / 2) * RS * 4 <= kScoreLds && BT / 2 <= NT) ? BT / 2 : BT / 4;
+    static constexpr int NPASS = BT / TPP;
     static constexpr int TPT = NT / TPP;
     static constexpr int VPT = BE / TPT;  // slice columns per thread: every TPT-th 16-column block
     static constexpr int NBL = VPT / 16;  // 16-column blocks per thread
     static constexpr int NG = 32;         // group maxima per token
     static constexpr int GPT = NG / TPT;  // group maxima per thread
     static constexpr int GSZ = VPT / GPT;
-    static constexpr int MW = (VPT + 31) / 32;  // candidate mask words
+    static constexpr int MW = (VPT + 31) / 32;          // candidate mask words
     static constexpr int NCI = (kCap + TPT - 1) / TPT;  // list entries ranked per thread
     static constexpr int NBIAS = (BE + NT - 1) / NT;    // bias values staged per thread
-    static constexpr int GMS = NG + 4;          // group-maximum row stride (words, 16-byte aligned)
-    static constexpr int CNS = TPT + 1;         // count row stride
-    static constexpr int LKS = kCap + 2;        // candidate-key row stride (8-byte keys)
-    static constexpr int LSS = kMaxK + 4;       // selection row stride
+    static constexpr int GMS = NG + 4;                  // group-maximum row stride (words, 16-byte aligned)
+    static constexpr int CNS = TPT + 1;                 // count row stride
+    static constexpr int LKS = kCap + 2;                // candidate-key row stride (8-byte keys)
+    static constexpr int LSS = kMaxK + 4;               // selection row stride
     static constexpr int OFF_SC = 0;
     static constexpr int OFF_BIAS = OFF_SC + TPP * RS * 4;
     static constexpr int OFF_GM = OFF_BIAS + BE * 4;
@@ -94,191 +99,54 @@ struct Cfg {
     static constexpr int OFF_OVF = OFF_SI + TPP * LSS * 4;
     static constexpr int OFF_HIST = OFF_OVF + 16 * 4;
     static constexpr int EPI_LDS = OFF_HIST + 1024 * 4;
-    static constexpr int LDS = MAIN_LDS > EPI_LDS ? MAIN_LDS : EPI_LDS;
-    static_assert(PPT * NT == BT * 8, "token-tile pieces must split evenly over threads");
+    static constexpr int LDS = MAIN_LDS_ > EPI_LDS ? MAIN_LDS_ : EPI_LDS;
+    static_assert(NPASS * TPP == BT && TPP % 32 == 0, "passes of whole 32-token groups");
     static_assert(TPT * TPP == NT && TPT <= 16 && 16 % TPT == 0, "a token's threads share one wave");
     static_assert(VPT * TPT == BE && VPT % 16 == 0 && GSZ * GPT == VPT && GPT * TPT == NG, "columns split evenly");
+    static_assert(TPP * RS * 4 <= kScoreLds, "score rows of a pass fit");
     static_assert(TPP <= 16 * 32, "overflow bitmask size");
     static_assert(LDS <= 160 * 1024, "LDS of one workgroup");
 };
 
-// One 16-byte unit of both operands: bf16 -> one 32x32x16 MFMA; fp32 -> four
-// 32x32x2 MFMAs, float i of each lane's unit feeding the i-th.
-template <bool F32>
-__device__ __forceinline__ floatx16 mfma_unit(uint4 a, uint4 b, floatx16 c) {
-    if constexpr (F32) {
-        c = __builtin_amdgcn_mfma_f32_32x32x2f32(__builtin_bit_cast(float, a.x), __builtin_bit_cast(float, b.x), c,
-                                                 0, 0, 0);
-        c = __builtin_amdgcn_mfma_f32_32x32x2f32(__builtin_bit_cast(float, a.y), __builtin_bit_cast(float, b.y), c,
-                                                 0, 0, 0);
-        c = __builtin_amdgcn_mfma_f32_32x32x2f32(__builtin_bit_cast(float, a.z), __builtin_bit_cast(float, b.z), c,
-                                                 0, 0, 0);
-        c = __builtin_amdgcn_mfma_f32_32x32x2f32(__builtin_bit_cast(float, a.w), __builtin_bit_cast(float, b.w), c,
-                                                 0, 0, 0);
-        return c;
-    } else {
-        return __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a), as_bf16x8(b), c, 0, 0, 0);
+// Adds a workgroup's LDS histogram into the global counts, one atomic per
+// non-zero bin.  Each workgroup starts at a different bin, so workgroups that
+// finish together do not queue on the same counter.
+__device__ __forceinline__ void flush_hist(const int* hist, int32_t* counts, int E) {
+    const int rot = (int)((blockIdx.x * 97u) % (unsigned)E);
+    for (int i = threadIdx.x; i < E; i += blockDim.x) {
+        int e = i + rot;
+        e = e < E ? e : e - E;
+        if (hist[e] != 0) atomicAdd(&counts[e], hist[e]);
     }
 }
 
-template <bool F32, bool PACKED, int WAVES, int TBW, int NBLK>
-__global__ __launch_bounds__(WAVES * 64) void router_score_select_kernel(RouterArgs a, int NS) {
-    using C = Cfg<F32, WAVES, TBW, NBLK>;
-    __shared__ __attribute__((aligned(16))) unsigned char smem[C::LDS];
+// Loads the slice's bias into registers (issued before the contraction, so
+// it arrives meanwhile); the epilogue moves it to LDS.
+template <class EC>
+__device__ __forceinline__ void prefetch_bias(const RouterArgs& a, int sbase, float (&breg)[EC::NBIAS]) {
+#pragma unroll
+    for (int i = 0; i < EC::NBIAS; ++i) {
+        const int c = threadIdx.x + EC::NT * i;
+        breg[i] = (c < EC::BE && sbase + c < a.E) ? a.bias[sbase + c] : 0.0f;
+    }
+}
 
+// Steps A-G for the workgroup's BT tokens of one slice.  store_pass(pass, sc)
+// writes the sigmoid scores of tokens [pass*TPP, (pass+1)*TPP) of the tile
+// into rows 0..TPP-1 of the LDS score matrix sc (and the debug dump).
+template <class EC, class StoreFn>
+__device__ __forceinline__ void select_epilogue(const RouterArgs& a, int NS, int slice, int64_t tok0,
+                                                unsigned char* smem, const float (&breg)[EC::NBIAS],
+                                                StoreFn&& store_pass) {
+    using C = EC;
+    constexpr int WAVES = C::NT / 64;
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: keep it scalar
-    const int h = lane >> 5;
-    const int l32 = lane & 31;
-
-    // XCD-aware block order: consecutive blocks land on different XCDs, so
-    // remap to give each XCD a contiguous run of (tile, slice) pairs; the
-    // slices of one token tile then share their token rows in that XCD's L2.
-    const int nb = gridDim.x;
-    int L = blockIdx.x;
-    if ((nb & 7) == 0) L = (blockIdx.x & 7) * (nb >> 3) + (blockIdx.x >> 3);
-    const int tile = L / NS;
-    const int slice = L - tile * NS;
-
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int64_t T = a.T;
     const int E = a.E;
     const int K = a.K;
-    const int64_t tok0 = (int64_t)tile * C::BT;
-    const int e_wave0 = slice * C::BE + wave * C::WE;
-    const int64_t RB = (int64_t)a.d * (F32 ? 4 : 2);
-    const int NCH = (int)(RB / 128);
-
-    if (a.zero_counts && blockIdx.x == 0)
-        for (int e = tid; e < E; e += C::NT) a.counts[e] = 0;
-
-    // The slice's bias, fetched now (it arrives during the contraction) and
-    // moved to LDS by the epilogue.
-    const int sbase = slice * C::BE;  // first expert of the slice
-    float breg[C::NBIAS];
-#pragma unroll
-    for (int i = 0; i < C::NBIAS; ++i) {
-        const int c = tid + C::NT * i;
-        breg[i] = (c < C::BE && sbase + c < E) ? a.bias[sbase + c] : 0.0f;
-    }
-
-    // ---------------------------------------------------------------- contraction
-    // Operands are fetched with buffer loads: a scalar resource per operand
-    // and a 32-bit per-lane offset, with the chunk and block advance in the
-    // scalar offset, so the unrolled loads need no 64-bit address registers.
-    // Every load stays inside its resource by construction (the scalar offset
-    // is not range-checked).
-    //
-    // A operands (router rows): the per-lane offset and, per block, the
-    // block's scalar offset; a chunk adds WCH bytes, a unit WU.
-    constexpr int WU = PACKED ? 1024 : 16;
-    constexpr int WCH = PACKED ? 4096 : 128;
-    const __amdgpu_buffer_rsrc_t wres = make_rsrc(a.W, (int64_t)E * RB);
-    const int wvoff = PACKED ? lane * 16 : l32 * (int)RB + 64 * h;
-    int wsoff[NBLK];
-#pragma unroll
-    for (int nbk = 0; nbk < NBLK; ++nbk) {
-        int blk = (e_wave0 + nbk * 32) / 32;
-        blk = blk < E / 32 ? blk : E / 32 - 1;  // padding blocks read a valid block; masked later
-        wsoff[nbk] = PACKED ? blk * NCH * 4096 : blk * 32 * (int)RB;
-    }
-    // Token-tile pieces: thread piece p = tid + NT*q covers row p/8, bytes
-    // 16*(p%8) of the chunk.  Rows past T re-read row T-1 (never output).
-    const int nrows = (int)((T - tok0) < C::BT ? (T - tok0) : C::BT);
-    const __amdgpu_buffer_rsrc_t xres =
-        make_rsrc(reinterpret_cast<const char*>(a.x) + tok0 * RB, (int64_t)nrows * RB);
-    int xvoff[C::PPT];
-    int xdst[C::PPT];
-#pragma unroll
-    for (int q = 0; q < C::PPT; ++q) {
-        const int p = tid + C::NT * q;
-        const int row = p >> 3, c16 = p & 7;
-        const int rowc = row < nrows ? row : nrows - 1;
-        xvoff[q] = rowc * (int)RB + c16 * 16;
-        xdst[q] = row * kRowPad + c16 * 16;
-    }
-    const int boff = l32 * kRowPad + 64 * h;
-
-    floatx16 acc[TBW][NBLK];
-#pragma unroll
-    for (int tb = 0; tb < TBW; ++tb)
-#pragma unroll
-        for (int nbk = 0; nbk < NBLK; ++nbk)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) acc[tb][nbk][r] = 0.0f;
-
-    // Software pipeline, two chunks deep for both operands.  W operands: two
-    // register sets; right after the MFMAs of unit u of chunk c, set c&1
-    // starts loading unit u of chunk c+2.  Token tile: two sets of staging
-    // registers; the top of chunk c loads chunk c+2 into the set that held
-    // chunk c, and the end of chunk c stores chunk c+1 (loaded a whole chunk
-    // earlier) into the idle LDS stage.  Every fetch thus has about two
-    // chunks of MFMA work to arrive.
-    //
-    // The loop body is branch-free so that the compiler's vector-memory wait
-    // counts stay exact (loads complete in order; a conditional load would
-    // make every later wait drain the queue): prefetch targets are clamped
-    // to the last chunk (a cached re-read at the end), the last store goes to
-    // a stage that is never read, and an odd last chunk is peeled.
-    uint4 w[2][NBLK][4], xr[2][C::PPT];
-    auto load_x = [&](int c, int j) {
-#pragma unroll
-        for (int q = 0; q < C::PPT; ++q) xr[j][q] = bload16(xres, xvoff[q], c * 128);
-    };
-    auto store_x = [&](int stage, int j) {
-#pragma unroll
-        for (int q = 0; q < C::PPT; ++q) *reinterpret_cast<uint4*>(smem + stage * C::STAGE + xdst[q]) = xr[j][q];
-    };
-    auto load_w = [&](int c, int j) {
-#pragma unroll
-        for (int nbk = 0; nbk < NBLK; ++nbk)
-#pragma unroll
-            for (int u = 0; u < 4; ++u) w[j][nbk][u] = bload16(wres, wvoff + WU * u, wsoff[nbk] + c * WCH);
-    };
-    // MFMAs of one chunk from LDS stage / W set j; with prefetch, each W unit
-    // is refilled from chunk cn right after its MFMAs.
-    auto compute = [&](int j, bool prefetch, int cn) {
-        const unsigned char* st = smem + j * C::STAGE + boff;
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            uint4 bx[TBW];
-#pragma unroll
-            for (int tb = 0; tb < TBW; ++tb) bx[tb] = *reinterpret_cast<const uint4*>(st + tb * 32 * kRowPad + 16 * u);
-#pragma unroll
-            for (int tb = 0; tb < TBW; ++tb)
-#pragma unroll
-                for (int nbk = 0; nbk < NBLK; ++nbk) acc[tb][nbk] = mfma_unit<F32>(w[j][nbk][u], bx[tb], acc[tb][nbk]);
-            if (prefetch) {
-#pragma unroll
-                for (int nbk = 0; nbk < NBLK; ++nbk) w[j][nbk][u] = bload16(wres, wvoff + WU * u, wsoff[nbk] + cn * WCH);
-            }
-        }
-    };
-
-    const int last = NCH - 1;
-    load_x(0, 0);
-    load_w(0, 0);
-    load_x(last < 1 ? last : 1, 1);
-    load_w(last < 1 ? last : 1, 1);
-    store_x(0, 0);
-    __syncthreads();
-    for (int c0 = 0; c0 + 1 < NCH; c0 += 2) {
-#pragma unroll
-        for (int j = 0; j < 2; ++j) {
-            const int c = c0 + j;
-            const int cn = c + 2 < last ? c + 2 : last;
-            load_x(cn, j);
-            compute(j, true, cn);
-            store_x(1 - j, 1 - j);
-            __syncthreads();
-        }
-    }
-    if (NCH & 1) {
-        compute(0, false, 0);
-        __syncthreads();
-    }
-
-    // ---------------------------------------------------------------- epilogue
+    const int sbase = slice * C::BE;
     float* sc = reinterpret_cast<float*>(smem + C::OFF_SC);
     float* bias_s = reinterpret_cast<float*>(smem + C::OFF_BIAS);
     float* gm = reinterpret_cast<float*>(smem + C::OFF_GM);
@@ -296,9 +164,6 @@ __global__ __launch_bounds__(WAVES * 64) void router_score_select_kernel(RouterA
     }
     for (int e = tid; e < 1024; e += C::NT) hist[e] = 0;
 
-    // Slice column of accumulator (nbk, r): ccol + 32 nbk + 8 (r/4) + (r%4).
-    // E is a multiple of 32, so a whole 32-expert block is real or padding.
-    const int ccol = wave * C::WE + 4 * h;
     const int tl = tid / C::TPT, q = tid % C::TPT;  // token of the pass and part, in steps B-G
     // This thread's value j sits in slice column col(j) = 16 (q + TPT (j/16)) + j%16.
     auto col_of = [&](int j) { return 16 * (q + C::TPT * (j >> 4)) + (j & 15); };
@@ -316,29 +181,8 @@ __global__ __launch_bounds__(WAVES * 64) void router_score_select_kernel(RouterA
 
 #pragma unroll
     for (int pass = 0; pass < C::NPASS; ++pass) {
-        // A. scores of the pass's token blocks into the LDS score matrix
-#pragma unroll
-        for (int pb = 0; pb < C::PB; ++pb) {
-            const int tb = pass * C::PB + pb;
-            const int row = pb * 32 + l32;
-            const int64_t tok = tok0 + tb * 32 + l32;
-#pragma unroll
-            for (int nbk = 0; nbk < NBLK; ++nbk) {
-                const bool real = sbase + ccol - 4 * h + nbk * 32 < E;
-#pragma unroll
-                for (int r4 = 0; r4 < 4; ++r4) {
-                    float4 s4;
-                    s4.x = real ? sigmoid_fast(acc[tb][nbk][4 * r4 + 0]) : -INFINITY;
-                    s4.y = real ? sigmoid_fast(acc[tb][nbk][4 * r4 + 1]) : -INFINITY;
-                    s4.z = real ? sigmoid_fast(acc[tb][nbk][4 * r4 + 2]) : -INFINITY;
-                    s4.w = real ? sigmoid_fast(acc[tb][nbk][4 * r4 + 3]) : -INFINITY;
-                    const int col = ccol + nbk * 32 + 8 * r4;
-                    *reinterpret_cast<float4*>(sc + row * C::RS + col) = s4;
-                    if (a.dump && real && tok < T)
-                        *reinterpret_cast<float4*>(a.dump + tok * E + sbase + col) = s4;
-                }
-            }
-        }
+        // A. scores of the pass's tokens into the LDS score matrix
+        store_pass(pass, sc);
         if (tid < 16) ovf[tid] = 0;
         __syncthreads();
 
@@ -449,6 +293,7 @@ __global__ __launch_bounds__(WAVES * 64) void router_score_select_kernel(RouterA
                 mine[i] = c < n ? lk[tl * C::LKS + c] : ~0ull;  // ~0: beyond the list, never written
                 rank[i] = 0;
             }
+#pragma unroll 4
             for (int o = 0; o < n; ++o) {
                 const unsigned long long ko = lk[tl * C::LKS + o];
 #pragma unroll
@@ -511,6 +356,7 @@ __global__ __launch_bounds__(WAVES * 64) void router_score_select_kernel(RouterA
                     // gate weights: den is the fp32 sum of the selected
                     // unbiased scores in rank order
                     float den = 0.0f;
+#pragma unroll 8
                     for (int r = 0; r < K; ++r) den = den + sc[tl * C::RS + (si[tl * C::LSS + r] - sbase)];
                     for (int r = q; r < K; r += C::TPT) {
                         const int e = si[tl * C::LSS + r];
@@ -524,9 +370,393 @@ __global__ __launch_bounds__(WAVES * 64) void router_score_select_kernel(RouterA
         }
         __syncthreads();
     }
-    if (NS == 1)
-        for (int e = tid; e < E; e += C::NT)
-            if (hist[e] != 0) atomicAdd(&a.counts[e], hist[e]);
+    if (NS == 1) flush_hist(hist, a.counts, E);
+}
+
+// One 16-byte unit of both operands: bf16 -> one 32x32x16 MFMA; fp32 -> four
+// 32x32x2 MFMAs, float i of each lane's unit feeding the i-th.
+template <bool F32>
+__device__ __forceinline__ floatx16 mfma_unit(uint4 a, uint4 b, floatx16 c) {
+    if constexpr (F32) {
+        c = __builtin_amdgcn_mfma_f32_32x32x2f32(__builtin_bit_cast(float, a.x), __builtin_bit_cast(float, b.x), c,
+                                                 0, 0, 0);
+        c = __builtin_amdgcn_mfma_f32_32x32x2f32(__builtin_bit_cast(float, a.y), __builtin_bit_cast(float, b.y), c,
+                                                 0, 0, 0);
+        c = __builtin_amdgcn_mfma_f32_32x32x2f32(__builtin_bit_cast(float, a.z), __builtin_bit_cast(float, b.z), c,
+                                                 0, 0, 0);
+        c = __builtin_amdgcn_mfma_f32_32x32x2f32(__builtin_bit_cast(float, a.w), __builtin_bit_cast(float, b.w), c,
+                                                 0, 0, 0);
+        return c;
+    } else {
+        return __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a), as_bf16x8(b), c, 0, 0, 0);
+    }
+}
+
+// XCD-aware block order: consecutive blocks land on different XCDs, so remap
+// to give each XCD a contiguous run of (tile, slice) pairs; the slices of one
+// token tile then share their token rows in that XCD's L2.
+__device__ __forceinline__ int xcd_block_order() {
+    const int nb = gridDim.x;
+    int L = blockIdx.x;
+    if ((nb & 7) == 0) L = (blockIdx.x & 7) * (nb >> 3) + (blockIdx.x >> 3);
+    return L;
+}
+
+template <bool F32, int WAVES, int TBW, int NBLK>
+struct Cfg32 {
+    static constexpr int NT = WAVES * 64;
+    static constexpr int BT = 32 * TBW;
+    static constexpr int WE = 32 * NBLK;
+    static constexpr int BE = WAVES * WE;
+    static constexpr int PPT = BT * 8 / NT;  // 16-byte token-tile pieces per thread per chunk
+    static constexpr int STAGE = BT * kRowPad;
+    static constexpr int MAIN_LDS = 2 * STAGE;
+    using Epi = EpiCfg<NT, BT, BE, MAIN_LDS>;
+    static_assert(PPT * NT == BT * 8, "token-tile pieces must split evenly over threads");
+};
+
+template <bool F32, bool PACKED, int WAVES, int TBW, int NBLK>
+__global__ __launch_bounds__(WAVES * 64) void router32_kernel(RouterArgs a, int NS) {
+    using C = Cfg32<F32, WAVES, TBW, NBLK>;
+    using EC = typename C::Epi;
+    __shared__ __attribute__((aligned(16))) unsigned char smem[EC::LDS];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: keep it scalar
+    const int h = lane >> 5;
+    const int l32 = lane & 31;
+    const int L = xcd_block_order();
+    const int tile = L / NS;
+    const int slice = L - tile * NS;
+
+    const int64_t T = a.T;
+    const int E = a.E;
+    const int64_t tok0 = (int64_t)tile * C::BT;
+    const int e_wave0 = slice * C::BE + wave * C::WE;
+    const int64_t RB = (int64_t)a.d * (F32 ? 4 : 2);
+    const int NCH = (int)(RB / 128);
+
+    if (a.zero_counts && blockIdx.x == 0)
+        for (int e = tid; e < E; e += C::NT) a.counts[e] = 0;
+    const int sbase = slice * C::BE;
+    float breg[EC::NBIAS];
+    prefetch_bias<EC>(a, sbase, breg);
+
+    // ---------------------------------------------------------------- contraction
+    // Operands are fetched with buffer loads: a scalar resource per operand
+    // and a 32-bit per-lane offset, with the chunk and block advance in the
+    // scalar offset, so the unrolled loads need no 64-bit address registers.
+    // Every load stays inside its resource by construction (the scalar offset
+    // is not range-checked).
+    //
+    // A operands (router rows): lane (h, m = l32) reads row 32 blk + m, bytes
+    // c*128 + 64 h + 16 u.  Packed: the piece of 16-row block 2 blk + m/16,
+    // chunk c and half h, at lane slot m%16 + 16 u.  A chunk adds WCH bytes to
+    // the scalar offset, a unit WU to the lane offset.
+    constexpr int WU = PACKED ? 256 : 16;
+    constexpr int WCH = PACKED ? 2048 : 128;
+    const __amdgpu_buffer_rsrc_t wres = make_rsrc(a.W, (int64_t)E * RB);
+    const int wvoff = PACKED ? (l32 >> 4) * NCH * 2048 + h * 1024 + (l32 & 15) * 16 : l32 * (int)RB + 64 * h;
+    int wsoff[NBLK];
+#pragma unroll
+    for (int nbk = 0; nbk < NBLK; ++nbk) {
+        int blk = (e_wave0 + nbk * 32) / 32;
+        blk = blk < E / 32 ? blk : E / 32 - 1;  // padding blocks read a valid block; masked later
+        wsoff[nbk] = PACKED ? blk * NCH * 4096 : blk * 32 * (int)RB;
+    }
+    // Token-tile pieces: thread piece p = tid + NT*q covers row p/8, bytes
+    // 16*(p%8) of the chunk.  Rows past T re-read row T-1 (never output).
+    const int nrows = (int)((T - tok0) < C::BT ? (T - tok0) : C::BT);
+    const __amdgpu_buffer_rsrc_t xres =
+        make_rsrc(reinterpret_cast<const char*>(a.x) + tok0 * RB, (int64_t)nrows * RB);
+    int xvoff[C::PPT];
+    int xdst[C::PPT];
+#pragma unroll
+    for (int q = 0; q < C::PPT; ++q) {
+        const int p = tid + C::NT * q;
+        const int row = p >> 3, c16 = p & 7;
+        const int rowc = row < nrows ? row : nrows - 1;
+        xvoff[q] = rowc * (int)RB + c16 * 16;
+        xdst[q] = row * kRowPad + c16 * 16;
+    }
+    const int boff = l32 * kRowPad + 64 * h;
+
+    floatx16 acc[TBW][NBLK];
+#pragma unroll
+    for (int tb = 0; tb < TBW; ++tb)
+#pragma unroll
+        for (int nbk = 0; nbk < NBLK; ++nbk)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[tb][nbk][r] = 0.0f;
+
+    // Software pipeline, two chunks deep for both operands.  W operands: two
+    // register sets; right after the MFMAs of unit u of chunk c, set c&1
+    // starts loading unit u of chunk c+2.  Token tile: two sets of staging
+    // registers; the top of chunk c loads chunk c+2 into the set that held
+    // chunk c, and the end of chunk c stores chunk c+1 (loaded a whole chunk
+    // earlier) into the idle LDS stage.  Every fetch thus has about two
+    // chunks of MFMA work to arrive.
+    //
+    // The loop body is branch-free so that the compiler's vector-memory wait
+    // counts stay exact (loads complete in order; a conditional load would
+    // make every later wait drain the queue): prefetch targets are clamped
+    // to the last chunk (a cached re-read at the end), the last store goes to
+    // a stage that is never read, and an odd last chunk is peeled.
+    uint4 w[2][NBLK][4], xr[2][C::PPT];
+    auto load_x = [&](int c, int j) {
+#pragma unroll
+        for (int q = 0; q < C::PPT; ++q) xr[j][q] = bload16(xres, xvoff[q], c * 128);
+    };
+    auto store_x = [&](int stage, int j) {
+#pragma unroll
+        for (int q = 0; q < C::PPT; ++q) *reinterpret_cast<uint4*>(smem + stage * C::STAGE + xdst[q]) = xr[j][q];
+    };
+    auto load_w = [&](int c, int j) {
+#pragma unroll
+        for (int nbk = 0; nbk < NBLK; ++nbk)
+#pragma unroll
+            for (int u = 0; u < 4; ++u) w[j][nbk][u] = bload16(wres, wvoff + WU * u, wsoff[nbk] + c * WCH);
+    };
+    // MFMAs of one chunk from LDS stage / W set j; with prefetch, each W unit
+    // is refilled from chunk cn right after its MFMAs.
+    auto compute = [&](int j, bool prefetch, int cn) {
+        const unsigned char* st = smem + j * C::STAGE + boff;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            uint4 bx[TBW];
+#pragma unroll
+            for (int tb = 0; tb < TBW; ++tb) bx[tb] = *reinterpret_cast<const uint4*>(st + tb * 32 * kRowPad + 16 * u);
+#pragma unroll
+            for (int tb = 0; tb < TBW; ++tb)
+#pragma unroll
+                for (int nbk = 0; nbk < NBLK; ++nbk) acc[tb][nbk] = mfma_unit<F32>(w[j][nbk][u], bx[tb], acc[tb][nbk]);
+            if (prefetch) {
+#pragma unroll
+                for (int nbk = 0; nbk < NBLK; ++nbk) w[j][nbk][u] = bload16(wres, wvoff + WU * u, wsoff[nbk] + cn * WCH);
+            }
+        }
+    };
+
+    const int last = NCH - 1;
+    load_x(0, 0);
+    load_w(0, 0);
+    load_x(last < 1 ? last : 1, 1);
+    load_w(last < 1 ? last : 1, 1);
+    store_x(0, 0);
+    __syncthreads();
+    for (int c0 = 0; c0 + 1 < NCH; c0 += 2) {
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            const int c = c0 + j;
+            const int cn = c + 2 < last ? c + 2 : last;
+            load_x(cn, j);
+            compute(j, true, cn);
+            store_x(1 - j, 1 - j);
+            __syncthreads();
+        }
+    }
+    if (NCH & 1) {
+        compute(0, false, 0);
+        __syncthreads();
+    }
+
+    // ---------------------------------------------------------------- selection
+    // Slice column of accumulator (nbk, r): wave*WE + 4 h + 32 nbk + 8 (r/4) +
+    // (r%4).  E is a multiple of 32, so a whole 32-expert block is real or
+    // padding.
+    const int ccol = wave * C::WE + 4 * h;
+    auto store_pass = [&](int pass, float* sc) {
+        constexpr int PB = EC::TPP / 32;
+#pragma unroll
+        for (int pb = 0; pb < PB; ++pb) {
+            const int tb = pass * PB + pb;
+            const int row = pb * 32 + l32;
+            const int64_t tok = tok0 + tb * 32 + l32;
+#pragma unroll
+            for (int nbk = 0; nbk < NBLK; ++nbk) {
+                const bool real = sbase + wave * C::WE + nbk * 32 < E;
+#pragma unroll
+                for (int r4 = 0; r4 < 4; ++r4) {
+                    float4 s4;
+                    s4.x = real ? sigmoid_fast(acc[tb][nbk][4 * r4 + 0]) : -INFINITY;
+                    s4.y = real ? sigmoid_fast(acc[tb][nbk][4 * r4 + 1]) : -INFINITY;
+                    s4.z = real ? sigmoid_fast(acc[tb][nbk][4 * r4 + 2]) : -INFINITY;
+                    s4.w = real ? sigmoid_fast(acc[tb][nbk][4 * r4 + 3]) : -INFINITY;
+                    const int col = ccol + nbk * 32 + 8 * r4;
+                    *reinterpret_cast<float4*>(sc + row * EC::RS + col) = s4;
+                    if (a.dump && real && tok < T) *reinterpret_cast<float4*>(a.dump + tok * E + sbase + col) = s4;
+                }
+            }
+        }
+    };
+    select_epilogue<EC>(a, NS, slice, tok0, smem, breg, store_pass);
+}
+
+template <int WAVES, int TT, int ET>
+struct Cfg16 {
+    static constexpr int NT = WAVES * 64;
+    static constexpr int BT = 16 * TT;
+    static constexpr int WE = 16 * ET;
+    static constexpr int BE = WAVES * WE;
+    static constexpr int PPT = BT * 8 / NT;  // 16-byte token-tile pieces per thread per chunk
+    static constexpr int STAGE = BT * kRowPad;
+    static constexpr int MAIN_LDS = 2 * STAGE;
+    using Epi = EpiCfg<NT, BT, BE, MAIN_LDS>;
+    static_assert(PPT * NT == BT * 8, "token-tile pieces must split evenly over threads");
+};
+
+template <bool PACKED, int WAVES, int TT, int ET>
+__global__ __launch_bounds__(WAVES * 64) void router16_kernel(RouterArgs a, int NS) {
+    using C = Cfg16<WAVES, TT, ET>;
+    using EC = typename C::Epi;
+    __shared__ __attribute__((aligned(16))) unsigned char smem[EC::LDS];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: keep it scalar
+    const int l16 = lane & 15, g4 = lane >> 4;
+    const int L = xcd_block_order();
+    const int tile = L / NS;
+    const int slice = L - tile * NS;
+
+    const int64_t T = a.T;
+    const int E = a.E;
+    const int64_t tok0 = (int64_t)tile * C::BT;
+    const int e_wave0 = slice * C::BE + wave * C::WE;
+    const int64_t RB = (int64_t)a.d * 2;
+    const int NCH = (int)(RB / 128);
+
+    if (a.zero_counts && blockIdx.x == 0)
+        for (int e = tid; e < E; e += C::NT) a.counts[e] = 0;
+    const int sbase = slice * C::BE;
+    float breg[EC::NBIAS];
+    prefetch_bias<EC>(a, sbase, breg);
+
+    // ---------------------------------------------------------------- contraction
+    // Buffer loads as in router32_kernel.  A operand of expert tile et, chunk
+    // c, half s (k bytes [64 s, 64 s + 64) of the chunk): lane l reads row
+    // 16 b + l%16, bytes c*128 + 64 s + 16 (l/16) of its 16-row block b.
+    // Packed, that is the piece of (b, c, s) at lane slot l.
+    constexpr int WS = PACKED ? 1024 : 64;     // lane-offset step of a half
+    constexpr int WCH = PACKED ? 2048 : 128;   // scalar-offset step of a chunk
+    const __amdgpu_buffer_rsrc_t wres = make_rsrc(a.W, (int64_t)E * RB);
+    const int wvoff = PACKED ? lane * 16 : l16 * (int)RB + 16 * g4;
+    int wsoff[ET];
+#pragma unroll
+    for (int et = 0; et < ET; ++et) {
+        int blk = (e_wave0 + et * 16) / 16;
+        blk = blk < E / 16 ? blk : E / 16 - 1;  // padding tiles read a valid block; masked later
+        wsoff[et] = PACKED ? blk * NCH * 2048 : blk * 16 * (int)RB;
+    }
+    // Token-tile pieces: thread piece p = tid + NT*q covers row p/8, bytes
+    // 16*(p%8) of the chunk.  Rows past T re-read row T-1 (never output).
+    const int nrows = (int)((T - tok0) < C::BT ? (T - tok0) : C::BT);
+    const __amdgpu_buffer_rsrc_t xres =
+        make_rsrc(reinterpret_cast<const char*>(a.x) + tok0 * RB, (int64_t)nrows * RB);
+    int xvoff[C::PPT];
+    int xdst[C::PPT];
+#pragma unroll
+    for (int q = 0; q < C::PPT; ++q) {
+        const int p = tid + C::NT * q;
+        const int row = p >> 3, c16 = p & 7;
+        const int rowc = row < nrows ? row : nrows - 1;
+        xvoff[q] = rowc * (int)RB + c16 * 16;
+        xdst[q] = row * kRowPad + c16 * 16;
+    }
+    // B operand of token tile tt, half s: token 16 tt + l%16, bytes 64 s + 16 (l/16).
+    const int boff = l16 * kRowPad + 16 * g4;
+
+    floatx4 acc[TT][ET];
+#pragma unroll
+    for (int tt = 0; tt < TT; ++tt)
+#pragma unroll
+        for (int et = 0; et < ET; ++et) acc[tt][et] = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
+
+    // Software pipeline as in router32_kernel: two W register sets and two
+    // token-tile staging sets, two chunks deep, branch-free loop body.
+    uint4 w[2][ET][2], xr[2][C::PPT];
+    auto load_x = [&](int c, int j) {
+#pragma unroll
+        for (int q = 0; q < C::PPT; ++q) xr[j][q] = bload16(xres, xvoff[q], c * 128);
+    };
+    auto store_x = [&](int stage, int j) {
+#pragma unroll
+        for (int q = 0; q < C::PPT; ++q) *reinterpret_cast<uint4*>(smem + stage * C::STAGE + xdst[q]) = xr[j][q];
+    };
+    auto load_w = [&](int c, int j) {
+#pragma unroll
+        for (int et = 0; et < ET; ++et)
+#pragma unroll
+            for (int s = 0; s < 2; ++s) w[j][et][s] = bload16(wres, wvoff + WS * s, wsoff[et] + c * WCH);
+    };
+    auto compute = [&](int j, bool prefetch, int cn) {
+        const unsigned char* st = smem + j * C::STAGE + boff;
+#pragma unroll
+        for (int s = 0; s < 2; ++s) {
+#pragma unroll
+            for (int tt = 0; tt < TT; ++tt) {
+                const uint4 bx = *reinterpret_cast<const uint4*>(st + tt * 16 * kRowPad + 64 * s);
+#pragma unroll
+                for (int et = 0; et < ET; ++et)
+                    acc[tt][et] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(w[j][et][s]), as_bf16x8(bx),
+                                                                          acc[tt][et], 0, 0, 0);
+            }
+            if (prefetch) {
+#pragma unroll
+                for (int et = 0; et < ET; ++et) w[j][et][s] = bload16(wres, wvoff + WS * s, wsoff[et] + cn * WCH);
+            }
+        }
+    };
+
+    const int last = NCH - 1;
+    load_x(0, 0);
+    load_w(0, 0);
+    load_x(last < 1 ? last : 1, 1);
+    load_w(last < 1 ? last : 1, 1);
+    store_x(0, 0);
+    __syncthreads();
+    for (int c0 = 0; c0 + 1 < NCH; c0 += 2) {
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            const int c = c0 + j;
+            const int cn = c + 2 < last ? c + 2 : last;
+            load_x(cn, j);
+            compute(j, true, cn);
+            store_x(1 - j, 1 - j);
+            __syncthreads();
+        }
+    }
+    if (NCH & 1) {
+        compute(0, false, 0);
+        __syncthreads();
+    }
+
+    // ---------------------------------------------------------------- selection
+    // Slice column of accumulator (et, r): wave*WE + 16 et + 4 (l/16) + r.
+    // E is a multiple of 32, so a whole 16-expert tile is real or padding.
+    auto store_pass = [&](int pass, float* sc) {
+        constexpr int PT = EC::TPP / 16;  // token tiles per pass
+#pragma unroll
+        for (int pt = 0; pt < PT; ++pt) {
+            const int tt = pass * PT + pt;
+            const int row = pt * 16 + l16;
+            const int64_t tok = tok0 + tt * 16 + l16;
+#pragma unroll
+            for (int et = 0; et < ET; ++et) {
+                const bool real = sbase + wave * C::WE + et * 16 < E;
+                float4 s4;
+                s4.x = real ? sigmoid_fast(acc[tt][et][0]) : -INFINITY;
+                s4.y = real ? sigmoid_fast(acc[tt][et][1]) : -INFINITY;
+                s4.z = real ? sigmoid_fast(acc[tt][et][2]) : -INFINITY;
+                s4.w = real ? sigmoid_fast(acc[tt][et][3]) : -INFINITY;
+                const int col = wave * C::WE + et * 16 + 4 * g4;
+                *reinterpret_cast<float4*>(sc + row * EC::RS + col) = s4;
+                if (a.dump && real && tok < T) *reinterpret_cast<float4*>(a.dump + tok * E + sbase + col) = s4;
+            }
+        }
+    };
+    select_epilogue<EC>(a, NS, slice, tok0, smem, breg, store_pass);
 }
 
 // Merge the slices' rank-ordered candidate lists into the final Top-K, compute
@@ -588,53 +818,160 @@ __global__ __launch_bounds__(kMergeThreads) void router_merge_kernel(RouterArgs 
         }
     }
     __syncthreads();
-    for (int e = tid; e < E; e += kMergeThreads)
-        if (hist[e] != 0) atomicAdd(&a.counts[e], hist[e]);
+    flush_hist(hist, a.counts, E);
 }
 
-// Router matrix [E][d] -> packed layout: for 32-expert block b, chunk c
-// (128 bytes of each row), unit u (16 bytes), lane l = 32h + m, the 16 bytes
-// at ((b*NCH + c)*4 + u)*1024 + 16 l are row 32b + m, bytes c*128 + 64h + 16u.
+// Merge by token tile (NS*K <= 64): a few workgroups walk the 128-token tiles
+// in a grid-stride loop.  A tile's NS*K candidates per token go to LDS; each
+// candidate's final rank is its position in its slice's list plus the other
+// slices' candidates above it (keys are distinct, as the experts are).  The
+// next tile's candidates are fetched into registers while the current one is
+// ranked, and the workgroup's histogram is flushed once at the end (few
+// workgroups: few, spread-out flushes instead of a burst on the same
+// counters).
+constexpr int kTileThreads = 512;
+constexpr int kTileTokens = 128;
+constexpr int kTileBlocks = 4096;
+
+__global__ __launch_bounds__(kTileThreads) void router_merge_tile_kernel(RouterArgs a, int NS) {
+    __shared__ int hist[1024];
+    __shared__ unsigned long long mk[kTileTokens * 64];
+    __shared__ float ms[kTileTokens * 64];
+    __shared__ float msel[kTileTokens * kMaxK];
+    __shared__ int midx[kTileTokens * kMaxK];
+    const int E = a.E, K = a.K;
+    const int NSK = NS * K;  // <= 64
+    const int tid = threadIdx.x;
+    for (int e = tid; e < E; e += kTileThreads) hist[e] = 0;
+    const int64_t ntiles = (a.T + kTileTokens - 1) / kTileTokens;
+
+    // A thread's candidates of tile g (indices past the tile's candidates
+    // re-read the last one; they are never used).
+    constexpr int kIt = kTileTokens * 64 / kTileThreads;
+    float cv[kIt], cs[kIt];
+    int ci[kIt];
+    auto fetch = [&](int64_t g) {
+        const int64_t t0 = g * kTileTokens;
+        const int nt = (int)((a.T - t0) < kTileTokens ? (a.T - t0) : kTileTokens);
+        const int n = nt * NSK;
+#pragma unroll
+        for (int it = 0; it < kIt; ++it) {
+            int c = tid + it * kTileThreads;
+            c = c < n ? c : n - 1;
+            const int64_t gi = t0 * NSK + c;  // candidates of token t: [t][slice][K]
+            cv[it] = a.cand_v[gi];
+            cs[it] = a.cand_s[gi];
+            ci[it] = a.cand_i[gi];
+        }
+    };
+    int64_t g = blockIdx.x;
+    if (g < ntiles) fetch(g);
+    for (; g < ntiles; g += gridDim.x) {
+        const int64_t tok0 = g * kTileTokens;
+        const int ntok = (int)((a.T - tok0) < kTileTokens ? (a.T - tok0) : kTileTokens);
+        const int n = ntok * NSK;
+        __syncthreads();  // the previous tile is done with the LDS arrays
+#pragma unroll
+        for (int it = 0; it < kIt; ++it) {
+            const int c = tid + it * kTileThreads;
+            if (c < n) {
+                mk[c] = rank_key(cv[it], ci[it]);
+                ms[c] = cs[it];
+            }
+        }
+        if (g + gridDim.x < ntiles) fetch(g + gridDim.x);
+        __syncthreads();
+        for (int c = tid; c < n; c += kTileThreads) {
+            const int t = c / NSK, pos = c - t * NSK;
+            const int sl = pos / K, r = pos - sl * K;
+            const unsigned long long k = mk[c];
+            int rank = r;
+            for (int o = 0; o < NS; ++o) {
+                if (o == sl) continue;
+                const unsigned long long* lo = mk + t * NSK + o * K;
+#pragma unroll 8
+                for (int j = 0; j < K; ++j) rank += (lo[j] > k) ? 1 : 0;
+            }
+            if (rank < K) {
+                msel[t * kMaxK + rank] = ms[c];
+                midx[t * kMaxK + rank] = (int)~(unsigned)k;
+            }
+        }
+        __syncthreads();
+        // gate weights: den is the fp32 sum of the selected unbiased scores
+        // in rank order
+        for (int c = tid; c < ntok * K; c += kTileThreads) {
+            const int t = c / K, r = c - t * K;
+            float den = 0.0f;
+#pragma unroll 8
+            for (int j = 0; j < K; ++j) den = den + msel[t * kMaxK + j];
+            const int e = midx[t * kMaxK + r];
+            const int64_t tok = tok0 + t;
+            a.idx[tok * K + r] = e;
+            a.w[tok * K + r] = (den == 0.0f) ? 1.0f / (float)K : msel[t * kMaxK + r] / den;
+            atomicAdd(&hist[e], 1);
+        }
+    }
+    __syncthreads();
+    flush_hist(hist, a.counts, E);
+}
+
+// Router matrix [E][d] -> packed layout: output piece p (16 bytes) = lane
+// slot l = p%64 of the 1 KB piece (b, c, s) with p/64 = (b*NCH + c)*2 + s,
+// i.e. row 16 b + l%16, bytes c*128 + 64 s + 16 (l/16).
 __global__ void pack_weight_kernel(const char* __restrict__ W, char* __restrict__ P, int64_t RB, int64_t pieces) {
     const int64_t nch = RB / 128;
     for (int64_t o = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; o < pieces;
          o += (int64_t)gridDim.x * blockDim.x) {
-        const int l = (int)(o & 63), u = (int)((o >> 6) & 3);
-        const int64_t c = (o >> 8) % nch, b = (o >> 8) / nch;
-        const int m = l & 31, hh = l >> 5;
-        const int64_t src = (b * 32 + m) * RB + c * 128 + 64 * hh + 16 * u;
+        const int l = (int)(o & 63), s = (int)((o >> 6) & 1);
+        const int64_t c = (o >> 7) % nch, b = (o >> 7) / nch;
+        const int64_t src = (b * 16 + (l & 15)) * RB + c * 128 + 64 * s + 16 * (l >> 4);
         *reinterpret_cast<uint4*>(P + o * 16) = *reinterpret_cast<const uint4*>(W + src);
     }
 }
 
 template <bool F32, bool PACKED, int WAVES, int TBW, int NBLK>
-hipError_t launch_tiling(const RouterArgs& a, int NS, hipStream_t stream) {
-    using C = Cfg<F32, WAVES, TBW, NBLK>;
-    const int64_t tiles = (a.T + C::BT - 1) / C::BT;
-    const int64_t blocks = tiles * NS;
-    hipLaunchKernelGGL((router_score_select_kernel<F32, PACKED, WAVES, TBW, NBLK>), dim3((unsigned)blocks),
-                       dim3(C::NT), 0, stream, a, NS);
+hipError_t launch32(const RouterArgs& a, int NS, hipStream_t stream) {
+    using C = Cfg32<F32, WAVES, TBW, NBLK>;
+    const int64_t blocks = (a.T + C::BT - 1) / C::BT * NS;
+    hipLaunchKernelGGL((router32_kernel<F32, PACKED, WAVES, TBW, NBLK>), dim3((unsigned)blocks), dim3(C::NT), 0,
+                       stream, a, NS);
+    return hipGetLastError();
+}
+
+template <bool PACKED, int WAVES, int TT, int ET>
+hipError_t launch16(const RouterArgs& a, int NS, hipStream_t stream) {
+    using C = Cfg16<WAVES, TT, ET>;
+    const int64_t blocks = (a.T + C::BT - 1) / C::BT * NS;
+    hipLaunchKernelGGL((router16_kernel<PACKED, WAVES, TT, ET>), dim3((unsigned)blocks), dim3(C::NT), 0, stream, a,
+                       NS);
     return hipGetLastError();
 }
 
 template <bool PACKED>
 hipError_t launch_layout(const RouterTiling& t, const RouterArgs& a, int NS, hipStream_t stream) {
     switch (t.id) {
-        case 1: return launch_tiling<false, PACKED, 4, 4, 3>(a, NS, stream);
-        case 2: return launch_tiling<false, PACKED, 8, 2, 3>(a, NS, stream);
-        case 3: return launch_tiling<false, PACKED, 4, 4, 2>(a, NS, stream);
-        case 4: return launch_tiling<false, PACKED, 4, 4, 1>(a, NS, stream);
-        case 5: return launch_tiling<true, PACKED, 4, 4, 1>(a, NS, stream);
+        case 1: return launch32<false, PACKED, 4, 4, 3>(a, NS, stream);
+        case 2: return launch32<false, PACKED, 8, 2, 3>(a, NS, stream);
+        case 3: return launch32<false, PACKED, 4, 4, 2>(a, NS, stream);
+        case 4: return launch32<false, PACKED, 4, 4, 1>(a, NS, stream);
+        case 5: return launch32<true, PACKED, 4, 4, 1>(a, NS, stream);
+        case 6: return launch16<PACKED, 8, 8, 3>(a, NS, stream);
+        case 7: return launch16<PACKED, 8, 4, 6>(a, NS, stream);
         default: return hipErrorInvalidValue;
     }
 }
 
+// id, fp32 input, waves, tokens per workgroup, experts per wave, preference
+// among tilings with equally few padded experts (lower first).
 const RouterTiling kTilings[] = {
-    {1, 0, 4, 4, 3},  // bf16: 128 tokens x 384 experts per workgroup
-    {2, 0, 8, 2, 3},  // bf16: 64 tokens x 768 experts per workgroup
-    {3, 0, 4, 4, 2},  // bf16: 128 tokens x 256 experts
-    {4, 0, 4, 4, 1},  // bf16: 128 tokens x 128 experts
-    {5, 1, 4, 4, 1},  // fp32: 128 tokens x 128 experts
+    {1, 0, 4, 128, 96, 2},  // bf16 32x32 tiles: 128 tokens x 384 experts per workgroup
+    {2, 0, 8, 64, 96, 1},   // bf16 32x32 tiles: 64 tokens x 768 experts
+    {3, 0, 4, 128, 64, 3},  // bf16 32x32 tiles: 128 tokens x 256 experts
+    {4, 0, 4, 128, 32, 4},  // bf16 32x32 tiles: 128 tokens x 128 experts
+    {5, 1, 4, 128, 32, 0},  // fp32 32x32 tiles: 128 tokens x 128 experts
+    {6, 0, 8, 128, 48, 0},  // bf16 16x16 tiles: 128 tokens x 384 experts, two waves per SIMD
+    {7, 0, 8, 64, 96, 5},   // bf16 16x16 tiles: 64 tokens x 768 experts, two waves per SIMD
 };
 
 }  // namespace
@@ -650,6 +987,12 @@ hipError_t launch_router_score_select(const RouterTiling& t, const RouterArgs& a
 hipError_t launch_router_merge(const RouterTiling& t, const RouterArgs& a, hipStream_t stream) {
     const int NS = router_slices(t, a.E);
     if (NS <= 1) return hipSuccess;
+    if (NS * a.K <= 64) {
+        int64_t blocks = (a.T + kTileTokens - 1) / kTileTokens;
+        if (blocks > kTileBlocks) blocks = kTileBlocks;
+        hipLaunchKernelGGL(router_merge_tile_kernel, dim3((unsigned)blocks), dim3(kTileThreads), 0, stream, a, NS);
+        return hipGetLastError();
+    }
     const int tpg = kMergeThreads / (NS * a.K);
     int64_t groups = (a.T + tpg - 1) / tpg;
     if (groups > kMergeBlocks) groups = kMergeBlocks;

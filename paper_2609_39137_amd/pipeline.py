@@ -66,8 +66,11 @@ class RouterStep:
     def load_stats(self, stream=None):
         B.idb_load_stats(self.counts, self.stats, stream)
 
+    def update_and_stats(self, stream=None):
+        """MaxVio/MinVio of this step's counts and the bias update, one launch."""
+        B.idb_controller_step(self.counts, self.cfg, self.state, self.stats, stream)
+
     def step(self, x, W=None, stream=None):
-        """Route, update the bias, compute MaxVio/MinVio (all asynchronous)."""
+        """Route, then compute MaxVio/MinVio and update the bias (all asynchronous)."""
         self.route(x, W, stream=stream)
-        self.update(stream)
-        self.load_stats(stream)
+        self.update_and_stats(stream)

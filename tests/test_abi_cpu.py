@@ -89,15 +89,17 @@ def test_merge_rejects_invalid_arguments():
 
 
 def test_workspace_and_variant_info():
-    # 768 experts in bf16: the automatic tiling covers them in one 768-expert
-    # slice (8 waves, 64 tokens per workgroup) and needs no workspace.
+    # 768 experts in bf16: the automatic tiling is the 16x16-tile kernel, two
+    # 384-expert slices of 8 waves x 48 experts, 128 tokens per workgroup; the
+    # slices' candidates are staged in the workspace.
     info = B.idb_router_variant_info(16384, 2048, 768, 10, B.IDB_DTYPE_BF16, 0)
-    assert info == {"tokens_per_wg": 64, "slices": 1, "waves": 8, "blocks_per_wave": 3, "variant": 2}
-    assert B.idb_router_workspace_bytes(16384, 2048, 768, 10, B.IDB_DTYPE_BF16, 0) == 0
-    # the two-slice tiling stages the slices' candidates in the workspace
-    info1 = B.idb_router_variant_info(16384, 2048, 768, 10, B.IDB_DTYPE_BF16, 1)
-    assert info1["slices"] == 2 and info1["tokens_per_wg"] == 128
-    assert B.idb_router_workspace_bytes(16384, 2048, 768, 10, B.IDB_DTYPE_BF16, 1) == 3 * 16384 * 2 * 10 * 4
+    assert info == {"tokens_per_wg": 128, "slices": 2, "waves": 8, "experts_per_wave": 48, "variant": 6}
+    # candidates (value, score, index) per token, slice and rank
+    assert B.idb_router_workspace_bytes(16384, 2048, 768, 10, B.IDB_DTYPE_BF16, 0) == 3 * 16384 * 2 * 10 * 4
+    # a single 768-expert slice needs no workspace
+    info2 = B.idb_router_variant_info(16384, 2048, 768, 10, B.IDB_DTYPE_BF16, 2)
+    assert info2["slices"] == 1 and info2["tokens_per_wg"] == 64 and info2["experts_per_wave"] == 96
+    assert B.idb_router_workspace_bytes(16384, 2048, 768, 10, B.IDB_DTYPE_BF16, 2) == 0
     # fp32 input, 64 experts: one 128-expert slice, half padding
     info3 = B.idb_router_variant_info(4096, 256, 64, 4, B.IDB_DTYPE_F32, 0)
     assert info3["slices"] == 1 and info3["variant"] == 5

@@ -114,3 +114,34 @@ def test_load_stats_matches_oracle(E):
         got = out.cpu().numpy()
         assert np.array_equal(got, ref) or (np.isnan(ref).all() and np.isnan(got).all())
         assert np.all(np.abs(got - ref) <= 1e-6) or np.isnan(ref).all()
+
+
+def run_fused(stream, E, Ki, Kd, mode=0, center=True):
+    """The one-launch controller step against the oracle, at every step."""
+    cfg = B.ControllerCfg(E, Ki, Kd, mode, center)
+    st = B.ControllerState(E, DEV)
+    ref = oracle.ControllerState(E)
+    stats = torch.zeros(2, dtype=torch.float64, device=DEV)
+    for t, n in enumerate(stream):
+        counts = torch.from_numpy(np.ascontiguousarray(n)).to(DEV)
+        B.idb_controller_step(counts, cfg, st, stats)
+        rs = oracle.controller(n, ref, Ki, Kd, mode=mode, center=center)
+        np.testing.assert_array_equal(st.bias.cpu().numpy(), ref.bias, err_msg=f"bias step {t}")
+        np.testing.assert_array_equal(st.e_prev.cpu().numpy(), ref.e_prev, err_msg=f"e_prev step {t}")
+        assert int(st.step.item()) == int(ref.step[0]) and int(st.status.item()) == rs
+        np.testing.assert_array_equal(stats.cpu().numpy(), oracle.load_stats(n))
+
+
+@pytest.mark.parametrize("E", [4, 63, 64, 65, 768, 1000, 1024])
+@pytest.mark.parametrize("mode,center", [(0, True), (0, False), (1, False), (1, True)])
+def test_fused_controller_step_matches_oracle(E, mode, center):
+    stream = synth.count_stream(E, 12 * E, 25, "mixed", seed=E + mode)
+    run_fused(stream, E, 6e-3 if mode == 0 else 1e-3, 6e-3, mode=mode, center=center)
+
+
+def test_fused_controller_step_empty_and_invalid_batches():
+    E = 96
+    stream = synth.count_stream(E, 8 * E, 6, "multinomial", seed=3)
+    stream[2] = 0            # empty batch: state untouched, status 3, statistics NaN
+    stream[4][5] = -1        # a negative count: state untouched, status 1
+    run_fused(stream, E, 6e-3, 6e-3)

@@ -148,15 +148,29 @@ def test_all_variants_identical():
     x, W = synth.normal_router_inputs(T, d, E, seed=3, w_std=0.05)
     b = synth.bias(E, "small", seed=4)
     ref = run_router(x, W, b, K, variant=1)
+    # the 32x32-tile variants accumulate in the same order: identical outputs
     for v in (2, 3, 4):
         got = run_router(x, W, b, K, variant=v)
         for a, g in zip(ref, got):
             np.testing.assert_array_equal(a, g)
+    # the 16x16-tile variant sums the contraction in another order: scores
+    # agree to fp32 rounding, and its selection is exact on its own scores
+    got6 = run_router(x, W, b, K, variant=6)
+    check_scores(got6[3], ref[3], rtol=1e-5)
+    check_invariants(*got6[:3], T, E, K)
+    si, sw, sc = gpu_select(got6[3], b, K)
+    np.testing.assert_array_equal(got6[0], si)
+    np.testing.assert_array_equal(got6[1].view(np.uint32), sw.view(np.uint32))
+    np.testing.assert_array_equal(got6[2], sc)
+    # the two 16x16-tile variants accumulate in the same order
+    got7 = run_router(x, W, b, K, variant=7)
+    for a, g in zip(got6, got7):
+        np.testing.assert_array_equal(a, g)
     again = run_router(x, W, b, K, variant=0)
-    for a, g in zip(ref, again):
+    for a, g in zip(got6, again):
         np.testing.assert_array_equal(a, g)
     nodump = run_router(x, W, b, K, variant=0, dump=False)
-    for a, g in zip(ref[:3], nodump[:3]):
+    for a, g in zip(got6[:3], nodump[:3]):
         np.testing.assert_array_equal(a, g)
 
 
@@ -187,7 +201,8 @@ def test_edge_shapes(T, E, K):
     check_against_oracle(x, W, b, K, idx, w, c, s, max_uncertain=0.02)
 
 
-@pytest.mark.parametrize("E,K,variant", [(1024, 32, 4), (1024, 17, 3), (800, 10, 4), (768, 16, 1), (768, 32, 1)])
+@pytest.mark.parametrize("E,K,variant", [(1024, 32, 4), (1024, 17, 3), (800, 10, 4), (768, 16, 1), (768, 32, 1),
+                                         (1024, 32, 6), (800, 10, 6), (768, 24, 6), (1024, 20, 7), (800, 10, 7)])
 def test_many_slices_and_large_k(E, K, variant):
     # up to 8 expert slices merged, K above the threshold path's 16 (every
     # list takes the per-token fallback), and E not a multiple of the slice
@@ -257,6 +272,7 @@ def test_workload_full_size_sampled_rows(name):
 @pytest.mark.parametrize("T,d,E,K,dtype,variant", [
     (517, 512, 768, 10, "bf16", 1), (517, 512, 768, 10, "bf16", 2), (300, 256, 768, 5, "bf16", 3),
     (129, 128, 800, 10, "bf16", 4), (1000, 256, 64, 4, "f32", 5), (64, 2048, 256, 8, "bf16", 0),
+    (517, 512, 768, 10, "bf16", 6), (300, 192, 800, 7, "bf16", 6), (200, 192, 800, 7, "bf16", 7),
 ])
 def test_packed_weight_layout_is_bit_identical(T, d, E, K, dtype, variant):
     x, W = synth.normal_router_inputs(T, d, E, seed=11, dtype=dtype, w_std=0.05)
@@ -276,12 +292,22 @@ def test_packed_weight_layout_is_bit_identical(T, d, E, K, dtype, variant):
 
 
 def test_pack_weight_is_the_documented_permutation():
+    # include/idb.h: piece (b, c, s) at byte ((b*NCH + c)*2 + s)*1024 holds, for
+    # lane slot l, bytes [c*128 + 64 s + 16 (l/16), +16) of row 16 b + l%16
     E, d = 96, 256
     _, W = synth.normal_router_inputs(1, d, E, seed=13, dtype="bf16")
     Wt = to_dev(W)
     P = torch.empty_like(Wt)
     B.idb_router_pack_weight(Wt, P)
-    nch = d // 64  # 128-byte chunks of a bf16 row
-    want = W.view(np.uint16).reshape(E // 32, 32, nch, 2, 4, 8).transpose(0, 2, 4, 3, 1, 5).reshape(E, d)
-    got = P.cpu().view(torch.int16).numpy().view(np.uint16)
+    got = P.cpu().view(torch.int16).numpy().view(np.uint8).reshape(-1)
+    src = W.view(np.uint8).reshape(E, d * 2)
+    nch = d * 2 // 128
+    want = np.empty_like(got)
+    for b in range(E // 16):
+        for c in range(nch):
+            for s in range(2):
+                base = ((b * nch + c) * 2 + s) * 1024
+                for l in range(64):
+                    lo = c * 128 + 64 * s + 16 * (l // 16)
+                    want[base + 16 * l: base + 16 * l + 16] = src[16 * b + l % 16, lo:lo + 16]
     np.testing.assert_array_equal(got, want)
