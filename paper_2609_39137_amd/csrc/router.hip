@@ -19,8 +19,8 @@
 // operands, so the k order agrees between A and B.
 //
 // Token tile: staged through registers into two LDS stages of 144-byte rows
-// (128 bytes + 16 of padding, so the B-operand reads are free of bank
-// conflicts), loaded two chunks ahead of use.
+// (128 bytes + 32 of padding, which measured fastest for the B-operand reads
+// and the staging writes), loaded two chunks ahead of use.
 //
 // Router matrix: either row-major [E][d] or the packed layout written by
 // idb_router_pack_weight: for every 16-expert block b, chunk c and 64-byte
@@ -61,7 +61,7 @@ namespace idb {
 namespace {
 
 constexpr int kCap = 32;      // candidate list capacity per token and slice
-constexpr int kRowPad = 144;  // LDS bytes per staged token row (128 + 16 pad)
+constexpr int kRowPad = 160;  // LDS bytes per staged token row (128 + 32 pad)
 constexpr int kMaxSlices = 8;
 constexpr int kScoreLds = 100000;  // LDS budget of the epilogue's score matrix
 
@@ -694,19 +694,31 @@ __global__ __launch_bounds__(WAVES * 64) void router16_kernel(RouterArgs a, int 
         const unsigned char* st = smem + j * C::STAGE + boff;
 #pragma unroll
         for (int s = 0; s < 2; ++s) {
+            // all of the half's B operands first, so their LDS latencies overlap
+            uint4 bx[TT];
 #pragma unroll
-            for (int tt = 0; tt < TT; ++tt) {
-                const uint4 bx = *reinterpret_cast<const uint4*>(st + tt * 16 * kRowPad + 64 * s);
+            for (int tt = 0; tt < TT; ++tt) bx[tt] = *reinterpret_cast<const uint4*>(st + tt * 16 * kRowPad + 64 * s);
+#pragma unroll
+            for (int tt = 0; tt < TT; ++tt)
 #pragma unroll
                 for (int et = 0; et < ET; ++et)
-                    acc[tt][et] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(w[j][et][s]), as_bf16x8(bx),
+                    acc[tt][et] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(w[j][et][s]), as_bf16x8(bx[tt]),
                                                                           acc[tt][et], 0, 0, 0);
-            }
             if (prefetch) {
 #pragma unroll
                 for (int et = 0; et < ET; ++et) w[j][et][s] = bload16(wres, wvoff + WS * s, wsoff[et] + cn * WCH);
             }
         }
+        // Schedule: half 0's eight B-operand reads, then its MFMAs with half
+        // 1's reads interleaved one per three MFMAs, then half 1's MFMAs, so
+        // no group of MFMAs waits for a fresh LDS read.
+        __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);  // LDS reads
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 3, 0);  // MFMA
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        }
+        __builtin_amdgcn_sched_group_barrier(0x008, 24, 0);
     };
 
     const int last = NCH - 1;
