@@ -6,15 +6,13 @@
 // bit-reproducible.  fp32 steps are evaluated exactly as written: no FMA
 // contraction in this file.
 #include "common.h"
+#include "controller_block.h"
 #include "internal.h"
 
 #pragma clang fp contract(off)
 
 namespace idb {
 
-// One workgroup, one expert per thread.  With a non-null stats pointer it
-// also writes MaxVio/MinVio of the same counts (as load_stats_kernel), so a
-// step needs one launch for both.
 __global__ __launch_bounds__(1024) void controller_update_kernel(const int32_t* __restrict__ counts, int E, int P,
                                                                  float Ki, float Kd, int sign_mode, int center,
                                                                  float* __restrict__ bias,
@@ -22,113 +20,8 @@ __global__ __launch_bounds__(1024) void controller_update_kernel(const int32_t* 
                                                                  int64_t* __restrict__ step,
                                                                  int32_t* __restrict__ status,
                                                                  double* __restrict__ stats) {
-    __shared__ long long w_sum[16];
-    __shared__ int w_max[16], w_min[16], w_neg[16];
-    __shared__ float tree[1024];
-    const int i = threadIdx.x;
-    const int lane = i & 63, wv = i >> 6, nw = blockDim.x >> 6;
-    const int n = (i < E) ? counts[i] : 0;
-    // Total assignments S = E * nbar (Eq. pid-error), and the largest and
-    // smallest count: exact integer reductions (order-free), across the wave
-    // by shuffles, then across the waves.
-    long long sum = n;
-    int mx = (i < E) ? n : INT32_MIN, mn = (i < E) ? n : INT32_MAX, neg = n < 0 ? 1 : 0;
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) {
-        sum += __shfl_xor(sum, o);
-        mx = max(mx, __shfl_xor(mx, o));
-        mn = min(mn, __shfl_xor(mn, o));
-        neg |= __shfl_xor(neg, o);
-    }
-    if (lane == 0) {
-        w_sum[wv] = sum;
-        w_max[wv] = mx;
-        w_min[wv] = mn;
-        w_neg[wv] = neg;
-    }
-    __syncthreads();
-    long long S = 0;
-    int any_negative = 0;
-    mx = INT32_MIN;
-    mn = INT32_MAX;
-    for (int w = 0; w < nw; ++w) {
-        S += w_sum[w];
-        mx = max(mx, w_max[w]);
-        mn = min(mn, w_min[w]);
-        any_negative |= w_neg[w];
-    }
-    if (stats && i == 0) {
-        // MaxVio, MinVio (Eq. vio): one fp64 division of an exact integer
-        // numerator each; NaN for an empty batch.
-        if (S == 0) {
-            stats[0] = __builtin_nan("");
-            stats[1] = __builtin_nan("");
-        } else {
-            stats[0] = (double)((long long)E * mx - S) / (double)S;
-            stats[1] = (double)(S - (long long)E * mn) / (double)S;
-        }
-    }
-    if (any_negative || S == 0) {
-        // Invalid or empty batch: report it and leave the state untouched.
-        if (i == 0) *status = any_negative ? kStatusInvalid : kStatusEmpty;
-        return;
-    }
-    float e = 0.0f, b = 0.0f;
-    if (i < E) {
-        // Normalised load error e = (nbar - n)/nbar = (S - E n)/S: exact integer
-        // numerator, one correctly rounded fp64 division, then fp32.
-        const long long num = S - (long long)E * (long long)n;
-        e = (float)((double)num / (double)S);
-        const float ep = e_prev[i];
-        const float de = e - ep;  // Eq. rapid-delta
-        // Worsening gate (Eq. rapid-gate) as a sign test: open iff the previous
-        // error and its change are both positive or both negative.
-        const bool g = (ep > 0.0f && de > 0.0f) || (ep < 0.0f && de < 0.0f);
-        float u;
-        if (sign_mode) {
-            const float sg = (e > 0.0f) ? 1.0f : ((e < 0.0f) ? -1.0f : 0.0f);
-            u = Ki * sg;  // DeepSeek fixed-step integral
-        } else {
-            u = Ki * e;  // magnitude-aware integral
-        }
-        b = bias[i] + u;
-        if (g) {
-            const float dterm = Kd * de;  // gated, accumulated derivative
-            b = b + dterm;
-        }
-    }
-    // Zero-mean centering (second line of Eq. rapid-update): fixed pairwise
-    // tree over b~ padded with +0 to P = next power of two >= E, level h
-    // adding a_{j+h} into a_j for j < h.  Levels h >= 64 go through LDS, the
-    // last six inside wave 0 by shuffles (same pairs, same order).
-    float m = 0.0f;
-    if (center) {
-        if (i < P) tree[i] = (i < E) ? b : 0.0f;
-        __syncthreads();
-        int h = P >> 1;
-        for (; h >= 64; h >>= 1) {
-            if (i < h) tree[i] = tree[i] + tree[i + h];
-            __syncthreads();
-        }
-        if (wv == 0) {
-            float a = (lane < P) ? tree[lane] : 0.0f;
-            for (; h >= 1; h >>= 1) {
-                const float up = __shfl_down(a, h);
-                if (lane < h) a = a + up;
-            }
-            if (lane == 0) tree[0] = a;
-        }
-        __syncthreads();
-        m = tree[0] / (float)E;
-    }
-    if (i < E) {
-        bias[i] = center ? (b - m) : b;
-        e_prev[i] = e;
-    }
-    if (i == 0) {
-        *step = *step + 1;
-        *status = kStatusOk;
-    }
+    __shared__ CtrlScratch sh;
+    controller_block(counts, E, P, Ki, Kd, sign_mode, center, bias, e_prev, step, status, stats, sh);
 }
 
 // MaxVio = (E max n - S)/S, MinVio = (S - E min n)/S (Eq. vio), one fp64
@@ -174,8 +67,7 @@ __global__ __launch_bounds__(1024) void load_stats_kernel(const int32_t* __restr
 hipError_t launch_controller_update(const int32_t* counts, int E, float Ki, float Kd, int sign_mode, int center,
                                     float* bias, float* e_prev, int64_t* step, int32_t* status, double* stats,
                                     hipStream_t stream) {
-    int P = 1;
-    while (P < E) P <<= 1;
+    const int P = ctrl_tree_size(E);
     const int threads = P < 64 ? 64 : P;
     hipLaunchKernelGGL(controller_update_kernel, dim3(1), dim3(threads), 0, stream, counts, E, P, Ki, Kd,
                        sign_mode, center, bias, e_prev, step, status, stats);

@@ -1,0 +1,164 @@
+// The ID bias controller update (Algorithm 1, Eq. rapid-update) and the load
+// statistics (Eq. vio) as a device function run by one workgroup; shared by
+// the stand-alone controller kernel and the router tail that runs it after the
+// last slice-merge workgroup.
+#pragma once
+
+#include "common.h"
+
+namespace idb {
+
+// LDS scratch of controller_block.
+struct CtrlScratch {
+    long long w_sum[16];
+    int w_max[16], w_min[16], w_neg[16];
+    float tree[1024];
+};
+
+// Leaves of the centering tree: the next power of two >= E.
+__host__ __device__ inline int ctrl_tree_size(int E) {
+    int P = 1;
+    while (P < E) P <<= 1;
+    return P;
+}
+
+// The whole O(E) update on one workgroup of any size that is a multiple of 64
+// (each thread takes experts i, i + blockDim, ...; E <= 1024).  With a
+// non-null stats pointer it also writes MaxVio/MinVio of the same counts.
+// Reductions: exact integer sums/extrema across waves (order-free); the
+// centering mean with the fixed pairwise tree (level h adds a_{j+h} into a_j
+// for j < h, P = next power of two >= E), levels h >= 64 in LDS, the last
+// six inside wave 0 by shuffles (same pairs, same order).
+__device__ inline void controller_block(const int32_t* __restrict__ counts, int E, int P, float Ki, float Kd, int sign_mode,
+                                 int center, float* __restrict__ bias, float* __restrict__ e_prev,
+                                 int64_t* __restrict__ step, int32_t* __restrict__ status,
+                                 double* __restrict__ stats, CtrlScratch& sh) {
+#pragma clang fp contract(off)
+    constexpr int kPer = 1024 / 64;  // experts per thread at the smallest block
+    const int i0 = threadIdx.x, nt = blockDim.x;
+    const int lane = i0 & 63, wv = i0 >> 6, nw = nt >> 6;
+    int n[kPer];
+    long long sum = 0;
+    int mx = INT32_MIN, mn = INT32_MAX, neg = 0;
+#pragma unroll
+    for (int q = 0; q < kPer; ++q) {
+        const int i = i0 + q * nt;
+        n[q] = (i < E) ? counts[i] : 0;
+        if (i < E) {
+            sum += n[q];
+            mx = max(mx, n[q]);
+            mn = min(mn, n[q]);
+            neg |= n[q] < 0 ? 1 : 0;
+        }
+    }
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) {
+        sum += __shfl_xor(sum, o);
+        mx = max(mx, __shfl_xor(mx, o));
+        mn = min(mn, __shfl_xor(mn, o));
+        neg |= __shfl_xor(neg, o);
+    }
+    if (lane == 0) {
+        sh.w_sum[wv] = sum;
+        sh.w_max[wv] = mx;
+        sh.w_min[wv] = mn;
+        sh.w_neg[wv] = neg;
+    }
+    __syncthreads();
+    // Total assignments S = E * nbar (Eq. pid-error).
+    long long S = 0;
+    int any_negative = 0;
+    mx = INT32_MIN;
+    mn = INT32_MAX;
+    for (int w = 0; w < nw; ++w) {
+        S += sh.w_sum[w];
+        mx = max(mx, sh.w_max[w]);
+        mn = min(mn, sh.w_min[w]);
+        any_negative |= sh.w_neg[w];
+    }
+    if (stats && i0 == 0) {
+        // MaxVio, MinVio (Eq. vio): one fp64 division of an exact integer
+        // numerator each; NaN for an empty batch.
+        if (S == 0) {
+            stats[0] = __builtin_nan("");
+            stats[1] = __builtin_nan("");
+        } else {
+            stats[0] = (double)((long long)E * mx - S) / (double)S;
+            stats[1] = (double)(S - (long long)E * mn) / (double)S;
+        }
+    }
+    if (any_negative || S == 0) {
+        // Invalid or empty batch: report it and leave the state untouched.
+        if (i0 == 0) *status = any_negative ? kStatusInvalid : kStatusEmpty;
+        return;
+    }
+    float e[kPer], b[kPer];
+#pragma unroll
+    for (int q = 0; q < kPer; ++q) {
+        const int i = i0 + q * nt;
+        e[q] = 0.0f;
+        b[q] = 0.0f;
+        if (i < E) {
+            // Normalised load error e = (nbar - n)/nbar = (S - E n)/S: exact
+            // integer numerator, one correctly rounded fp64 division, then fp32.
+            const long long num = S - (long long)E * (long long)n[q];
+            e[q] = (float)((double)num / (double)S);
+            const float ep = e_prev[i];
+            const float de = e[q] - ep;  // Eq. rapid-delta
+            // Worsening gate (Eq. rapid-gate) as a sign test: open iff the
+            // previous error and its change are both positive or both negative.
+            const bool g = (ep > 0.0f && de > 0.0f) || (ep < 0.0f && de < 0.0f);
+            float u;
+            if (sign_mode) {
+                const float sg = (e[q] > 0.0f) ? 1.0f : ((e[q] < 0.0f) ? -1.0f : 0.0f);
+                u = Ki * sg;  // DeepSeek fixed-step integral
+            } else {
+                u = Ki * e[q];  // magnitude-aware integral
+            }
+            b[q] = bias[i] + u;
+            if (g) {
+                const float dterm = Kd * de;  // gated, accumulated derivative
+                b[q] = b[q] + dterm;
+            }
+        }
+    }
+    // Zero-mean centering (second line of Eq. rapid-update).
+    float m = 0.0f;
+    if (center) {
+#pragma unroll
+        for (int q = 0; q < kPer; ++q) {
+            const int i = i0 + q * nt;
+            if (i < P) sh.tree[i] = (i < E) ? b[q] : 0.0f;
+        }
+        __syncthreads();
+        int h = P >> 1;
+        for (; h >= 64; h >>= 1) {
+            for (int i = i0; i < h; i += nt) sh.tree[i] = sh.tree[i] + sh.tree[i + h];
+            __syncthreads();
+        }
+        if (wv == 0) {
+            float a = (lane < P) ? sh.tree[lane] : 0.0f;
+            for (; h >= 1; h >>= 1) {
+                const float up = __shfl_down(a, h);
+                if (lane < h) a = a + up;
+            }
+            if (lane == 0) sh.tree[0] = a;
+        }
+        __syncthreads();
+        m = sh.tree[0] / (float)E;
+    }
+#pragma unroll
+    for (int q = 0; q < kPer; ++q) {
+        const int i = i0 + q * nt;
+        if (i < E) {
+            bias[i] = center ? (b[q] - m) : b[q];
+            e_prev[i] = e[q];
+        }
+    }
+    if (i0 == 0) {
+        *step = *step + 1;
+        *status = kStatusOk;
+    }
+}
+
+}  // namespace idb

@@ -709,16 +709,16 @@ __global__ __launch_bounds__(WAVES * 64) void router16_kernel(RouterArgs a, int 
                 for (int et = 0; et < ET; ++et) w[j][et][s] = bload16(wres, wvoff + WS * s, wsoff[et] + cn * WCH);
             }
         }
-        // Schedule: half 0's eight B-operand reads, then its MFMAs with half
-        // 1's reads interleaved one per three MFMAs, then half 1's MFMAs, so
-        // no group of MFMAs waits for a fresh LDS read.
-        __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);  // LDS reads
+        // Schedule: half 0's TT B-operand reads, then its MFMAs with half 1's
+        // reads interleaved one per ET MFMAs, then half 1's MFMAs, so no
+        // group of MFMAs waits for a fresh LDS read.
+        __builtin_amdgcn_sched_group_barrier(0x100, TT, 0);  // LDS reads
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            __builtin_amdgcn_sched_group_barrier(0x008, 3, 0);  // MFMA
+        for (int i = 0; i < TT; ++i) {
+            __builtin_amdgcn_sched_group_barrier(0x008, ET, 0);  // MFMA
             __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
         }
-        __builtin_amdgcn_sched_group_barrier(0x008, 24, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, TT * ET, 0);
     };
 
     const int last = NCH - 1;
