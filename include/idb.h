@@ -209,6 +209,26 @@ idb_status idb_load_stats(const int32_t* counts, int32_t E, double* out_maxvio_m
 idb_status idb_controller_step(const int32_t* counts, const idb_controller_cfg* cfg,
                                const idb_controller_state* state, double* out_maxvio_minvio, hipStream_t stream);
 
+/* ---------------------------------------------------------------------------
+ * One whole iteration of Alg. 1 for one batch and one MoE layer: the router
+ * step with bias = state->bias (frozen while routing), then, once every token
+ * is counted, MaxVio/MinVio of counts (when out_maxvio_minvio is not null)
+ * and the ID update of state from counts.  The results are exactly those of
+ * idb_router_forward (scores_dump = NULL) followed by idb_controller_step (or
+ * idb_controller_update) on the same stream; E is cfg->E, the other arguments
+ * as for those calls, with the same workspace size.  With accumulate_counts
+ * the update uses the accumulated counts (the last microbatch of an
+ * iteration).  Two launches for multi-slice tilings: the fused router kernel,
+ * then the slice merge, whose last workgroup to finish applies the update.
+ * The workspace must not be shared with a call still running on another
+ * stream.
+ * ------------------------------------------------------------------------- */
+idb_status idb_router_step(const void* x, const void* W_g, idb_dtype dtype, idb_weight_layout weight_layout,
+                           int64_t T, int32_t d, int32_t K, const idb_controller_cfg* cfg,
+                           const idb_controller_state* state, int32_t* expert_idx, float* gate_w, int32_t* counts,
+                           int32_t accumulate_counts, double* out_maxvio_minvio, void* workspace,
+                           size_t workspace_bytes, int32_t variant, hipStream_t stream);
+
 /* Static description of a status code; message of the last failing call on
  * this thread (empty string if none). */
 const char* idb_status_string(idb_status s);

@@ -33,7 +33,7 @@ EXPORTED = (
     "idb_router_workspace_bytes", "idb_router_forward", "idb_router_score_select", "idb_router_merge",
     "idb_router_variant_info", "idb_select_from_scores", "idb_controller_update", "idb_load_stats",
     "idb_status_string", "idb_last_error", "idb_router_packed_weight_bytes", "idb_router_pack_weight",
-    "idb_controller_step",
+    "idb_controller_step", "idb_router_step",
 )
 
 
@@ -88,6 +88,9 @@ def lib() -> ctypes.CDLL:
     L.idb_controller_step.argtypes = [P, ctypes.POINTER(idb_controller_cfg), ctypes.POINTER(idb_controller_state), P,
                                       P]
     L.idb_controller_step.restype = ctypes.c_int
+    L.idb_router_step.argtypes = [P, P, i32, i32, i64, i32, i32, ctypes.POINTER(idb_controller_cfg),
+                                  ctypes.POINTER(idb_controller_state), P, P, P, i32, P, P, sz, i32, P]
+    L.idb_router_step.restype = ctypes.c_int
     L.idb_status_string.argtypes = [ctypes.c_int]
     L.idb_status_string.restype = ctypes.c_char_p
     L.idb_last_error.argtypes = []
@@ -258,3 +261,25 @@ def idb_controller_step(counts, cfg: ControllerCfg, state: ControllerState, out,
     st = lib().idb_controller_step(_ptr(counts), ctypes.byref(c_cfg), ctypes.byref(c_state), _ptr(out),
                                    _stream(stream))
     _check("idb_controller_step", st)
+
+
+def idb_router_step(x, W_g, K, cfg: ControllerCfg, state: ControllerState, expert_idx, gate_w, counts,
+                    accumulate=False, out=None, workspace=None, variant=0, stream=None,
+                    weight_layout=IDB_WEIGHT_ROW_MAJOR):
+    """One iteration for one batch: route with ``state.bias``, then MaxVio/MinVio into ``out`` (optional)
+    and the ID update of ``state`` from the finished ``counts``."""
+    T, d = x.shape
+    E = cfg.E
+    if W_g.shape != (E, d) or W_g.dtype != x.dtype or state.bias.shape != (E,):
+        raise ValueError("router operands disagree in shape or dtype")
+    if expert_idx.shape != (T, K) or gate_w.shape != (T, K) or counts.shape != (E,):
+        raise ValueError("router outputs have the wrong shape")
+    if out is not None and (out.dtype != torch.float64 or out.numel() != 2):
+        raise ValueError("out must be a float64 tensor of 2 elements")
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    c_cfg, c_state = cfg.c(), state.c()
+    st = lib().idb_router_step(_ptr(x), _ptr(W_g), _dtype_code(x), int(weight_layout), T, d, K, ctypes.byref(c_cfg),
+                               ctypes.byref(c_state), _ptr(expert_idx), _ptr(gate_w), _ptr(counts),
+                               int(bool(accumulate)), _ptr(out), _ptr(workspace), ws_bytes, int(variant),
+                               _stream(stream))
+    _check("idb_router_step", st)

@@ -89,13 +89,14 @@ idb_status check_router_shape(int64_t T, int32_t d, int32_t E, int32_t K, idb_dt
 size_t router_ws_bytes(int64_t T, int32_t E, int32_t K, const idb::RouterTiling& t) {
     const int ns = idb::router_slices(t, E);
     if (ns <= 1) return 0;
-    // candidates (value, score, index) [T][ns][K]
-    return 3 * round_up((size_t)T * ns * K * 4);
+    // candidates (value, score, index) [T][ns][K], then the merge's ticket
+    return 3 * round_up((size_t)T * ns * K * 4) + 256;
 }
 
 struct RouterCall {
     idb::RouterTiling tiling;
     idb::RouterArgs args;
+    unsigned* ticket;  // the merge's ticket in the workspace (multi-slice tilings)
 };
 
 idb_status prepare_router(const void* x, const void* W_g, idb_dtype dtype, idb_weight_layout layout,
@@ -145,6 +146,8 @@ idb_status prepare_router(const void* x, const void* W_g, idb_dtype dtype, idb_w
     a.cand_v = need ? reinterpret_cast<float*>(ws) : nullptr;
     a.cand_s = need ? reinterpret_cast<float*>(ws + part) : nullptr;
     a.cand_i = need ? reinterpret_cast<int32_t*>(ws + 2 * part) : nullptr;
+    a.ticket = nullptr;
+    call->ticket = need ? reinterpret_cast<unsigned*>(ws + 3 * part) : nullptr;
     return IDB_OK;
 }
 
@@ -202,7 +205,7 @@ idb_status idb_router_merge(int64_t T, int32_t d, int32_t E, int32_t K, idb_dtyp
     idb_status st = prepare_router(nullptr, nullptr, dtype, IDB_WEIGHT_ROW_MAJOR, nullptr, T, d, E, K, expert_idx, gate_w, counts, 1,
                                    nullptr, workspace, workspace_bytes, variant, false, &c);
     if (st != IDB_OK) return st;
-    return hip_result(idb::launch_router_merge(c.tiling, c.args, stream), "router merge launch");
+    return hip_result(idb::launch_router_merge(c.tiling, c.args, nullptr, stream), "router merge launch");
 }
 
 idb_status idb_router_forward(const void* x, const void* W_g, idb_dtype dtype, idb_weight_layout weight_layout,
@@ -215,7 +218,7 @@ idb_status idb_router_forward(const void* x, const void* W_g, idb_dtype dtype, i
     if (st != IDB_OK) return st;
     st = enqueue_score_select(c, accumulate_counts, stream);
     if (st != IDB_OK) return st;
-    return hip_result(idb::launch_router_merge(c.tiling, c.args, stream), "router merge launch");
+    return hip_result(idb::launch_router_merge(c.tiling, c.args, nullptr, stream), "router merge launch");
 }
 
 size_t idb_router_packed_weight_bytes(int32_t E, int32_t d, idb_dtype dtype) {
@@ -257,9 +260,8 @@ idb_status idb_select_from_scores(const float* scores, const float* bias, int64_
 }
 
 namespace {
-idb_status controller_call(const int32_t* counts, const idb_controller_cfg* cfg, const idb_controller_state* state,
-                           double* stats, hipStream_t stream) {
-    if (!counts || !cfg || !state) return fail(IDB_ERR_INVALID_ARG, "null pointer");
+idb_status check_controller(const idb_controller_cfg* cfg, const idb_controller_state* state, const double* stats) {
+    if (!cfg || !state) return fail(IDB_ERR_INVALID_ARG, "null pointer");
     if (!state->bias || !state->e_prev || !state->step || !state->status)
         return fail(IDB_ERR_INVALID_ARG, "null state buffer");
     if (cfg->E < 1 || cfg->E > kMaxExperts) return fail(IDB_ERR_INVALID_ARG, "E=%d out of [1, 1024]", cfg->E);
@@ -268,14 +270,28 @@ idb_status controller_call(const int32_t* counts, const idb_controller_cfg* cfg,
     if (cfg->integral_mode != IDB_INTEGRAL_ERROR && cfg->integral_mode != IDB_INTEGRAL_SIGN)
         return fail(IDB_ERR_INVALID_ARG, "unknown integral mode %d", cfg->integral_mode);
     if (cfg->center != 0 && cfg->center != 1) return fail(IDB_ERR_INVALID_ARG, "center must be 0 or 1");
-    if (!aligned(counts, 4) || !aligned(state->bias, 4) || !aligned(state->e_prev, 4) || !aligned(state->step, 8) ||
+    if (!aligned(state->bias, 4) || !aligned(state->e_prev, 4) || !aligned(state->step, 8) ||
         !aligned(state->status, 4) || (stats && !aligned(stats, 8)))
         return fail(IDB_ERR_INVALID_ARG, "misaligned buffer");
+    return IDB_OK;
+}
+
+idb_status enqueue_controller(const int32_t* counts, const idb_controller_cfg* cfg, const idb_controller_state* state,
+                              double* stats, hipStream_t stream) {
     return hip_result(idb::launch_controller_update(counts, cfg->E, cfg->Ki, cfg->Kd,
                                                     cfg->integral_mode == IDB_INTEGRAL_SIGN, cfg->center,
                                                     state->bias, state->e_prev, state->step, state->status, stats,
                                                     stream),
                       "controller launch");
+}
+
+idb_status controller_call(const int32_t* counts, const idb_controller_cfg* cfg, const idb_controller_state* state,
+                           double* stats, hipStream_t stream) {
+    if (!counts) return fail(IDB_ERR_INVALID_ARG, "null pointer");
+    idb_status st = check_controller(cfg, state, stats);
+    if (st != IDB_OK) return st;
+    if (!aligned(counts, 4)) return fail(IDB_ERR_INVALID_ARG, "misaligned buffer");
+    return enqueue_controller(counts, cfg, state, stats, stream);
 }
 }  // namespace
 
@@ -288,6 +304,40 @@ idb_status idb_controller_step(const int32_t* counts, const idb_controller_cfg* 
                                const idb_controller_state* state, double* out_maxvio_minvio, hipStream_t stream) {
     if (!out_maxvio_minvio) return fail(IDB_ERR_INVALID_ARG, "null statistics output");
     return controller_call(counts, cfg, state, out_maxvio_minvio, stream);
+}
+
+idb_status idb_router_step(const void* x, const void* W_g, idb_dtype dtype, idb_weight_layout weight_layout,
+                           int64_t T, int32_t d, int32_t K, const idb_controller_cfg* cfg,
+                           const idb_controller_state* state, int32_t* expert_idx, float* gate_w, int32_t* counts,
+                           int32_t accumulate_counts, double* out_maxvio_minvio, void* workspace,
+                           size_t workspace_bytes, int32_t variant, hipStream_t stream) {
+    idb_status st = check_controller(cfg, state, out_maxvio_minvio);
+    if (st != IDB_OK) return st;
+    RouterCall c;
+    st = prepare_router(x, W_g, dtype, weight_layout, state->bias, T, d, cfg->E, K, expert_idx, gate_w, counts,
+                        accumulate_counts, nullptr, workspace, workspace_bytes, variant, true, &c);
+    if (st != IDB_OK) return st;
+    if (!c.ticket) {
+        // one-slice tiling: the router kernel finishes the counts itself
+        st = enqueue_score_select(c, accumulate_counts, stream);
+        if (st != IDB_OK) return st;
+        return enqueue_controller(counts, cfg, state, out_maxvio_minvio, stream);
+    }
+    c.args.ticket = c.ticket;
+    st = enqueue_score_select(c, accumulate_counts, stream);
+    if (st != IDB_OK) return st;
+    idb::CtrlArgs k;
+    k.Ki = cfg->Ki;
+    k.Kd = cfg->Kd;
+    k.sign_mode = cfg->integral_mode == IDB_INTEGRAL_SIGN;
+    k.center = cfg->center;
+    k.bias = state->bias;
+    k.e_prev = state->e_prev;
+    k.step = state->step;
+    k.status = state->status;
+    k.stats = out_maxvio_minvio;
+    k.ticket = c.ticket;
+    return hip_result(idb::launch_router_merge(c.tiling, c.args, &k, stream), "router merge launch");
 }
 
 idb_status idb_load_stats(const int32_t* counts, int32_t E, double* out_maxvio_minvio, hipStream_t stream) {

@@ -21,7 +21,7 @@ __global__ __launch_bounds__(1024) void controller_update_kernel(const int32_t* 
                                                                  int32_t* __restrict__ status,
                                                                  double* __restrict__ stats) {
     __shared__ CtrlScratch sh;
-    controller_block(counts, E, P, Ki, Kd, sign_mode, center, bias, e_prev, step, status, stats, sh);
+    controller_block<1>(counts, E, P, Ki, Kd, sign_mode, center, bias, e_prev, step, status, stats, sh);
 }
 
 // MaxVio = (E max n - S)/S, MinVio = (S - E min n)/S (Eq. vio), one fp64

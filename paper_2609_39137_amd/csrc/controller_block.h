@@ -22,28 +22,37 @@ __host__ __device__ inline int ctrl_tree_size(int E) {
     return P;
 }
 
-// The whole O(E) update on one workgroup of any size that is a multiple of 64
-// (each thread takes experts i, i + blockDim, ...; E <= 1024).  With a
+// The whole O(E) update on one workgroup whose size is a multiple of 64, each
+// thread taking experts i, i + blockDim, ... (kPer of them): needs
+// kPer * blockDim >= P, the centering tree's size below, and E <= 1024.  With a
 // non-null stats pointer it also writes MaxVio/MinVio of the same counts.
 // Reductions: exact integer sums/extrema across waves (order-free); the
 // centering mean with the fixed pairwise tree (level h adds a_{j+h} into a_j
 // for j < h, P = next power of two >= E), levels h >= 64 in LDS, the last
 // six inside wave 0 by shuffles (same pairs, same order).
-__device__ inline void controller_block(const int32_t* __restrict__ counts, int E, int P, float Ki, float Kd, int sign_mode,
-                                 int center, float* __restrict__ bias, float* __restrict__ e_prev,
-                                 int64_t* __restrict__ step, int32_t* __restrict__ status,
-                                 double* __restrict__ stats, CtrlScratch& sh) {
+template <int kPer, bool kCoherentCounts = false>
+__device__ inline void controller_block(const int32_t* __restrict__ counts, int E, int P, float Ki, float Kd,
+                                        int sign_mode, int center, float* __restrict__ bias,
+                                        float* __restrict__ e_prev, int64_t* __restrict__ step,
+                                        int32_t* __restrict__ status, double* __restrict__ stats,
+                                        CtrlScratch& sh) {
 #pragma clang fp contract(off)
-    constexpr int kPer = 1024 / 64;  // experts per thread at the smallest block
     const int i0 = threadIdx.x, nt = blockDim.x;
     const int lane = i0 & 63, wv = i0 >> 6, nw = nt >> 6;
     int n[kPer];
+    float b0[kPer], ep0[kPer];  // state, loaded together with the counts
     long long sum = 0;
     int mx = INT32_MIN, mn = INT32_MAX, neg = 0;
 #pragma unroll
     for (int q = 0; q < kPer; ++q) {
         const int i = i0 + q * nt;
-        n[q] = (i < E) ? counts[i] : 0;
+        // counts written by atomics of other workgroups of the same launch
+        // are read with agent-scope loads.
+        n[q] = (i >= E) ? 0
+               : kCoherentCounts ? __hip_atomic_load(counts + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
+                                 : counts[i];
+        b0[q] = (i < E) ? bias[i] : 0.0f;
+        ep0[q] = (i < E) ? e_prev[i] : 0.0f;
         if (i < E) {
             sum += n[q];
             mx = max(mx, n[q]);
@@ -103,7 +112,7 @@ __device__ inline void controller_block(const int32_t* __restrict__ counts, int 
             // integer numerator, one correctly rounded fp64 division, then fp32.
             const long long num = S - (long long)E * (long long)n[q];
             e[q] = (float)((double)num / (double)S);
-            const float ep = e_prev[i];
+            const float ep = ep0[q];
             const float de = e[q] - ep;  // Eq. rapid-delta
             // Worsening gate (Eq. rapid-gate) as a sign test: open iff the
             // previous error and its change are both positive or both negative.
@@ -115,7 +124,7 @@ __device__ inline void controller_block(const int32_t* __restrict__ counts, int 
             } else {
                 u = Ki * e[q];  // magnitude-aware integral
             }
-            b[q] = bias[i] + u;
+            b[q] = b0[q] + u;
             if (g) {
                 const float dterm = Kd * de;  // gated, accumulated derivative
                 b[q] = b[q] + dterm;
@@ -159,6 +168,31 @@ __device__ inline void controller_block(const int32_t* __restrict__ counts, int 
         *step = *step + 1;
         *status = kStatusOk;
     }
+}
+
+// Run by every thread of each workgroup of a launch once it is done with
+// counts: the workgroup that finishes last (ticket) runs controller_block on
+// the complete counts.  Every wave first waits for its own memory operations
+// (the count atomics) to complete; after the barrier one thread's agent-scope
+// release fence publishes the workgroup's writes before its ticket increment
+// (one L2 write-back per workgroup, not per wave), and the last workgroup's
+// acquire fence orders the ticket before its count reads.
+template <int kPer>
+__device__ inline void controller_tail(const int32_t* counts, int E, float Ki, float Kd, int sign_mode, int center,
+                                       float* bias, float* e_prev, int64_t* step, int32_t* status, double* stats,
+                                       unsigned* ticket, CtrlScratch& sh) {
+    __shared__ int last;
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+        last = __hip_atomic_fetch_add(ticket, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == gridDim.x - 1;
+    }
+    __syncthreads();
+    if (!last) return;
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+    controller_block<kPer, true>(counts, E, ctrl_tree_size(E), Ki, Kd, sign_mode, center, bias, e_prev, step, status,
+                           stats, sh);
 }
 
 }  // namespace idb

@@ -46,6 +46,7 @@ struct RouterArgs {
     float* w;
     int32_t* counts;
     int zero_counts;  // workgroup 0 of the multi-slice kernel zeroes counts
+    unsigned* ticket;  // nullable; workgroup 0 of the multi-slice kernel zeroes it
     float* dump;
     // multi-slice candidates in the workspace: [T][slices][K]
     float* cand_v;
@@ -59,8 +60,25 @@ inline int router_slices(const RouterTiling& t, int E) {
     return (E + be - 1) / be;
 }
 
+// Controller update run by the last workgroup of the slice merge (after every
+// other workgroup has flushed its counts); the ticket counts finished
+// workgroups and must be zero at the merge launch.
+struct CtrlArgs {
+    float Ki, Kd;
+    int sign_mode, center;
+    float* bias;
+    float* e_prev;
+    int64_t* step;
+    int32_t* status;
+    double* stats;  // nullable
+    unsigned* ticket;
+};
+
 hipError_t launch_router_score_select(const RouterTiling& t, const RouterArgs& a, hipStream_t stream);
-hipError_t launch_router_merge(const RouterTiling& t, const RouterArgs& a, hipStream_t stream);
+// ctrl: nullable; with it, the merge also runs the controller update on the
+// finished counts (multi-slice tilings only).
+hipError_t launch_router_merge(const RouterTiling& t, const RouterArgs& a, const CtrlArgs* ctrl,
+                               hipStream_t stream);
 // Router matrix [E][d] (row_bytes per row) -> the packed A-operand layout.
 hipError_t launch_pack_weight(const void* W, void* P, int E, int64_t row_bytes, hipStream_t stream);
 

@@ -52,6 +52,7 @@
 //      atomic per non-zero bin.  Several slices: the slice's K candidates go
 //      to the workspace and router_merge_kernel combines them.
 #include "common.h"
+#include "controller_block.h"
 #include "internal.h"
 
 #pragma clang fp contract(off)
@@ -439,6 +440,7 @@ __global__ __launch_bounds__(WAVES * 64) void router32_kernel(RouterArgs a, int 
 
     if (a.zero_counts && blockIdx.x == 0)
         for (int e = tid; e < E; e += C::NT) a.counts[e] = 0;
+    if (a.ticket && blockIdx.x == 0 && tid == 0) *a.ticket = 0u;
     const int sbase = slice * C::BE;
     float breg[EC::NBIAS];
     prefetch_bias<EC>(a, sbase, breg);
@@ -629,6 +631,7 @@ __global__ __launch_bounds__(WAVES * 64) void router16_kernel(RouterArgs a, int 
 
     if (a.zero_counts && blockIdx.x == 0)
         for (int e = tid; e < E; e += C::NT) a.counts[e] = 0;
+    if (a.ticket && blockIdx.x == 0 && tid == 0) *a.ticket = 0u;
     const int sbase = slice * C::BE;
     float breg[EC::NBIAS];
     prefetch_bias<EC>(a, sbase, breg);
@@ -781,7 +784,7 @@ __global__ __launch_bounds__(WAVES * 64) void router16_kernel(RouterArgs a, int 
 constexpr int kMergeThreads = 256;
 constexpr int kMergeBlocks = 512;
 
-__global__ __launch_bounds__(kMergeThreads) void router_merge_kernel(RouterArgs a, int NS) {
+__global__ __launch_bounds__(kMergeThreads) void router_merge_kernel(RouterArgs a, int NS, CtrlArgs c) {
     __shared__ int hist[1024];
     __shared__ unsigned long long key[kMergeThreads];
     __shared__ float sel[kMergeThreads];  // selected scores, [token of the group][rank]
@@ -831,6 +834,11 @@ __global__ __launch_bounds__(kMergeThreads) void router_merge_kernel(RouterArgs 
     }
     __syncthreads();
     flush_hist(hist, a.counts, E);
+    if (c.ticket) {
+        __shared__ CtrlScratch csh;
+        controller_tail<1024 / kMergeThreads>(a.counts, E, c.Ki, c.Kd, c.sign_mode, c.center, c.bias, c.e_prev,
+                                          c.step, c.status, c.stats, c.ticket, csh);
+    }
 }
 
 // Merge by token tile (NS*K <= 64): a few workgroups walk the 128-token tiles
@@ -845,7 +853,7 @@ constexpr int kTileThreads = 512;
 constexpr int kTileTokens = 128;
 constexpr int kTileBlocks = 4096;
 
-__global__ __launch_bounds__(kTileThreads) void router_merge_tile_kernel(RouterArgs a, int NS) {
+__global__ __launch_bounds__(kTileThreads) void router_merge_tile_kernel(RouterArgs a, int NS, CtrlArgs c) {
     __shared__ int hist[1024];
     __shared__ unsigned long long mk[kTileTokens * 64];
     __shared__ float ms[kTileTokens * 64];
@@ -926,6 +934,11 @@ __global__ __launch_bounds__(kTileThreads) void router_merge_tile_kernel(RouterA
     }
     __syncthreads();
     flush_hist(hist, a.counts, E);
+    if (c.ticket) {
+        __shared__ CtrlScratch csh;
+        controller_tail<1024 / kTileThreads>(a.counts, E, c.Ki, c.Kd, c.sign_mode, c.center, c.bias, c.e_prev,
+                                          c.step, c.status, c.stats, c.ticket, csh);
+    }
 }
 
 // Router matrix [E][d] -> packed layout: output piece p (16 bytes) = lane
@@ -996,19 +1009,23 @@ hipError_t launch_router_score_select(const RouterTiling& t, const RouterArgs& a
     return a.w_packed ? launch_layout<true>(t, a, NS, stream) : launch_layout<false>(t, a, NS, stream);
 }
 
-hipError_t launch_router_merge(const RouterTiling& t, const RouterArgs& a, hipStream_t stream) {
+hipError_t launch_router_merge(const RouterTiling& t, const RouterArgs& a, const CtrlArgs* ctrl,
+                               hipStream_t stream) {
     const int NS = router_slices(t, a.E);
     if (NS <= 1) return hipSuccess;
+    CtrlArgs c{};
+    if (ctrl) c = *ctrl;
     if (NS * a.K <= 64) {
         int64_t blocks = (a.T + kTileTokens - 1) / kTileTokens;
         if (blocks > kTileBlocks) blocks = kTileBlocks;
-        hipLaunchKernelGGL(router_merge_tile_kernel, dim3((unsigned)blocks), dim3(kTileThreads), 0, stream, a, NS);
+        hipLaunchKernelGGL(router_merge_tile_kernel, dim3((unsigned)blocks), dim3(kTileThreads), 0, stream, a, NS,
+                           c);
         return hipGetLastError();
     }
     const int tpg = kMergeThreads / (NS * a.K);
     int64_t groups = (a.T + tpg - 1) / tpg;
     if (groups > kMergeBlocks) groups = kMergeBlocks;
-    hipLaunchKernelGGL(router_merge_kernel, dim3((unsigned)groups), dim3(kMergeThreads), 0, stream, a, NS);
+    hipLaunchKernelGGL(router_merge_kernel, dim3((unsigned)groups), dim3(kMergeThreads), 0, stream, a, NS, c);
     return hipGetLastError();
 }
 

@@ -70,7 +70,9 @@ class RouterStep:
         """MaxVio/MinVio of this step's counts and the bias update, one launch."""
         B.idb_controller_step(self.counts, self.cfg, self.state, self.stats, stream)
 
-    def step(self, x, W=None, stream=None):
-        """Route, then compute MaxVio/MinVio and update the bias (all asynchronous)."""
-        self.route(x, W, stream=stream)
-        self.update_and_stats(stream)
+    def step(self, x, W=None, accumulate: bool = False, stream=None):
+        """Route, then compute MaxVio/MinVio and update the bias (all asynchronous; the update runs in
+        the slice merge's last workgroup when the tiling has several slices)."""
+        Wt, layout = self._weights(W)
+        B.idb_router_step(x, Wt, self.K, self.cfg, self.state, self.idx, self.w, self.counts, accumulate,
+                          self.stats, self.workspace, self.variant, stream, layout)

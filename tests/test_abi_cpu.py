@@ -94,8 +94,9 @@ def test_workspace_and_variant_info():
     # slices' candidates are staged in the workspace.
     info = B.idb_router_variant_info(16384, 2048, 768, 10, B.IDB_DTYPE_BF16, 0)
     assert info == {"tokens_per_wg": 128, "slices": 2, "waves": 8, "experts_per_wave": 48, "variant": 6}
-    # candidates (value, score, index) per token, slice and rank
-    assert B.idb_router_workspace_bytes(16384, 2048, 768, 10, B.IDB_DTYPE_BF16, 0) == 3 * 16384 * 2 * 10 * 4
+    # candidates (value, score, index) per token, slice and rank, then 256
+    # bytes for the merge's ticket
+    assert B.idb_router_workspace_bytes(16384, 2048, 768, 10, B.IDB_DTYPE_BF16, 0) == 3 * 16384 * 2 * 10 * 4 + 256
     # a single 768-expert slice needs no workspace
     info2 = B.idb_router_variant_info(16384, 2048, 768, 10, B.IDB_DTYPE_BF16, 2)
     assert info2["slices"] == 1 and info2["tokens_per_wg"] == 64 and info2["experts_per_wave"] == 96
@@ -150,6 +151,38 @@ def test_controller_rejects_invalid_arguments(cfg, state, code):
     ccfg = B.idb_controller_cfg(c["E"], c["Ki"], c["Kd"], c["integral_mode"], c["center"])
     st = B.lib().idb_controller_update(A16, ctypes.byref(ccfg), ctypes.byref(_state(**state)), None)
     assert st == code
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(cfg=None), B.IDB_ERR_INVALID_ARG),
+    (dict(state=None), B.IDB_ERR_INVALID_ARG),
+    (dict(E=0), B.IDB_ERR_INVALID_ARG),
+    (dict(Ki=-1.0), B.IDB_ERR_INVALID_ARG),
+    (dict(center=3), B.IDB_ERR_INVALID_ARG),
+    (dict(bias=None), B.IDB_ERR_INVALID_ARG),
+    (dict(bias=A16 + 2), B.IDB_ERR_INVALID_ARG),
+    (dict(stats=A16 + 4), B.IDB_ERR_INVALID_ARG),
+    (dict(T=0), B.IDB_ERR_INVALID_ARG),
+    (dict(K=0), B.IDB_ERR_INVALID_ARG),
+    (dict(x=None), B.IDB_ERR_INVALID_ARG),
+    (dict(counts=None), B.IDB_ERR_INVALID_ARG),
+    (dict(ws=None, variant=6), B.IDB_ERR_INVALID_ARG),
+    (dict(ws_bytes=3 * 128 * 2 * 10 * 4, variant=6), B.IDB_ERR_INVALID_ARG),  # no room for the ticket
+    (dict(E=100), B.IDB_ERR_UNSUPPORTED),
+    (dict(K=33), B.IDB_ERR_UNSUPPORTED),
+])
+def test_router_step_rejects_invalid_arguments(kw, code):
+    a = dict(x=A16, W=A16, T=128, d=256, K=10, E=768, Ki=6e-3, Kd=6e-3, center=1, bias=A16, stats=None,
+             counts=A16, ws=A16, ws_bytes=1 << 30, variant=0, cfg=True, state=True)
+    a.update(kw)
+    ccfg = B.idb_controller_cfg(a["E"], a["Ki"], a["Kd"], 0, a["center"])
+    cfg = ctypes.byref(ccfg) if a["cfg"] else None
+    sts = _state(bias=a["bias"])
+    state = ctypes.byref(sts) if a["state"] else None
+    st = B.lib().idb_router_step(a["x"], a["W"], B.IDB_DTYPE_BF16, 0, a["T"], a["d"], a["K"], cfg, state, A16, A16,
+                                 a["counts"], 0, a["stats"], a["ws"], a["ws_bytes"], a["variant"], None)
+    assert st == code
+    assert B.idb_last_error() != ""
 
 
 def test_controller_and_stats_null_pointers():

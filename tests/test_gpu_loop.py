@@ -90,3 +90,101 @@ def test_tiny_workload_router_loop():
     assert flips <= 0.01 * wl.T * wl.steps
     np.testing.assert_allclose(rs.state.bias.cpu().numpy(), ref.bias, atol=5e-4)
     print(f"tiny loop: {flips} token selections differ from the free-running oracle over {wl.steps} steps")
+
+
+def _bf16(a: np.ndarray) -> torch.Tensor:
+    return torch.from_numpy(a.view(np.int16)).to(DEV).view(torch.bfloat16)
+
+
+def _assert_same_step(f: RouterStep, s: RouterStep, ref, msg):
+    """The one-call step (f) against route + controller step (s) and the oracle
+    controller run on the GPU's counts: everything bit-identical."""
+    assert torch.equal(f.idx, s.idx), msg
+    assert torch.equal(f.w.view(torch.int32), s.w.view(torch.int32)), msg
+    assert torch.equal(f.counts, s.counts), msg
+    for name in ("bias", "e_prev", "step", "status"):
+        a, b = getattr(f.state, name), getattr(s.state, name)
+        assert torch.equal(a.view(torch.int32) if a.dtype == torch.float32 else a,
+                           b.view(torch.int32) if b.dtype == torch.float32 else b), f"{msg}: {name}"
+    assert torch.equal(f.stats.view(torch.int64), s.stats.view(torch.int64)), msg
+    counts = f.counts.cpu().numpy()
+    stats = oracle.load_stats(counts)
+    assert oracle.controller(counts, ref, f.cfg.Ki, f.cfg.Kd, f.cfg.integral_mode, f.cfg.center) == 0
+    np.testing.assert_array_equal(f.state.bias.cpu().numpy().view(np.uint32), ref.bias.view(np.uint32), msg)
+    np.testing.assert_array_equal(f.state.e_prev.cpu().numpy().view(np.uint32), ref.e_prev.view(np.uint32), msg)
+    np.testing.assert_array_equal(f.stats.cpu().numpy(), stats, msg)
+
+
+@pytest.mark.parametrize("T,d,E,K,variant,packed", [
+    (2048, 256, 768, 10, 0, True),    # two slices: the update runs in the merge's last workgroup
+    (1000, 256, 768, 10, 6, False),   # ragged last token tile
+    (2048, 256, 768, 10, 7, True),    # one slice: the controller is its own launch
+    (513, 256, 1024, 32, 0, False),   # 4 slices x 32 candidates: the generic merge kernel
+    (777, 128, 512, 8, 1, False),     # 32x32 tiles, a padded second slice
+    (300, 256, 768, 10, 0, True),     # three token tiles: a three-workgroup merge
+])
+def test_router_step_equals_route_then_controller(T, d, E, K, variant, packed):
+    x0, W = synth.normal_router_inputs(T, d, E, seed=77)
+    Wt = _bf16(W)
+    cfg = B.ControllerCfg(E, 6e-3, 6e-3)
+    f = RouterStep(T, d, E, K, torch.bfloat16, cfg=cfg, variant=variant)
+    s = RouterStep(T, d, E, K, torch.bfloat16, cfg=cfg, variant=variant)
+    if packed:
+        f.pack(Wt)
+        s.pack(Wt)
+    ref = oracle.ControllerState(E)
+    for t in range(5):
+        x = _bf16(synth.normal_router_inputs(T, d, E, seed=100 + t)[0])
+        # a component shared by every token skews the load, so the
+        # controller has work to do
+        x[:, :16] += 1.5
+        f.step(x, None if packed else Wt)
+        s.route(x, None if packed else Wt)
+        s.update_and_stats()
+        _assert_same_step(f, s, ref, f"step {t}")
+    assert int(f.state.step.item()) == 5
+
+
+def test_router_step_accumulates_microbatches():
+    T, d, E, K = 1024, 256, 768, 10
+    _, W = synth.normal_router_inputs(T, d, E, seed=5)
+    Wt = _bf16(W)
+    f = RouterStep(T, d, E, K, torch.bfloat16)
+    s = RouterStep(T, d, E, K, torch.bfloat16)
+    ref = oracle.ControllerState(E)
+    for t in range(3):
+        xa = _bf16(synth.normal_router_inputs(T, d, E, seed=200 + 2 * t)[0])
+        xb = _bf16(synth.normal_router_inputs(T, d, E, seed=201 + 2 * t)[0])
+        f.route(xa, Wt)
+        f.step(xb, Wt, accumulate=True)
+        s.route(xa, Wt)
+        s.route(xb, Wt, accumulate=True)
+        s.update_and_stats()
+        assert int(f.counts.sum().item()) == 2 * T * K
+        _assert_same_step(f, s, ref, f"step {t}")
+
+
+def test_router_step_graph_replays():
+    """Captured in a graph and replayed: every replay equals the eager calls."""
+    T, d, E, K = 2048, 256, 768, 10
+    _, W = synth.normal_router_inputs(T, d, E, seed=9)
+    Wt = _bf16(W)
+    xs = [_bf16(synth.normal_router_inputs(T, d, E, seed=300 + t)[0]) for t in range(4)]
+    x = torch.empty_like(xs[0])
+    f = RouterStep(T, d, E, K, torch.bfloat16)
+    s = RouterStep(T, d, E, K, torch.bfloat16)
+    f.pack(Wt)
+    s.pack(Wt)
+    ref = oracle.ControllerState(E)
+    side = torch.cuda.Stream()
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=side):
+        f.step(x, None)
+    for t, xt in enumerate(xs):
+        x.copy_(xt)
+        g.replay()
+        s.route(xt, None)
+        s.update_and_stats()
+        torch.cuda.synchronize()
+        _assert_same_step(f, s, ref, f"replay {t}")
