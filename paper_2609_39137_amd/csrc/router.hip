@@ -901,20 +901,49 @@ __global__ __launch_bounds__(kTileThreads) void router_merge_tile_kernel(RouterA
         }
         if (g + gridDim.x < ntiles) fetch(g + gridDim.x);
         __syncthreads();
-        for (int c = tid; c < n; c += kTileThreads) {
-            const int t = c / NSK, pos = c - t * NSK;
-            const int sl = pos / K, r = pos - sl * K;
-            const unsigned long long k = mk[c];
-            int rank = r;
-            for (int o = 0; o < NS; ++o) {
-                if (o == sl) continue;
-                const unsigned long long* lo = mk + t * NSK + o * K;
-#pragma unroll 8
-                for (int j = 0; j < K; ++j) rank += (lo[j] > k) ? 1 : 0;
+        if (NS == 2) {
+            // Each slice's list is in rank order: a two-pointer merge per
+            // token (the lists hold K distinct keys each; key 0 marks an
+            // exhausted list).
+            for (int t = tid; t < ntok; t += kTileThreads) {
+                const unsigned long long* L0 = mk + t * NSK;
+                const unsigned long long* L1 = L0 + K;
+                const float* S0 = ms + t * NSK;
+                const float* S1 = S0 + K;
+                int p0 = 0, p1 = 0;
+                unsigned long long k0 = L0[0], k1 = L1[0];
+                for (int r = 0; r < K; ++r) {
+                    const bool take0 = k0 > k1;
+                    const unsigned long long k = take0 ? k0 : k1;
+                    msel[t * kMaxK + r] = take0 ? S0[p0] : S1[p1];
+                    midx[t * kMaxK + r] = (int)~(unsigned)k;
+                    if (take0) {
+                        ++p0;
+                        k0 = p0 < K ? L0[p0] : 0ull;
+                    } else {
+                        ++p1;
+                        k1 = p1 < K ? L1[p1] : 0ull;
+                    }
+                }
             }
-            if (rank < K) {
-                msel[t * kMaxK + rank] = ms[c];
-                midx[t * kMaxK + rank] = (int)~(unsigned)k;
+        } else {
+            // A candidate's final rank: its rank in its own slice plus the
+            // other slices' candidates above it.
+            for (int c = tid; c < n; c += kTileThreads) {
+                const int t = c / NSK, pos = c - t * NSK;
+                const int sl = pos / K, r = pos - sl * K;
+                const unsigned long long k = mk[c];
+                int rank = r;
+                for (int o = 0; o < NS; ++o) {
+                    if (o == sl) continue;
+                    const unsigned long long* lo = mk + t * NSK + o * K;
+#pragma unroll 8
+                    for (int j = 0; j < K; ++j) rank += (lo[j] > k) ? 1 : 0;
+                }
+                if (rank < K) {
+                    msel[t * kMaxK + rank] = ms[c];
+                    midx[t * kMaxK + rank] = (int)~(unsigned)k;
+                }
             }
         }
         __syncthreads();

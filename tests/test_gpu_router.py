@@ -311,3 +311,37 @@ def test_pack_weight_is_the_documented_permutation():
                     lo = c * 128 + 64 * s + 16 * (l // 16)
                     want[base + 16 * l: base + 16 * l + 16] = src[16 * b + l % 16, lo:lo + 16]
     np.testing.assert_array_equal(got, want)
+
+@pytest.mark.parametrize("T,E,K,variant", [
+    (1000, 768, 10, 6),   # two slices: the two-pointer merge
+    (300, 768, 10, 3),    # three slices: the rank-counting tile merge
+    (513, 1024, 32, 4),   # 8 slices x 32 candidates: the generic merge kernel
+    (777, 512, 8, 1),     # 32x32 tiles, a padded second slice
+])
+def test_split_calls_equal_forward(T, E, K, variant):
+    """score_select then merge, called separately, give exactly the outputs of
+    the one-call forward, with and without accumulation."""
+    d = 256
+    x, W = synth.normal_router_inputs(T, d, E, seed=T + K, w_std=0.05)
+    b = synth.bias(E, "small", seed=3)
+    xt, Wt, bt = to_dev(x), to_dev(W), torch.from_numpy(b).to(DEV)
+    code = B.IDB_DTYPE_BF16
+    ws = torch.zeros(max(B.idb_router_workspace_bytes(T, d, E, K, code, variant), 16), dtype=torch.uint8,
+                     device=DEV)
+    outs = []
+    for split in (False, True):
+        idx = torch.full((T, K), -1, dtype=torch.int32, device=DEV)
+        w = torch.full((T, K), -1.0, dtype=torch.float32, device=DEV)
+        c = torch.full((E,), 7, dtype=torch.int32, device=DEV)
+        for acc in (False, True):
+            if split:
+                B.idb_router_score_select(xt, Wt, bt, K, idx, w, c, acc, workspace=ws, variant=variant)
+                B.idb_router_merge(T, d, E, K, code, idx, w, c, workspace=ws, variant=variant)
+            else:
+                B.idb_router_forward(xt, Wt, bt, K, idx, w, c, acc, workspace=ws, variant=variant)
+        outs.append((idx.cpu().numpy(), w.cpu().numpy(), c.cpu().numpy()))
+    (i0, w0, c0), (i1, w1, c1) = outs
+    np.testing.assert_array_equal(i0, i1)
+    np.testing.assert_array_equal(w0.view(np.uint32), w1.view(np.uint32))
+    np.testing.assert_array_equal(c0, c1)
+    assert int(c0.sum()) == 2 * T * K
