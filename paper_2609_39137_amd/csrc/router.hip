@@ -18,7 +18,7 @@
 // In both, lanes of a wave consume the same k bytes of a chunk for both
 // operands, so the k order agrees between A and B.
 //
-// Token tile: staged through registers into two LDS stages of 144-byte rows
+// Token tile: staged through registers into two LDS stages of 160-byte rows
 // (128 bytes + 32 of padding, which measured fastest for the B-operand reads
 // and the staging writes), loaded two chunks ahead of use.
 //
@@ -32,27 +32,13 @@
 // of the block and experts 8 (r/4) + 4 (l/32) + r%4, r < 16; 16x16 - lane l
 // holds token l%16 of the tile and experts 4 (l/16) + r, r < 4.
 //
-// Epilogue (exact for any input).  The scores of TPP tokens at a time are
-// written token-major into LDS (the contraction's staging area is free by
-// then); TPT adjacent threads then own one token, each every TPT-th block of
-// 16 experts (so a wave's LDS reads of the score rows hit distinct banks).
-//   A. s = sigmoid(z) into the LDS score matrix (padding experts: -inf); this
-//      step is the contraction kernel's, as it depends on the MFMA layout.
-//   B. v = fl32(s + b) into registers; 32 group maxima per token.
-//   C. tau = the K-th largest group maximum, <= the token's K-th largest v;
-//      each thread marks its values >= tau in a bitmask and counts them.
-//   D. A prefix over the token's threads gives write offsets; the candidates
-//      (typically about K + 2) go to an LDS list as 64-bit rank keys.
-//   E. Candidate rank = number of list keys above it; ranks < K are the
-//      slice's selection, in rank order.
-//   F. Tokens whose list would overflow (heavy ties, large K) are resolved by
-//      one wave each: K rounds of "best key strictly below the previous pick"
-//      over the token's LDS score row.
-//   G. One slice: gate weights, outputs and an LDS histogram flushed with one
-//      atomic per non-zero bin.  Several slices: the slice's K candidates go
-//      to the workspace and router_merge_kernel combines them.
+// Epilogue: epilogue.h, steps A-G; step A (sigmoid of the accumulators into
+// the LDS score matrix) is the contraction kernel's, as it depends on the MFMA
+// layout.  Several slices: router_merge_kernel combines their candidates.
+
 #include "common.h"
 #include "controller_block.h"
+#include "epilogue.h"
 #include "internal.h"
 
 #pragma clang fp contract(off)
@@ -61,318 +47,8 @@ namespace idb {
 
 namespace {
 
-constexpr int kCap = 32;      // candidate list capacity per token and slice
 constexpr int kRowPad = 160;  // LDS bytes per staged token row (128 + 32 pad)
 constexpr int kMaxSlices = 8;
-constexpr int kScoreLds = 100000;  // LDS budget of the epilogue's score matrix
-
-// Epilogue layout for NT threads, BT tokens, BE experts per workgroup; the
-// contraction's MAIN_LDS bytes of LDS are reused.
-template <int NT_, int BT_, int BE_, int MAIN_LDS_>
-struct EpiCfg {
-    static constexpr int NT = NT_;
-    static constexpr int BT = BT_;
-    static constexpr int BE = BE_;
-    static constexpr int RS = BE + 4;  // score row stride in floats (odd number of 16-byte units)
-    // tokens per pass: the largest of BT, BT/2, BT/4 whose score rows fit
-    static constexpr int TPP = (BT * RS * 4 <= kScoreLds && BT <= NT) ? BT
-                               : ((BT / 2) * RS * 4 <= kScoreLds && BT / 2 <= NT) ? BT / 2 : BT / 4;
-    static constexpr int NPASS = BT / TPP;
-    static constexpr int TPT = NT / TPP;
-    static constexpr int VPT = BE / TPT;  // slice columns per thread: every TPT-th 16-column block
-    static constexpr int NBL = VPT / 16;  // 16-column blocks per thread
-    static constexpr int NG = 32;         // group maxima per token
-    static constexpr int GPT = NG / TPT;  // group maxima per thread
-    static constexpr int GSZ = VPT / GPT;
-    static constexpr int MW = (VPT + 31) / 32;          // candidate mask words
-    static constexpr int NCI = (kCap + TPT - 1) / TPT;  // list entries ranked per thread
-    static constexpr int NBIAS = (BE + NT - 1) / NT;    // bias values staged per thread
-    static constexpr int GMS = NG + 4;                  // group-maximum row stride (words, 16-byte aligned)
-    static constexpr int CNS = TPT + 1;                 // count row stride
-    static constexpr int LKS = kCap + 2;                // candidate-key row stride (8-byte keys)
-    static constexpr int LSS = kMaxK + 4;               // selection row stride
-    static constexpr int OFF_SC = 0;
-    static constexpr int OFF_BIAS = OFF_SC + TPP * RS * 4;
-    static constexpr int OFF_GM = OFF_BIAS + BE * 4;
-    static constexpr int OFF_CNT = OFF_GM + TPP * GMS * 4;
-    static constexpr int OFF_LK = (OFF_CNT + TPP * CNS * 4 + 15) / 16 * 16;
-    static constexpr int OFF_SI = OFF_LK + TPP * LKS * 8;
-    static constexpr int OFF_OVF = OFF_SI + TPP * LSS * 4;
-    static constexpr int OFF_HIST = OFF_OVF + 16 * 4;
-    static constexpr int EPI_LDS = OFF_HIST + 1024 * 4;
-    static constexpr int LDS = MAIN_LDS_ > EPI_LDS ? MAIN_LDS_ : EPI_LDS;
-    static_assert(NPASS * TPP == BT && TPP % 32 == 0, "passes of whole 32-token groups");
-    static_assert(TPT * TPP == NT && TPT <= 16 && 16 % TPT == 0, "a token's threads share one wave");
-    static_assert(VPT * TPT == BE && VPT % 16 == 0 && GSZ * GPT == VPT && GPT * TPT == NG, "columns split evenly");
-    static_assert(TPP * RS * 4 <= kScoreLds, "score rows of a pass fit");
-    static_assert(TPP <= 16 * 32, "overflow bitmask size");
-    static_assert(LDS <= 160 * 1024, "LDS of one workgroup");
-};
-
-// Adds a workgroup's LDS histogram into the global counts, one atomic per
-// non-zero bin.  Each workgroup starts at a different bin, so workgroups that
-// finish together do not queue on the same counter.
-__device__ __forceinline__ void flush_hist(const int* hist, int32_t* counts, int E) {
-    const int rot = (int)((blockIdx.x * 97u) % (unsigned)E);
-    for (int i = threadIdx.x; i < E; i += blockDim.x) {
-        int e = i + rot;
-        e = e < E ? e : e - E;
-        if (hist[e] != 0) atomicAdd(&counts[e], hist[e]);
-    }
-}
-
-// Loads the slice's bias into registers (issued before the contraction, so
-// it arrives meanwhile); the epilogue moves it to LDS.
-template <class EC>
-__device__ __forceinline__ void prefetch_bias(const RouterArgs& a, int sbase, float (&breg)[EC::NBIAS]) {
-#pragma unroll
-    for (int i = 0; i < EC::NBIAS; ++i) {
-        const int c = threadIdx.x + EC::NT * i;
-        breg[i] = (c < EC::BE && sbase + c < a.E) ? a.bias[sbase + c] : 0.0f;
-    }
-}
-
-// Steps A-G for the workgroup's BT tokens of one slice.  store_pass(pass, sc)
-// writes the sigmoid scores of tokens [pass*TPP, (pass+1)*TPP) of the tile
-// into rows 0..TPP-1 of the LDS score matrix sc (and the debug dump).
-template <class EC, class StoreFn>
-__device__ __forceinline__ void select_epilogue(const RouterArgs& a, int NS, int slice, int64_t tok0,
-                                                unsigned char* smem, const float (&breg)[EC::NBIAS],
-                                                StoreFn&& store_pass) {
-    using C = EC;
-    constexpr int WAVES = C::NT / 64;
-    const int tid = threadIdx.x;
-    const int lane = tid & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int64_t T = a.T;
-    const int E = a.E;
-    const int K = a.K;
-    const int sbase = slice * C::BE;
-    float* sc = reinterpret_cast<float*>(smem + C::OFF_SC);
-    float* bias_s = reinterpret_cast<float*>(smem + C::OFF_BIAS);
-    float* gm = reinterpret_cast<float*>(smem + C::OFF_GM);
-    int* cnt = reinterpret_cast<int*>(smem + C::OFF_CNT);
-    unsigned long long* lk = reinterpret_cast<unsigned long long*>(smem + C::OFF_LK);
-    int* si = reinterpret_cast<int*>(smem + C::OFF_SI);
-    unsigned* ovf = reinterpret_cast<unsigned*>(smem + C::OFF_OVF);
-    int* hist = reinterpret_cast<int*>(smem + C::OFF_HIST);
-
-    // The contraction ended with a barrier, so its staging area is free.
-#pragma unroll
-    for (int i = 0; i < C::NBIAS; ++i) {
-        const int c = tid + C::NT * i;
-        if (c < C::BE) bias_s[c] = breg[i];
-    }
-    for (int e = tid; e < 1024; e += C::NT) hist[e] = 0;
-
-    const int tl = tid / C::TPT, q = tid % C::TPT;  // token of the pass and part, in steps B-G
-    // This thread's value j sits in slice column col(j) = 16 (q + TPT (j/16)) + j%16.
-    auto col_of = [&](int j) { return 16 * (q + C::TPT * (j >> 4)) + (j & 15); };
-    unsigned valid[C::MW];  // bit j: column j is a real expert
-    {
-#pragma unroll
-        for (int w = 0; w < C::MW; ++w) valid[w] = 0u;
-#pragma unroll
-        for (int m = 0; m < C::NBL; ++m) {
-            const int nreal = E - sbase - 16 * (q + C::TPT * m);  // may be <= 0 or >= 16
-            const unsigned bits = nreal >= 16 ? 0xffffu : (nreal <= 0 ? 0u : ((1u << nreal) - 1u));
-            valid[m >> 1] |= bits << (16 * (m & 1));
-        }
-    }
-
-#pragma unroll
-    for (int pass = 0; pass < C::NPASS; ++pass) {
-        // A. scores of the pass's tokens into the LDS score matrix
-        store_pass(pass, sc);
-        if (tid < 16) ovf[tid] = 0;
-        __syncthreads();
-
-        // B. biased values of this thread's columns; group maxima
-        float v[C::VPT];
-#pragma unroll
-        for (int m = 0; m < C::NBL; ++m)
-#pragma unroll
-            for (int i4 = 0; i4 < 4; ++i4) {
-                const int col = 16 * (q + C::TPT * m) + 4 * i4;
-                const float4 s4 = *reinterpret_cast<const float4*>(sc + tl * C::RS + col);
-                const float4 b4 = *reinterpret_cast<const float4*>(bias_s + col);
-                const int j = 16 * m + 4 * i4;
-                v[j + 0] = s4.x + b4.x;
-                v[j + 1] = s4.y + b4.y;
-                v[j + 2] = s4.z + b4.z;
-                v[j + 3] = s4.w + b4.w;
-            }
-        float own[C::GPT];
-#pragma unroll
-        for (int g = 0; g < C::GPT; ++g) {
-            float mx = -INFINITY;
-#pragma unroll
-            for (int j = 0; j < C::GSZ; ++j) mx = fmaxf(mx, v[g * C::GSZ + j]);
-            own[g] = mx;
-            gm[tl * C::GMS + q * C::GPT + g] = mx;
-        }
-        __syncthreads();
-
-        // C. threshold; candidate masks and counts
-        // tau = the K-th largest of the token's 32 group maxima, i.e. the
-        // largest maximum m with #{maxima >= m} >= K (K <= 32): each thread
-        // tests its own maxima against all 32, a max over the token's lanes
-        // combines them.
-        float tau = -INFINITY;
-        {
-            float g[C::NG];
-#pragma unroll
-            for (int i4 = 0; i4 < C::NG / 4; ++i4) {
-                const float4 t4 = *reinterpret_cast<const float4*>(gm + tl * C::GMS + 4 * i4);
-                g[4 * i4 + 0] = t4.x;
-                g[4 * i4 + 1] = t4.y;
-                g[4 * i4 + 2] = t4.z;
-                g[4 * i4 + 3] = t4.w;
-            }
-#pragma unroll
-            for (int i = 0; i < C::GPT; ++i) {
-                int ge = 0;
-#pragma unroll
-                for (int j = 0; j < C::NG; ++j) ge += (g[j] >= own[i]) ? 1 : 0;
-                if (ge >= K) tau = fmaxf(tau, own[i]);
-            }
-#pragma unroll
-            for (int o = 1; o < C::TPT; o <<= 1) tau = fmaxf(tau, __shfl_xor(tau, o));
-        }
-        // Bit j: v_j >= tau, read off the sign of v_j - tau (a difference of
-        // two finite floats is +0 only when they are equal, and -inf - tau is
-        // negative); padding columns are masked out, which also covers the
-        // NaN of -inf - -inf when tau = -inf.
-        unsigned msk[C::MW];
-#pragma unroll
-        for (int w = 0; w < C::MW; ++w) msk[w] = 0u;
-#pragma unroll
-        for (int j = 0; j < C::VPT; ++j)
-            msk[j / 32] |= ((__float_as_uint(v[j] - tau) >> 31) ^ 1u) << (j % 32);
-        int mine_n = 0;
-#pragma unroll
-        for (int w = 0; w < C::MW; ++w) {
-            msk[w] &= valid[w];
-            mine_n += __builtin_popcount(msk[w]);
-        }
-        cnt[tl * C::CNS + q] = mine_n;
-        __syncthreads();
-
-        // D. write offsets; candidate keys into the token's list
-        int off = 0, n = 0;
-#pragma unroll
-        for (int o = 0; o < C::TPT; ++o) {
-            const int m = cnt[tl * C::CNS + o];
-            off += (o < q) ? m : 0;
-            n += m;
-        }
-        const bool listed = n <= kCap;
-        if (!listed) {
-            if (q == 0) atomicOr(&ovf[tl >> 5], 1u << (tl & 31));
-        } else {
-#pragma unroll
-            for (int w = 0; w < C::MW; ++w) {
-                unsigned m = msk[w];
-                while (m) {
-                    const int col = col_of(w * 32 + __builtin_ctz(m));
-                    m &= m - 1u;
-                    lk[tl * C::LKS + off] = rank_key(sc[tl * C::RS + col] + bias_s[col], sbase + col);
-                    ++off;
-                }
-            }
-        }
-        __syncthreads();
-
-        // E. ranks of the listed candidates: thread q ranks entries q, q+TPT, ...
-        // against the n list keys, reading each list key once.
-        if (listed) {
-            unsigned long long mine[C::NCI];
-            int rank[C::NCI];
-#pragma unroll
-            for (int i = 0; i < C::NCI; ++i) {
-                const int c = q + C::TPT * i;
-                mine[i] = c < n ? lk[tl * C::LKS + c] : ~0ull;  // ~0: beyond the list, never written
-                rank[i] = 0;
-            }
-#pragma unroll 4
-            for (int o = 0; o < n; ++o) {
-                const unsigned long long ko = lk[tl * C::LKS + o];
-#pragma unroll
-                for (int i = 0; i < C::NCI; ++i) rank[i] += (ko > mine[i]) ? 1 : 0;
-            }
-#pragma unroll
-            for (int i = 0; i < C::NCI; ++i)
-                if (q + C::TPT * i < n && rank[i] < K) si[tl * C::LSS + rank[i]] = (int)~(unsigned)mine[i];
-        }
-
-        // F. overflowing tokens, one wave each (the bitmask is uniform: it was
-        // complete at the last barrier)
-        {
-            int k = 0;
-            for (int word = 0; word < C::TPP / 32; ++word) {
-                unsigned bits = ovf[word];
-                while (bits) {
-                    const int t = word * 32 + __builtin_ctz(bits);
-                    bits &= bits - 1u;
-                    if ((k++ % WAVES) != wave) continue;
-                    unsigned long long prev = ~0ull;
-                    for (int r = 0; r < K; ++r) {
-                        unsigned long long best = 0ull;
-                        for (int c = lane; c < C::BE; c += 64) {
-                            if (sbase + c < E) {
-                                const unsigned long long kk = rank_key(sc[t * C::RS + c] + bias_s[c], sbase + c);
-                                if (kk < prev && kk > best) best = kk;
-                            }
-                        }
-#pragma unroll
-                        for (int o = 32; o >= 1; o >>= 1) {
-                            const unsigned lo = __shfl_xor((unsigned)best, o);
-                            const unsigned hi = __shfl_xor((unsigned)(best >> 32), o);
-                            const unsigned long long other = ((unsigned long long)hi << 32) | lo;
-                            best = other > best ? other : best;
-                        }
-                        prev = best;
-                        if (lane == 0) si[t * C::LSS + r] = (int)~(unsigned)best;
-                    }
-                }
-            }
-        }
-        __syncthreads();
-
-        // G. outputs of the pass's tokens (selected scores read back from the
-        // token's LDS score row)
-        {
-            const int64_t tok = tok0 + pass * C::TPP + tl;
-            if (tok < T) {
-                if (NS > 1) {
-                    const int64_t base = (tok * NS + slice) * K;
-                    for (int r = q; r < K; r += C::TPT) {
-                        const int e = si[tl * C::LSS + r];
-                        const float s = sc[tl * C::RS + (e - sbase)];
-                        a.cand_v[base + r] = s + bias_s[e - sbase];
-                        a.cand_s[base + r] = s;
-                        a.cand_i[base + r] = e;
-                    }
-                } else {
-                    // gate weights: den is the fp32 sum of the selected
-                    // unbiased scores in rank order
-                    float den = 0.0f;
-#pragma unroll 8
-                    for (int r = 0; r < K; ++r) den = den + sc[tl * C::RS + (si[tl * C::LSS + r] - sbase)];
-                    for (int r = q; r < K; r += C::TPT) {
-                        const int e = si[tl * C::LSS + r];
-                        const float s = sc[tl * C::RS + (e - sbase)];
-                        a.idx[tok * K + r] = e;
-                        a.w[tok * K + r] = (den == 0.0f) ? 1.0f / (float)K : s / den;
-                        atomicAdd(&hist[e], 1);
-                    }
-                }
-            }
-        }
-        __syncthreads();
-    }
-    if (NS == 1) flush_hist(hist, a.counts, E);
-}
 
 // One 16-byte unit of both operands: bf16 -> one 32x32x16 MFMA; fp32 -> four
 // 32x32x2 MFMAs, float i of each lane's unit feeding the i-th.

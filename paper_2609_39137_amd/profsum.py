@@ -30,7 +30,12 @@ import statistics
 import sys
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
-ROUTER_KERNEL = "router_score_select_kernel"
+# the fused router kernel's instantiations (16x16 and 32x32 MFMA tilings)
+ROUTER_KERNELS = ("router16_kernel", "router32_kernel")
+
+
+def _is_router(name: str) -> bool:
+    return any(k in name for k in ROUTER_KERNELS)
 
 
 def router_source_hash() -> str:
@@ -67,8 +72,8 @@ def _counter_rows(csv_path: str, counter: str):
 
 def _calibrated(csv_path: str, counter: str, copy_bytes: int):
     rows = _counter_rows(csv_path, counter)
-    router = [v for n, v in rows if ROUTER_KERNEL in n]
-    copies = [v for n, v in rows if ROUTER_KERNEL not in n and "copy" in n.lower()]
+    router = [v for n, v in rows if _is_router(n)]
+    copies = [v for n, v in rows if not _is_router(n) and "copy" in n.lower()]
     if not router or not copies:
         raise SystemExit(f"{csv_path}: no {counter} readings for the router kernel or the calibration copy")
     copy_kib = max(copies)
