@@ -2,9 +2,10 @@
 
 One step = the whole hot path over one batch: repacking the router matrix
 into the MFMA operand layout (a training step changes it after every
-optimizer update), the fused gate contraction + sigmoid + biased Top-K + gate
-weights + load counts (idb_router_forward), the ID controller update
-(idb_controller_update) and MaxVio/MinVio (idb_load_stats).  Inputs are
+optimizer update), then idb_router_step: the fused gate contraction +
+sigmoid + biased Top-K (per expert slice), the slice merge with gate weights
+and load counts, and in the merge's last workgroup MaxVio/MinVio and the ID
+controller update.  Inputs are
 synthetic, seeded, resident in HBM before the timed region; the hidden-state
 batch rotates over several distinct buffers so it is not served from the
 256 MB Infinity Cache.  Steps are issued as HIP graph replays, each graph
@@ -16,8 +17,9 @@ collection: one device-to-device copy of known size (the calibration for the
 HBM byte counters) followed by a few launches of the fused router kernel.
 
 Prints one JSON line: routed tokens/s for the step, with the dominant
-kernel's roofline and the CPU oracle timed on a bounded sample of the same
-workload.
+kernel's roofline, the unfused selection's HBM roofline (idb_select_from_scores
+over the router's own fp32 scores, materialised for this measurement only) and
+the CPU oracle timed on a bounded sample of the same workload.
 """
 from __future__ import annotations
 
@@ -45,7 +47,7 @@ def load_traffic(workload: str, variant_id: int):
     """HBM bytes per launch of the dominant kernel from a committed counter summary, or None if stale/absent."""
     from paper_2609_39137_amd.profsum import router_source_hash
 
-    path = os.path.join(PROFILES, f"router_score_select_{workload}_pmc.json")
+    path = os.path.join(PROFILES, f"router_fused_kernel_{workload}_pmc.json")
     if not os.path.exists(path):
         return None
     with open(path) as f:
@@ -244,10 +246,54 @@ def main() -> int:
         "unit": "TFLOP/s",
         "frac": round(achieved / peak, 4),
         "traffic": load_traffic(wl.name, rs.info["variant"]),
-        "kernel": "router_score_select_kernel",
+        "kernel": f"fused router kernel, variant {rs.info['variant']} ({rs.info['tokens_per_wg']} tokens x "
+                  f"{rs.info['waves'] * rs.info['experts_per_wave']} experts per workgroup)",
         "kernel_us": round(k1_ms * 1000, 2),
         "flops_per_launch": flops,
     }
+    # the unfused selection (scores given) over materialised fp32 scores, an
+    # HBM-bound pass: the router's own scores of each input batch, dumped
+    # once; timed in accumulate mode, so each call is exactly one launch of
+    # the select kernel
+    sel_bufs = max(2, min(8, math.ceil(512 * 2**20 / (wl.T * wl.E * 4))))
+    scores = []
+    for i in range(sel_bufs):
+        buf = torch.empty((wl.T, wl.E), dtype=torch.float32, device=dev)
+        with torch.cuda.stream(stream):
+            rs.route(xs[i % nbuf], None, scores_dump=buf, stream=stream)
+        scores.append(buf)
+    sidx = torch.empty((wl.T, wl.K), dtype=torch.int32, device=dev)
+    sw = torch.empty((wl.T, wl.K), dtype=torch.float32, device=dev)
+    sc = torch.zeros(wl.E, dtype=torch.int32, device=dev)
+    torch.cuda.synchronize()
+    sel_per = sel_bufs * max(1, 16 // sel_bufs)
+    sel_graph = capture(lambda i: B.idb_select_from_scores(scores[i % sel_bufs], rs.state.bias, wl.K, sidx, sw, sc,
+                                                           accumulate=True, stream=stream), sel_per)
+    with torch.cuda.stream(stream):
+        sel_graph.replay()
+    torch.cuda.synchronize()
+    ev0.record(stream)
+    with torch.cuda.stream(stream):
+        for _ in range(n_rep):
+            sel_graph.replay()
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    sel_ms = ev0.elapsed_time(ev1) / (n_rep * sel_per)
+    sel_bytes = wl.T * wl.E * 4 + wl.T * wl.K * 8 + 2 * wl.E * 4
+    sel_gbs = sel_bytes / (sel_ms * 1e-3) / 1e9
+    log(f"select from scores: {sel_ms * 1000:.2f} us/launch, {sel_gbs:.0f} GB/s")
+    select_roofline = {
+        "bound": "hbm",
+        "achieved": round(sel_gbs, 1),
+        "peak": PEAK_HBM_GBS,
+        "unit": "GB/s",
+        "frac": round(sel_gbs / PEAK_HBM_GBS, 4),
+        "kernel": "select_kernel (idb_select_from_scores, fp32 scores [T][E] read from HBM)",
+        "kernel_us": round(sel_ms * 1000, 2),
+        "bytes_per_launch": sel_bytes,
+    }
+    del scores
+
     value = wl.T / (ms_step * 1e-3)
     out = {
         "metric": "routed tokens/sec for router+ID-update step, Top-10-of-768; % MFMA/HBM roofline",
@@ -268,6 +314,7 @@ def main() -> int:
                    "weight": "bf16 row-major, repacked every step" if wl.dtype == "bf16" else
                              "fp32 row-major, repacked every step"},
         "roofline": roofline,
+        "select_roofline": select_roofline,
         "last_step": {"maxvio": stats[0], "minvio": stats[1]},
     }
     if not args.no_cpu_baseline:

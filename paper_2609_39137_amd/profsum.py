@@ -41,7 +41,7 @@ def _is_router(name: str) -> bool:
 def router_source_hash() -> str:
     """Hash of the sources that define the fused router kernel (a counter summary is valid only for them)."""
     h = hashlib.sha256()
-    for f in ("router.hip", "common.h"):
+    for f in ("router.hip", "epilogue.h", "common.h"):
         with open(os.path.join(_PKG, "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
