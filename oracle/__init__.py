@@ -16,6 +16,8 @@ readings of points the paper leaves open):
 * :func:`controller` -- one ID bias update (Alg. 1, Eq. rapid-update) or the
   DeepSeek sign rule (Eq. pid-deepseek)
 * :func:`load_stats` -- MaxVio / MinVio (Eq. vio)
+* :func:`qb_alpha`, :func:`qb_update` -- Quantile Balancing's cutoffs and
+  target bias, with the EMA variant (Eq. pid-quantile, Eq. pid-quantile-def)
 """
 from __future__ import annotations
 
@@ -77,6 +79,8 @@ def _declare(lib):
     lib.oracle_load_stats.argtypes = [P, i32, P]
     lib.oracle_step_seconds.argtypes = [P, P, c_int, i64, i32, i32, i32, f32, f32, P, P, P, P, P, P, P, P]
     lib.oracle_step_seconds.restype = ctypes.c_double
+    lib.oracle_qb_alpha.argtypes = [P, P, i64, i32, i32, P]
+    lib.oracle_qb_update.argtypes = [P, P, i64, i32, i32, f32, P]
     return lib
 
 
@@ -208,3 +212,27 @@ def step_seconds(x: np.ndarray, W: np.ndarray, K: int, Ki: float, Kd: float, sta
     return float(lib.oracle_step_seconds(_ptr(x), _ptr(W), code, T, d, E, K, float(Ki), float(Kd),
                                          _ptr(state.bias), _ptr(state.e_prev), _ptr(state.step),
                                          _ptr(state.status), _ptr(idx), _ptr(w), _ptr(c), _ptr(stats)))
+
+
+def qb_alpha(scores: np.ndarray, bias: np.ndarray, K: int) -> np.ndarray:
+    """Quantile Balancing cutoffs (Eq. pid-quantile-def): per token the (K+1)-th largest fp32 ``s + b``."""
+    lib = _load()
+    s = np.ascontiguousarray(scores, dtype=np.float32)
+    b = np.ascontiguousarray(bias, dtype=np.float32)
+    T, E = s.shape
+    assert 1 <= K < E and b.shape == (E,)
+    alpha = np.empty(T, np.float32)
+    lib.oracle_qb_alpha(_ptr(s), _ptr(b), T, E, K, _ptr(alpha))
+    return alpha
+
+
+def qb_update(scores: np.ndarray, alpha: np.ndarray, K: int, rho: float, bias: np.ndarray) -> np.ndarray:
+    """Quantile Balancing's bias update (Eq. pid-quantile; EMA with ``rho`` > 0) in place on ``bias``."""
+    lib = _load()
+    s = np.ascontiguousarray(scores, dtype=np.float32)
+    a = np.ascontiguousarray(alpha, dtype=np.float32)
+    T, E = s.shape
+    assert 1 <= K < E and a.shape == (T,) and bias.shape == (E,) and bias.dtype == np.float32
+    assert bias.flags.c_contiguous
+    lib.oracle_qb_update(_ptr(s), _ptr(a), T, E, K, float(rho), _ptr(bias))
+    return bias

@@ -23,6 +23,9 @@
  *                                                            rapid-update)
  *   SIGN mode: DeepSeek's fixed-step integral rule         (Eq. pid-deepseek)
  *   S1  MaxVio / MinVio                                    (Sec. 4.1, Eq. vio)
+ *   Q1..Q4 Quantile Balancing's target bias, with the EMA   (Eq. pid-quantile,
+ *          variant used as a diagnostic                      Eq. pid-quantile-def; Sec. 3,
+ *                                                            EMA smoothing of the target)
  *
  * Readings of points the paper leaves open (each is listed in the design
  * notes of the repository):
@@ -41,6 +44,13 @@
  *     power of two P >= E, then a_j <- a_j + a_{j+h} for h = P/2, ..., 1.
  *   - an empty batch (sum of counts == 0) leaves the state untouched and
  *     reports status 3; a negative count reports status 1.
+ *   - Quantile Balancing: the cutoff alpha_i is the (K+1)-th largest biased
+ *     score fl32(s + b) of token i; margins are fl32(s_ij - alpha_i) with -0
+ *     read as +0; quantile_{1-K/E} over the m tokens of a batch is the
+ *     inverted empirical CDF, i.e. the k-th smallest margin with
+ *     k = ceil(m (E - K) / E) computed in exact integers; the target is its
+ *     negation.  The EMA variant is fl32(fl32(rho b) + fl32(fl32(1 - rho) Q)),
+ *     and rho == 0 is the plain target b = Q.
  *
  * Build: gcc -O2 -ffp-contract=off -fopenmp -shared -fPIC (never -ffast-math:
  * the fp32 steps must round exactly as written).
@@ -281,6 +291,72 @@ void oracle_load_stats(const int32_t* counts, int32_t E, double* out) {
     }
     out[0] = (double)((int64_t)E * mx - S) / (double)S;
     out[1] = (double)(S - (int64_t)E * mn) / (double)S;
+}
+
+/* Q1: the cutoff of Eq. pid-quantile-def for each token: the (K+1)-th largest
+ * biased score fl32(s + b) in the order of Eq. pid-routing (K + 1 passes of
+ * "best not yet taken"; K + 1 <= E). */
+void oracle_qb_alpha(const float* s, const float* bias, int64_t T, int32_t E, int32_t K, float* alpha) {
+#pragma omp parallel
+    {
+        unsigned char* taken = (unsigned char*)malloc((size_t)E);
+#pragma omp for schedule(static)
+        for (int64_t t = 0; t < T; ++t) {
+            const float* st = s + t * (int64_t)E;
+            memset(taken, 0, (size_t)E);
+            float pick = 0.0f;
+            for (int32_t r = 0; r <= K; ++r) {
+                int32_t best = -1;
+                float best_v = 0.0f;
+                for (int32_t i = 0; i < E; ++i) {
+                    if (taken[i]) continue;
+                    float v = st[i] + bias[i];
+                    if (best < 0 || ranks_above(v, i, best_v, best)) {
+                        best = i;
+                        best_v = v;
+                    }
+                }
+                taken[best] = 1;
+                pick = best_v;
+            }
+            alpha[t] = pick;
+        }
+        free(taken);
+    }
+}
+
+static int cmp_float_asc(const void* a, const void* b) {
+    float x = *(const float*)a, y = *(const float*)b;
+    return (x > y) - (x < y);
+}
+
+/* Q2-Q4: Quantile Balancing's bias update (Eq. pid-quantile) from the batch's
+ * scores s [T][E] and cutoffs alpha [T].  For each expert j: the margins
+ * d_ij = fl32(s_ij - alpha_i) (-0 read as +0), their (1 - K/E) quantile q_j
+ * as the k-th smallest with k = ceil(T (E - K) / E), the target Q_j = -q_j
+ * (Eq. pid-quantile-def), then b_j = Q_j for rho == 0, else the EMA
+ * fl32(fl32(rho b_j) + fl32(fl32(1 - rho) Q_j)).  1 <= K < E. */
+void oracle_qb_update(const float* s, const float* alpha, int64_t T, int32_t E, int32_t K, float rho, float* bias) {
+    const int64_t k = (T * (int64_t)(E - K) + E - 1) / E; /* ceil(T (E-K) / E), 1-based */
+#pragma omp parallel
+    {
+        float* d = (float*)malloc(sizeof(float) * (size_t)T);
+#pragma omp for schedule(static)
+        for (int32_t j = 0; j < E; ++j) {
+            for (int64_t t = 0; t < T; ++t) d[t] = (s[t * (int64_t)E + j] - alpha[t]) + 0.0f;
+            qsort(d, (size_t)T, sizeof(float), cmp_float_asc);
+            const float q = d[k - 1];
+            const float Q = -q;
+            if (rho == 0.0f) {
+                bias[j] = Q;
+            } else {
+                const float keep = rho * bias[j];
+                const float take = (1.0f - rho) * Q;
+                bias[j] = keep + take;
+            }
+        }
+        free(d);
+    }
 }
 
 /* Wall-clock seconds of one whole oracle step (R1-R6, C1-C7, S1) on the host,

@@ -28,6 +28,15 @@ MUTANTS = {
     "sigmoid-sign": ("exp(-z)", "exp(z)"),
     "maxvio-uses-min": ("(int64_t)E * mx - S", "(int64_t)E * mn - S"),
     "mean-over-P": ("tree_sum(bt, E) / (float)E", "tree_sum(bt, E) / (float)(E + 1)"),
+    "qb-alpha-kth": ("for (int32_t r = 0; r <= K; ++r) {", "for (int32_t r = 0; r < K; ++r) {"),
+    "qb-quantile-level": ("const int64_t k = (T * (int64_t)(E - K) + E - 1) / E;",
+                          "const int64_t k = (T * (int64_t)K + E - 1) / E;"),
+    "qb-floor": ("const int64_t k = (T * (int64_t)(E - K) + E - 1) / E;",
+                 "const int64_t k = (T * (int64_t)(E - K)) / E;"),
+    "qb-no-negation": ("const float Q = -q;", "const float Q = q;"),
+    "qb-ema-weights": ("const float take = (1.0f - rho) * Q;", "const float take = rho * Q;"),
+    "qb-biased-margin": ("d[t] = (s[t * (int64_t)E + j] - alpha[t]) + 0.0f;",
+                         "d[t] = (s[t * (int64_t)E + j] + bias[j] - alpha[t]) + 0.0f;"),
 }
 
 

@@ -415,3 +415,93 @@ def test_load_stats_within_paper_bounds_on_real_selections():
         _, _, c = oracle.select(s, synth.bias(64, "large", seed=52), K)
         mx, mn = oracle.load_stats(c)
         assert 0.0 <= mx <= 64 / K - 1 + 1e-12 and 0.0 <= mn <= 1.0
+
+
+# ------------------------------------------------------------------ Quantile Balancing
+
+
+def _qb_margins(s, alpha):
+    return (s - alpha[:, None]).astype(F32) + F32(0.0)
+
+
+def test_qb_worked_example(golden):
+    g = golden("qb_worked_example.txt")
+    K = int(g["K"][0][0])
+    b = np.array([frac_to_f32(v) for v in g["b"][0]], F32)
+    s = np.array([[frac_to_f32(v) for v in g[f"s{t}"][0]] for t in range(6)], F32)
+    alpha = oracle.qb_alpha(s, b, K)
+    np.testing.assert_array_equal(alpha, np.array([frac_to_f32(v) for v in g["alpha"][0]], F32))
+    target = oracle.qb_update(s, alpha, K, 0.0, b.copy())
+    np.testing.assert_array_equal(target, np.array([frac_to_f32(v) for v in g["Q"][0]], F32))
+    rho = float(g["rho"][0][0])
+    ema = oracle.qb_update(s, alpha, K, rho, b.copy())
+    np.testing.assert_array_equal(ema, np.array([frac_to_f32(v) for v in g["ema"][0]], F32))
+
+
+@pytest.mark.parametrize("kind", ["beta", "grid", "edges", "saturated"])
+def test_qb_alpha_is_the_k_plus_one_th_largest_value(kind):
+    T, E, K = 300, 48, 5
+    s = synth.scores(T, E, kind, seed=31)
+    b = synth.bias(E, "grid" if kind == "grid" else "small", seed=32)
+    alpha = oracle.qb_alpha(s, b, K)
+    v = (s + b[None, :]).astype(F32)
+    # the (K+1)-th largest value does not depend on how ties are broken
+    np.testing.assert_array_equal(alpha, -np.sort(-v, axis=1)[:, K])
+
+
+@pytest.mark.parametrize("T,E,K", [(1000, 64, 5), (777, 96, 3), (333, 32, 10)])
+def test_qb_quantile_is_numpys_inverted_cdf(T, E, K):
+    # shapes where T (E - K) / E is not an integer, so numpy's floating-point
+    # level p = 1 - K/E cannot round across an order statistic
+    assert (T * (E - K)) % E != 0
+    s = synth.scores(T, E, "beta", seed=T + E)
+    b = synth.bias(E, "small", seed=K)
+    alpha = oracle.qb_alpha(s, b, K)
+    target = oracle.qb_update(s, alpha, K, 0.0, np.zeros(E, F32))
+    d = _qb_margins(s, alpha)
+    want = -np.quantile(d, 1.0 - K / E, axis=0, method="inverted_cdf").astype(F32)
+    np.testing.assert_array_equal(target, want)
+
+
+def test_qb_target_places_k_over_e_of_the_margins_above_zero():
+    # Eq. pid-quantile-def: with the cutoffs held fixed, at most floor(m K / E)
+    # margins per expert end up above zero, and at least m - k + 1 are >= 0
+    T, E, K = 1500, 64, 6
+    s = synth.scores(T, E, "beta", seed=5)
+    b = synth.bias(E, "small", seed=6)
+    alpha = oracle.qb_alpha(s, b, K)
+    target = oracle.qb_update(s, alpha, K, 0.0, b.copy())
+    d = _qb_margins(s, alpha)
+    k = -(-(T * (E - K)) // E)
+    above = ((d + target[None, :]) > 0).sum(axis=0)
+    at_or_above = ((d + target[None, :]) >= 0).sum(axis=0)
+    assert above.max() <= (T * K) // E
+    assert at_or_above.min() >= T - k + 1
+
+
+def test_qb_target_invariant_under_per_token_score_shift():
+    # adding c_t to every score of token t shifts its cutoff by c_t, so the
+    # margins and the target are unchanged (exact on a 1/64 grid)
+    rng = np.random.default_rng(7)
+    T, E, K = 200, 16, 3
+    s = (rng.integers(0, 64, size=(T, E)) / 64.0).astype(F32)
+    b = (rng.integers(-8, 8, size=E) / 64.0).astype(F32)
+    c = (rng.integers(-16, 16, size=T) / 64.0).astype(F32)
+    base = oracle.qb_update(s, oracle.qb_alpha(s, b, K), K, 0.0, np.zeros(E, F32))
+    s2 = (s + c[:, None]).astype(F32)
+    shifted = oracle.qb_update(s2, oracle.qb_alpha(s2, b, K), K, 0.0, np.zeros(E, F32))
+    np.testing.assert_array_equal(base, shifted)
+
+
+def test_qb_ema_blends_previous_bias_and_target():
+    rng = np.random.default_rng(11)
+    T, E, K = 256, 32, 4
+    s = (rng.integers(0, 128, size=(T, E)) / 128.0).astype(F32)
+    b = (rng.integers(-32, 32, size=E) / 128.0).astype(F32)
+    alpha = oracle.qb_alpha(s, b, K)
+    target = oracle.qb_update(s, alpha, K, 0.0, b.copy())
+    for rho in (0.5, 0.75, 0.25):
+        got = oracle.qb_update(s, alpha, K, rho, b.copy())
+        want = [Fraction(rho) * Fraction(float(b[j])) + (1 - Fraction(rho)) * Fraction(float(target[j]))
+                for j in range(E)]
+        np.testing.assert_array_equal(got, np.array([frac_to_f32(v) for v in want], F32))
