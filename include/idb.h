@@ -229,6 +229,37 @@ idb_status idb_router_step(const void* x, const void* W_g, idb_dtype dtype, idb_
                            int32_t accumulate_counts, double* out_maxvio_minvio, void* workspace,
                            size_t workspace_bytes, int32_t variant, hipStream_t stream);
 
+/* ---------------------------------------------------------------------------
+ * Quantile Balancing (Eq. pid-quantile, Eq. pid-quantile-def): the paper's
+ * strongest baseline controller, on the same fused router.
+ *
+ * idb_qb_router_forward: idb_router_forward's outputs (identical values),
+ * plus, for Quantile Balancing's update,
+ *   alpha     [T] fp32 out: per token the (K+1)-th largest biased score
+ *             fl32(s + b) in the order of Eq. pid-routing (-0 written +0);
+ *   scores_t  [E][T] fp32 out: the scores s, expert-major.
+ * Needs K + 1 <= E and K + 1 <= 32, and a workspace of at least
+ * idb_qb_router_workspace_bytes() (K + 1 candidates per token and slice).
+ *
+ * idb_qb_update: for each expert j, with margins d_ij = fl32(s_ij - alpha_i)
+ * (-0 read as +0) and k = ceil(T (E - K) / E) in exact integers, q_j = the
+ * k-th smallest d_.j (the 1 - K/E quantile as the inverted empirical CDF),
+ * Q_j = -q_j, and bias[j] = Q_j for rho == 0, else the EMA variant
+ * fl32(fl32(rho bias[j]) + fl32(fl32(1 - rho) Q_j)).  scores_t [E][T] and
+ * alpha [T] as written by idb_qb_router_forward; bias [E] is updated in
+ * place.  1 <= T <= 2^26, 1 <= K < E <= 1024, 0 <= rho < 1.  One workgroup
+ * per expert (exact radix select of the k-th margin).
+ * ------------------------------------------------------------------------- */
+size_t idb_qb_router_workspace_bytes(int64_t T, int32_t d, int32_t E, int32_t K, idb_dtype dtype,
+                                     int32_t variant);
+idb_status idb_qb_router_forward(const void* x, const void* W_g, idb_dtype dtype, idb_weight_layout weight_layout,
+                                 const float* bias, int64_t T, int32_t d, int32_t E, int32_t K, int32_t* expert_idx,
+                                 float* gate_w, int32_t* counts, int32_t accumulate_counts, float* scores_t,
+                                 float* alpha, void* workspace, size_t workspace_bytes, int32_t variant,
+                                 hipStream_t stream);
+idb_status idb_qb_update(const float* scores_t, const float* alpha, int64_t T, int32_t E, int32_t K, float rho,
+                         float* bias, hipStream_t stream);
+
 /* Static description of a status code; message of the last failing call on
  * this thread (empty string if none). */
 const char* idb_status_string(idb_status s);

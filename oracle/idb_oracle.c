@@ -319,7 +319,7 @@ void oracle_qb_alpha(const float* s, const float* bias, int64_t T, int32_t E, in
                 taken[best] = 1;
                 pick = best_v;
             }
-            alpha[t] = pick;
+            alpha[t] = pick + 0.0f; /* -0 read as +0 */
         }
         free(taken);
     }

@@ -33,7 +33,8 @@ EXPORTED = (
     "idb_router_workspace_bytes", "idb_router_forward", "idb_router_score_select", "idb_router_merge",
     "idb_router_variant_info", "idb_select_from_scores", "idb_controller_update", "idb_load_stats",
     "idb_status_string", "idb_last_error", "idb_router_packed_weight_bytes", "idb_router_pack_weight",
-    "idb_controller_step", "idb_router_step",
+    "idb_controller_step", "idb_router_step", "idb_qb_router_workspace_bytes", "idb_qb_router_forward",
+    "idb_qb_update",
 )
 
 
@@ -91,6 +92,12 @@ def lib() -> ctypes.CDLL:
     L.idb_router_step.argtypes = [P, P, i32, i32, i64, i32, i32, ctypes.POINTER(idb_controller_cfg),
                                   ctypes.POINTER(idb_controller_state), P, P, P, i32, P, P, sz, i32, P]
     L.idb_router_step.restype = ctypes.c_int
+    L.idb_qb_router_workspace_bytes.argtypes = [i64, i32, i32, i32, i32, i32]
+    L.idb_qb_router_workspace_bytes.restype = sz
+    L.idb_qb_router_forward.argtypes = [P, P, i32, i32, P, i64, i32, i32, i32, P, P, P, i32, P, P, P, sz, i32, P]
+    L.idb_qb_router_forward.restype = ctypes.c_int
+    L.idb_qb_update.argtypes = [P, P, i64, i32, i32, ctypes.c_float, P, P]
+    L.idb_qb_update.restype = ctypes.c_int
     L.idb_status_string.argtypes = [ctypes.c_int]
     L.idb_status_string.restype = ctypes.c_char_p
     L.idb_last_error.argtypes = []
@@ -283,3 +290,39 @@ def idb_router_step(x, W_g, K, cfg: ControllerCfg, state: ControllerState, exper
                                int(bool(accumulate)), _ptr(out), _ptr(workspace), ws_bytes, int(variant),
                                _stream(stream))
     _check("idb_router_step", st)
+
+
+# ---------------------------------------------------------------------------- Quantile Balancing
+
+
+def idb_qb_router_workspace_bytes(T: int, d: int, E: int, K: int, dtype: int, variant: int = 0) -> int:
+    return int(lib().idb_qb_router_workspace_bytes(T, d, E, K, dtype, variant))
+
+
+def idb_qb_router_forward(x, W_g, bias, K, expert_idx, gate_w, counts, scores_t, alpha, accumulate=False,
+                          workspace=None, variant=0, stream=None, weight_layout=IDB_WEIGHT_ROW_MAJOR):
+    """Router step that also writes Quantile Balancing's inputs: ``alpha`` [T] (cutoffs) and ``scores_t`` [E][T]."""
+    T, d = x.shape
+    E = W_g.shape[0]
+    if W_g.shape[1] != d or W_g.dtype != x.dtype or bias.shape != (E,) or bias.dtype != torch.float32:
+        raise ValueError("router operands disagree in shape or dtype")
+    if expert_idx.shape != (T, K) or gate_w.shape != (T, K) or counts.shape != (E,):
+        raise ValueError("router outputs have the wrong shape")
+    if scores_t.shape != (E, T) or scores_t.dtype != torch.float32 or alpha.shape != (T,) or \
+            alpha.dtype != torch.float32:
+        raise ValueError("scores_t must be float32 [E][T] and alpha float32 [T]")
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    st = lib().idb_qb_router_forward(_ptr(x), _ptr(W_g), _dtype_code(x), int(weight_layout), _ptr(bias), T, d, E, K,
+                                     _ptr(expert_idx), _ptr(gate_w), _ptr(counts), int(bool(accumulate)),
+                                     _ptr(scores_t), _ptr(alpha), _ptr(workspace), ws_bytes, int(variant),
+                                     _stream(stream))
+    _check("idb_qb_router_forward", st)
+
+
+def idb_qb_update(scores_t, alpha, K, rho, bias, stream=None):
+    """Quantile Balancing's bias update (exact per-expert quantile; EMA for ``rho`` > 0), ``bias`` in place."""
+    E, T = scores_t.shape
+    if scores_t.dtype != torch.float32 or alpha.shape != (T,) or bias.shape != (E,) or bias.dtype != torch.float32:
+        raise ValueError("Quantile Balancing operands have the wrong shape or dtype")
+    st = lib().idb_qb_update(_ptr(scores_t), _ptr(alpha), T, E, K, float(rho), _ptr(bias), _stream(stream))
+    _check("idb_qb_update", st)

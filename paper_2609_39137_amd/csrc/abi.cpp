@@ -103,8 +103,10 @@ idb_status prepare_router(const void* x, const void* W_g, idb_dtype dtype, idb_w
                           const float* bias, int64_t T, int32_t d,
                           int32_t E, int32_t K, int32_t* expert_idx, float* gate_w, int32_t* counts,
                           int32_t accumulate_counts, float* scores_dump, void* workspace, size_t workspace_bytes,
-                          int32_t variant, bool need_inputs, RouterCall* call) {
-    idb_status st = check_router_shape(T, d, E, K, dtype);
+                          int32_t variant, bool need_inputs, RouterCall* call, bool qb = false) {
+    // Quantile Balancing keeps K + 1 candidates per token (the (K+1)-th is the cutoff)
+    const int32_t KL = qb ? K + 1 : K;
+    idb_status st = check_router_shape(T, d, E, KL, dtype);
     if (st != IDB_OK) return st;
     if (layout != IDB_WEIGHT_ROW_MAJOR && layout != IDB_WEIGHT_PACKED)
         return fail(IDB_ERR_INVALID_ARG, "unknown weight layout %d", layout);
@@ -120,7 +122,7 @@ idb_status prepare_router(const void* x, const void* W_g, idb_dtype dtype, idb_w
         return fail(IDB_ERR_INVALID_ARG, "outputs must be 4-byte aligned");
     st = resolve_tiling(E, dtype, variant, &call->tiling);
     if (st != IDB_OK) return st;
-    const size_t need = router_ws_bytes(T, E, K, call->tiling);
+    const size_t need = router_ws_bytes(T, E, KL, call->tiling);
     if (need > 0) {
         if (!workspace || workspace_bytes < need)
             return fail(IDB_ERR_INVALID_ARG, "workspace of %zu bytes needed, %zu given", need, workspace_bytes);
@@ -141,12 +143,14 @@ idb_status prepare_router(const void* x, const void* W_g, idb_dtype dtype, idb_w
     a.dump = scores_dump;
     const int ns = idb::router_slices(call->tiling, E);
     a.zero_counts = (!accumulate_counts && ns > 1) ? 1 : 0;
-    const size_t part = round_up((size_t)T * ns * K * 4);
+    const size_t part = round_up((size_t)T * ns * KL * 4);
     char* ws = static_cast<char*>(workspace);
     a.cand_v = need ? reinterpret_cast<float*>(ws) : nullptr;
     a.cand_s = need ? reinterpret_cast<float*>(ws + part) : nullptr;
     a.cand_i = need ? reinterpret_cast<int32_t*>(ws + 2 * part) : nullptr;
     a.ticket = nullptr;
+    a.alpha = nullptr;
+    a.scores_t = nullptr;
     call->ticket = need ? reinterpret_cast<unsigned*>(ws + 3 * part) : nullptr;
     return IDB_OK;
 }
@@ -338,6 +342,46 @@ idb_status idb_router_step(const void* x, const void* W_g, idb_dtype dtype, idb_
     k.stats = out_maxvio_minvio;
     k.ticket = c.ticket;
     return hip_result(idb::launch_router_merge(c.tiling, c.args, &k, stream), "router merge launch");
+}
+
+size_t idb_qb_router_workspace_bytes(int64_t T, int32_t d, int32_t E, int32_t K, idb_dtype dtype,
+                                     int32_t variant) {
+    if (K < 1 || check_router_shape(T, d, E, K + 1, dtype) != IDB_OK) return 0;
+    idb::RouterTiling t;
+    if (resolve_tiling(E, dtype, variant, &t) != IDB_OK) return 0;
+    return router_ws_bytes(T, E, K + 1, t);
+}
+
+idb_status idb_qb_router_forward(const void* x, const void* W_g, idb_dtype dtype, idb_weight_layout weight_layout,
+                                 const float* bias, int64_t T, int32_t d, int32_t E, int32_t K, int32_t* expert_idx,
+                                 float* gate_w, int32_t* counts, int32_t accumulate_counts, float* scores_t,
+                                 float* alpha, void* workspace, size_t workspace_bytes, int32_t variant,
+                                 hipStream_t stream) {
+    if (K < 1) return fail(IDB_ERR_INVALID_ARG, "K=%d below 1", K);
+    if (K + 1 > E) return fail(IDB_ERR_INVALID_ARG, "Quantile Balancing needs K + 1 <= E (K=%d, E=%d)", K, E);
+    if (!scores_t || !alpha) return fail(IDB_ERR_INVALID_ARG, "null scores_t or alpha");
+    if (!aligned(scores_t, 4) || !aligned(alpha, 4)) return fail(IDB_ERR_INVALID_ARG, "misaligned scores_t or alpha");
+    RouterCall c;
+    idb_status st = prepare_router(x, W_g, dtype, weight_layout, bias, T, d, E, K, expert_idx, gate_w, counts,
+                                   accumulate_counts, nullptr, workspace, workspace_bytes, variant, true, &c, true);
+    if (st != IDB_OK) return st;
+    c.args.alpha = alpha;
+    c.args.scores_t = scores_t;
+    st = enqueue_score_select(c, accumulate_counts, stream);
+    if (st != IDB_OK) return st;
+    return hip_result(idb::launch_router_merge(c.tiling, c.args, nullptr, stream), "router merge launch");
+}
+
+idb_status idb_qb_update(const float* scores_t, const float* alpha, int64_t T, int32_t E, int32_t K, float rho,
+                         float* bias, hipStream_t stream) {
+    if (!scores_t || !alpha || !bias) return fail(IDB_ERR_INVALID_ARG, "null pointer");
+    if (T < 1 || T > kMaxTokens) return fail(IDB_ERR_INVALID_ARG, "T=%lld out of [1, 2^26]", (long long)T);
+    if (E < 2 || E > kMaxExperts) return fail(IDB_ERR_INVALID_ARG, "E=%d out of [2, %d]", E, kMaxExperts);
+    if (K < 1 || K >= E) return fail(IDB_ERR_INVALID_ARG, "need 1 <= K < E (K=%d, E=%d)", K, E);
+    if (!(rho >= 0.0f && rho < 1.0f)) return fail(IDB_ERR_INVALID_ARG, "rho must lie in [0, 1)");
+    if (!aligned(scores_t, 4) || !aligned(alpha, 4) || !aligned(bias, 4))
+        return fail(IDB_ERR_INVALID_ARG, "misaligned buffer");
+    return hip_result(idb::launch_qb_update(scores_t, alpha, T, E, K, rho, bias, stream), "Quantile Balancing launch");
 }
 
 idb_status idb_load_stats(const int32_t* counts, int32_t E, double* out_maxvio_minvio, hipStream_t stream) {

@@ -37,6 +37,12 @@ __device__ __forceinline__ unsigned long long rank_key(float v, int idx) {
     return ((unsigned long long)o << 32) | (unsigned)(~(unsigned)idx);
 }
 
+// The value of a rank key (inverse of its high word; -0 comes back as +0).
+__device__ __forceinline__ float rank_key_value(unsigned long long key) {
+    const unsigned o = (unsigned)(key >> 32);
+    return __uint_as_float((o & 0x80000000u) ? (o & 0x7fffffffu) : ~o);
+}
+
 // Score activation s = sigmoid(z) = 1 / (1 + 2^(-z log2 e)) with the hardware
 // exp2 and reciprocal (each about 1 ulp).  Saturates to exactly 0 and 1.
 __device__ __forceinline__ float sigmoid_fast(float z) {

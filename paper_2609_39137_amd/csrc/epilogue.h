@@ -22,6 +22,10 @@
 //   G. One slice: gate weights, outputs and an LDS histogram flushed with one
 //      atomic per non-zero bin.  Several slices: the slice's K candidates go
 //      to the workspace for the slice merge.
+// With a.alpha set (Quantile Balancing), K + 1 candidates are kept in steps
+// C-G and the biased value of rank K (the cutoff alpha of Eq.
+// pid-quantile-def) is written per token; with a.scores_t set, the scores are
+// also written expert-major after step A.
 #pragma once
 
 #include "common.h"
@@ -74,6 +78,7 @@ struct EpiCfg {
     static_assert(VPT * TPT == BE && VPT % 16 == 0 && GSZ * GPT == VPT && GPT * TPT == NG, "columns split evenly");
     static_assert(TPP * RS * 4 <= SCORE_LDS, "score rows of a pass fit");
     static_assert(TPP <= 16 * 32, "overflow bitmask size");
+    static_assert(NT % TPP == 0, "whole token rows per thread group");
     static_assert(LDS <= 160 * 1024, "LDS of one workgroup");
 };
 
@@ -129,7 +134,8 @@ __device__ __forceinline__ void epi_tile(const RouterArgs& a, int NS, int slice,
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int64_t T = a.T;
     const int E = a.E;
-    const int K = a.K;
+    const int K = a.K;        // experts selected per token
+    const int KL = a.alpha ? K + 1 : K;  // candidates kept per token (the (K+1)-th gives the cutoff)
     const int sbase = slice * C::BE;
     float* sc = reinterpret_cast<float*>(smem + C::OFF_SC);
     float* bias_s = reinterpret_cast<float*>(smem + C::OFF_BIAS);
@@ -161,6 +167,26 @@ __device__ __forceinline__ void epi_tile(const RouterArgs& a, int NS, int slice,
         store_pass(pass, sc);
         if (tid < 16) ovf[tid] = 0;
         __syncthreads();
+
+        // The scores also go out expert-major, [E][T] (Quantile Balancing's
+        // input): a thread takes a token row and every (NT/TPP)-th group of 4
+        // experts, so each store instruction covers TPP consecutive tokens.
+        if (a.scores_t) {
+            const int row = tid % C::TPP;
+            const int64_t tok = tok0 + pass * C::TPP + row;
+            if (tok < T) {
+                for (int c4 = 4 * (tid / C::TPP); c4 < C::BE; c4 += 4 * (C::NT / C::TPP)) {
+                    const int e = sbase + c4;
+                    if (e < E) {
+                        const float4 v4 = *reinterpret_cast<const float4*>(sc + row * C::RS + c4);
+                        a.scores_t[(int64_t)e * T + tok] = v4.x;
+                        if (e + 1 < E) a.scores_t[(int64_t)(e + 1) * T + tok] = v4.y;
+                        if (e + 2 < E) a.scores_t[(int64_t)(e + 2) * T + tok] = v4.z;
+                        if (e + 3 < E) a.scores_t[(int64_t)(e + 3) * T + tok] = v4.w;
+                    }
+                }
+            }
+        }
 
         // B. biased values of this thread's columns; group maxima
         float v[C::VPT];
@@ -209,7 +235,7 @@ __device__ __forceinline__ void epi_tile(const RouterArgs& a, int NS, int slice,
                 int ge = 0;
 #pragma unroll
                 for (int j = 0; j < C::NG; ++j) ge += (g[j] >= own[i]) ? 1 : 0;
-                if (ge >= K) tau = fmaxf(tau, own[i]);
+                if (ge >= KL) tau = fmaxf(tau, own[i]);
             }
 #pragma unroll
             for (int o = 1; o < C::TPT; o <<= 1) tau = fmaxf(tau, __shfl_xor(tau, o));
@@ -277,7 +303,7 @@ __device__ __forceinline__ void epi_tile(const RouterArgs& a, int NS, int slice,
             }
 #pragma unroll
             for (int i = 0; i < C::NCI; ++i)
-                if (q + C::TPT * i < n && rank[i] < K) si[tl * C::LSS + rank[i]] = (int)~(unsigned)mine[i];
+                if (q + C::TPT * i < n && rank[i] < KL) si[tl * C::LSS + rank[i]] = (int)~(unsigned)mine[i];
         }
 
         // F. overflowing tokens, one wave each (the bitmask is uniform: it was
@@ -291,7 +317,7 @@ __device__ __forceinline__ void epi_tile(const RouterArgs& a, int NS, int slice,
                     bits &= bits - 1u;
                     if ((k++ % WAVES) != wave) continue;
                     unsigned long long prev = ~0ull;
-                    for (int r = 0; r < K; ++r) {
+                    for (int r = 0; r < KL; ++r) {
                         unsigned long long best = 0ull;
                         for (int c = lane; c < C::BE; c += 64) {
                             if (sbase + c < E) {
@@ -320,8 +346,8 @@ __device__ __forceinline__ void epi_tile(const RouterArgs& a, int NS, int slice,
             const int64_t tok = tok0 + pass * C::TPP + tl;
             if (tok < T) {
                 if (NS > 1) {
-                    const int64_t base = (tok * NS + slice) * K;
-                    for (int r = q; r < K; r += C::TPT) {
+                    const int64_t base = (tok * NS + slice) * KL;
+                    for (int r = q; r < KL; r += C::TPT) {
                         const int e = si[tl * C::LSS + r];
                         const float s = sc[tl * C::RS + (e - sbase)];
                         a.cand_v[base + r] = s + bias_s[e - sbase];
@@ -340,6 +366,11 @@ __device__ __forceinline__ void epi_tile(const RouterArgs& a, int NS, int slice,
                         a.idx[tok * K + r] = e;
                         a.w[tok * K + r] = (den == 0.0f) ? 1.0f / (float)K : s / den;
                         atomicAdd(&hist[e], 1);
+                    }
+                    if (a.alpha && q == 0) {
+                        // cutoff: the biased value of rank K
+                        const int e = si[tl * C::LSS + K];
+                        a.alpha[tok] = (sc[tl * C::RS + (e - sbase)] + bias_s[e - sbase]) + 0.0f;
                     }
                 }
             }

@@ -15,6 +15,9 @@ hipError_t launch_controller_update(const int32_t* counts, int E, float Ki, floa
 hipError_t launch_load_stats(const int32_t* counts, int E, double* out, hipStream_t stream);
 
 hipError_t launch_fill_i32(int32_t* p, int32_t value, int64_t n, hipStream_t stream);
+// Quantile Balancing's bias update from expert-major scores and cutoffs.
+hipError_t launch_qb_update(const float* scores_t, const float* alpha, int64_t T, int E, int K, float rho,
+                            float* bias, hipStream_t stream);
 // Selection from given scores; counts must already hold the starting values.
 hipError_t launch_select_from_scores(const float* scores, const float* bias, int64_t T, int E, int K,
                                      int32_t* idx, float* w, int32_t* counts, hipStream_t stream);
@@ -48,10 +51,15 @@ struct RouterArgs {
     int zero_counts;  // workgroup 0 of the multi-slice kernel zeroes counts
     unsigned* ticket;  // nullable; workgroup 0 of the multi-slice kernel zeroes it
     float* dump;
-    // multi-slice candidates in the workspace: [T][slices][K]
+    // multi-slice candidates in the workspace: [T][slices][KL], KL = K, or
+    // K + 1 with alpha set
     float* cand_v;
     float* cand_s;
     int32_t* cand_i;
+    // Quantile Balancing (Eq. pid-quantile-def), both nullable: alpha [T] the
+    // (K+1)-th largest biased score per token; scores_t [E][T] the scores.
+    float* alpha;
+    float* scores_t;
 };
 
 // Slices of E covered by one workgroup column for tiling t.

@@ -465,11 +465,12 @@ __global__ __launch_bounds__(kMergeThreads) void router_merge_kernel(RouterArgs 
     __shared__ unsigned long long key[kMergeThreads];
     __shared__ float sel[kMergeThreads];  // selected scores, [token of the group][rank]
     const int E = a.E, K = a.K;
-    const int per_tok = NS * K;  // <= kMaxSlices * kMaxK = kMergeThreads
+    const int KL = a.alpha ? K + 1 : K;  // candidates per slice
+    const int per_tok = NS * KL;         // <= kMaxSlices * kMaxK = kMergeThreads
     const int tpg = kMergeThreads / per_tok;
     const int tid = threadIdx.x;
     const int tt = tid / per_tok, pos = tid - tt * per_tok;
-    const int sl = pos / K, r = pos - sl * K;
+    const int sl = pos / KL, r = pos - sl * KL;
     for (int e = tid; e < E; e += kMergeThreads) hist[e] = 0;
     const int64_t groups = (a.T + tpg - 1) / tpg;
     for (int64_t g = blockIdx.x; g < groups; g += gridDim.x) {
@@ -491,13 +492,15 @@ __global__ __launch_bounds__(kMergeThreads) void router_merge_kernel(RouterArgs 
         if (act) {
             for (int o = 0; o < NS; ++o) {
                 if (o == sl) continue;
-                const int b = tt * per_tok + o * K;
-                for (int j = 0; j < K; ++j) rank += (key[b + j] > k) ? 1 : 0;
+                const int b = tt * per_tok + o * KL;
+                for (int j = 0; j < KL; ++j) rank += (key[b + j] > k) ? 1 : 0;
             }
             if (rank < K) {
                 sel[tt * K + rank] = s;
                 a.idx[tok * K + rank] = e;
                 atomicAdd(&hist[e], 1);
+            } else if (rank == K && a.alpha) {
+                a.alpha[tok] = rank_key_value(k);  // the cutoff: the biased value of rank K
             }
         }
         __syncthreads();
@@ -536,7 +539,8 @@ __global__ __launch_bounds__(kTileThreads) void router_merge_tile_kernel(RouterA
     __shared__ float msel[kTileTokens * kMaxK];
     __shared__ int midx[kTileTokens * kMaxK];
     const int E = a.E, K = a.K;
-    const int NSK = NS * K;  // <= 64
+    const int KL = a.alpha ? K + 1 : K;  // candidates per slice
+    const int NSK = NS * KL;             // <= 64
     const int tid = threadIdx.x;
     for (int e = tid; e < E; e += kTileThreads) hist[e] = 0;
     const int64_t ntiles = (a.T + kTileTokens - 1) / kTileTokens;
@@ -583,9 +587,9 @@ __global__ __launch_bounds__(kTileThreads) void router_merge_tile_kernel(RouterA
             // exhausted list).
             for (int t = tid; t < ntok; t += kTileThreads) {
                 const unsigned long long* L0 = mk + t * NSK;
-                const unsigned long long* L1 = L0 + K;
+                const unsigned long long* L1 = L0 + KL;
                 const float* S0 = ms + t * NSK;
-                const float* S1 = S0 + K;
+                const float* S1 = S0 + KL;
                 int p0 = 0, p1 = 0;
                 unsigned long long k0 = L0[0], k1 = L1[0];
                 for (int r = 0; r < K; ++r) {
@@ -595,30 +599,34 @@ __global__ __launch_bounds__(kTileThreads) void router_merge_tile_kernel(RouterA
                     midx[t * kMaxK + r] = (int)~(unsigned)k;
                     if (take0) {
                         ++p0;
-                        k0 = p0 < K ? L0[p0] : 0ull;
+                        k0 = p0 < KL ? L0[p0] : 0ull;
                     } else {
                         ++p1;
-                        k1 = p1 < K ? L1[p1] : 0ull;
+                        k1 = p1 < KL ? L1[p1] : 0ull;
                     }
                 }
+                // the cutoff: the biased value of rank K
+                if (a.alpha) a.alpha[tok0 + t] = rank_key_value(k0 > k1 ? k0 : k1);
             }
         } else {
             // A candidate's final rank: its rank in its own slice plus the
             // other slices' candidates above it.
             for (int c = tid; c < n; c += kTileThreads) {
                 const int t = c / NSK, pos = c - t * NSK;
-                const int sl = pos / K, r = pos - sl * K;
+                const int sl = pos / KL, r = pos - sl * KL;
                 const unsigned long long k = mk[c];
                 int rank = r;
                 for (int o = 0; o < NS; ++o) {
                     if (o == sl) continue;
-                    const unsigned long long* lo = mk + t * NSK + o * K;
+                    const unsigned long long* lo = mk + t * NSK + o * KL;
 #pragma unroll 8
-                    for (int j = 0; j < K; ++j) rank += (lo[j] > k) ? 1 : 0;
+                    for (int j = 0; j < KL; ++j) rank += (lo[j] > k) ? 1 : 0;
                 }
                 if (rank < K) {
                     msel[t * kMaxK + rank] = ms[c];
                     midx[t * kMaxK + rank] = (int)~(unsigned)k;
+                } else if (rank == K && a.alpha) {
+                    a.alpha[tok0 + t] = rank_key_value(k);
                 }
             }
         }
@@ -720,14 +728,15 @@ hipError_t launch_router_merge(const RouterTiling& t, const RouterArgs& a, const
     if (NS <= 1) return hipSuccess;
     CtrlArgs c{};
     if (ctrl) c = *ctrl;
-    if (NS * a.K <= 64) {
+    const int KL = a.alpha ? a.K + 1 : a.K;
+    if (NS * KL <= 64) {
         int64_t blocks = (a.T + kTileTokens - 1) / kTileTokens;
         if (blocks > kTileBlocks) blocks = kTileBlocks;
         hipLaunchKernelGGL(router_merge_tile_kernel, dim3((unsigned)blocks), dim3(kTileThreads), 0, stream, a, NS,
                            c);
         return hipGetLastError();
     }
-    const int tpg = kMergeThreads / (NS * a.K);
+    const int tpg = kMergeThreads / (NS * KL);
     int64_t groups = (a.T + tpg - 1) / tpg;
     if (groups > kMergeBlocks) groups = kMergeBlocks;
     hipLaunchKernelGGL(router_merge_kernel, dim3((unsigned)groups), dim3(kMergeThreads), 0, stream, a, NS, c);

@@ -76,3 +76,27 @@ class RouterStep:
         Wt, layout = self._weights(W)
         B.idb_router_step(x, Wt, self.K, self.cfg, self.state, self.idx, self.w, self.counts, accumulate,
                           self.stats, self.workspace, self.variant, stream, layout)
+
+    # ------------------------------------------------------------ Quantile Balancing
+
+    def qb_buffers(self):
+        """Allocate (once) the Quantile Balancing inputs and its larger workspace."""
+        if getattr(self, "scores_t", None) is None:
+            dev = self.idx.device
+            self.scores_t = torch.empty((self.E, self.T), dtype=torch.float32, device=dev)
+            self.alpha = torch.empty(self.T, dtype=torch.float32, device=dev)
+            n = B.idb_qb_router_workspace_bytes(self.T, self.d, self.E, self.K, self.dtype_code, self.variant)
+            self.qb_workspace = torch.empty(max(n, 16), dtype=torch.uint8, device=dev)
+
+    def qb_route(self, x, W=None, accumulate: bool = False, stream=None):
+        """Route with the current bias and write Quantile Balancing's cutoffs and expert-major scores."""
+        self.qb_buffers()
+        Wt, layout = self._weights(W)
+        B.idb_qb_router_forward(x, Wt, self.state.bias, self.K, self.idx, self.w, self.counts, self.scores_t,
+                                self.alpha, accumulate, self.qb_workspace, self.variant, stream, layout)
+
+    def qb_step(self, x, W=None, rho: float = 0.0, stream=None):
+        """One Quantile Balancing iteration (Eq. pid-quantile): route, MaxVio/MinVio, then the bias target."""
+        self.qb_route(x, W, stream=stream)
+        B.idb_load_stats(self.counts, self.stats, stream)
+        B.idb_qb_update(self.scores_t, self.alpha, self.K, rho, self.state.bias, stream)

@@ -213,3 +213,50 @@ def test_binding_rejects_short_score_dump():
     c = torch.zeros(E, dtype=torch.int32)
     with pytest.raises(ValueError, match="scores_dump"):
         B.idb_router_forward(x, W, b, K, idx, w, c, scores_dump=torch.zeros(T * E // 2, dtype=torch.float32))
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(K=0), B.IDB_ERR_INVALID_ARG),
+    (dict(E=32, K=32), B.IDB_ERR_INVALID_ARG),     # K + 1 > E
+    (dict(K=32), B.IDB_ERR_UNSUPPORTED),           # K + 1 candidates above 32
+    (dict(st=None), B.IDB_ERR_INVALID_ARG),
+    (dict(alpha=None), B.IDB_ERR_INVALID_ARG),
+    (dict(alpha=A16 + 2), B.IDB_ERR_INVALID_ARG),
+    (dict(ws_bytes=3 * 128 * 2 * 10 * 4 + 256, variant=6), B.IDB_ERR_INVALID_ARG),  # sized for K, not K + 1
+    (dict(x=None), B.IDB_ERR_INVALID_ARG),
+    (dict(E=100), B.IDB_ERR_UNSUPPORTED),
+])
+def test_qb_router_rejects_invalid_arguments(kw, code):
+    a = dict(x=A16, W=A16, T=128, d=256, E=768, K=10, st=A16, alpha=A16, ws=A16, ws_bytes=1 << 30, variant=0)
+    a.update(kw)
+    st = B.lib().idb_qb_router_forward(a["x"], a["W"], B.IDB_DTYPE_BF16, 0, A16, a["T"], a["d"], a["E"], a["K"],
+                                       A16, A16, A16, 0, a["st"], a["alpha"], a["ws"], a["ws_bytes"], a["variant"],
+                                       None)
+    assert st == code
+    assert B.idb_last_error() != ""
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(st=None), B.IDB_ERR_INVALID_ARG),
+    (dict(bias=None), B.IDB_ERR_INVALID_ARG),
+    (dict(T=0), B.IDB_ERR_INVALID_ARG),
+    (dict(E=1, K=0), B.IDB_ERR_INVALID_ARG),
+    (dict(K=0), B.IDB_ERR_INVALID_ARG),
+    (dict(K=768), B.IDB_ERR_INVALID_ARG),
+    (dict(E=1025), B.IDB_ERR_INVALID_ARG),
+    (dict(rho=1.0), B.IDB_ERR_INVALID_ARG),
+    (dict(rho=-0.25), B.IDB_ERR_INVALID_ARG),
+    (dict(rho=float("nan")), B.IDB_ERR_INVALID_ARG),
+    (dict(alpha=A16 + 1), B.IDB_ERR_INVALID_ARG),
+])
+def test_qb_update_rejects_invalid_arguments(kw, code):
+    a = dict(st=A16, alpha=A16, T=16384, E=768, K=10, rho=0.0, bias=A16)
+    a.update(kw)
+    assert B.lib().idb_qb_update(a["st"], a["alpha"], a["T"], a["E"], a["K"], a["rho"], a["bias"], None) == code
+
+
+def test_qb_workspace_holds_k_plus_one_candidates():
+    assert B.idb_qb_router_workspace_bytes(16384, 2048, 768, 10, B.IDB_DTYPE_BF16, 0) == \
+        B.idb_router_workspace_bytes(16384, 2048, 768, 11, B.IDB_DTYPE_BF16, 0)
+    assert B.idb_qb_router_workspace_bytes(16384, 2048, 768, 32, B.IDB_DTYPE_BF16, 0) == 0
+    assert B.idb_qb_router_workspace_bytes(16384, 2048, 768, 10, B.IDB_DTYPE_BF16, 7) == 0  # one slice
