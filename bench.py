@@ -104,6 +104,9 @@ def main() -> int:
                     help="eager copy calibration + a few router launches, for rocprofv3 counter passes")
     ap.add_argument("--copy-mib", type=int, default=512, help="size of the calibration copy of --pmc-pass")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--controller", choices=("id", "qb"), default="id",
+                    help="id: ID Balancing (the headline step); qb: Quantile Balancing, the paper's baseline")
+    ap.add_argument("--rho", type=float, default=0.0, help="Quantile Balancing EMA weight (0: the plain target)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="wall-clock target of the CPU oracle sample")
     args = ap.parse_args()
 
@@ -146,9 +149,14 @@ def main() -> int:
     stream = torch.cuda.Stream()  # default priority
     torch.cuda.synchronize()
 
+    qb = args.controller == "qb"
+
     def one_step(i):
         rs.pack(W, stream=stream)
-        rs.step(xs[i % nbuf], None, stream=stream)
+        if qb:
+            rs.qb_step(xs[i % nbuf], None, rho=args.rho, stream=stream)
+        else:
+            rs.step(xs[i % nbuf], None, stream=stream)
 
     # eager warm-up (also validates every call)
     with torch.cuda.stream(stream):
@@ -217,6 +225,8 @@ def main() -> int:
     assert int(counts.sum()) == wl.T * wl.K, "counts do not sum to T*K"
     assert int(rs.state.status.item()) == 0
     stats = rs.stats.cpu().tolist()
+    if qb:
+        return qb_report(args, wl, rs, xs, nbuf, stream, capture, ms_step, stats)
 
     # live timing of the dominant kernel: back-to-back launches of the fused
     # router kernel alone, on the stream the steps run on, between HIP events
@@ -320,6 +330,67 @@ def main() -> int:
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on a bounded sample")
         out["cpu_baseline"] = cpu_baseline(wl, W_np, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+def qb_report(args, wl, rs, xs, nbuf, stream, capture, ms_step, stats) -> int:
+    """JSON line of the Quantile Balancing step (router in its QB mode, MaxVio/MinVio, the update)."""
+    import torch
+
+    from paper_2609_39137_amd import binding as B
+
+    def time_per_call(fn, per, reps):
+        g = capture(fn, per)
+        with torch.cuda.stream(stream):
+            g.replay()
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        with torch.cuda.stream(stream):
+            for _ in range(reps):
+                g.replay()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / (reps * per)
+
+    per = nbuf * max(1, 16 // nbuf)
+    reps = max(1, -(-max(args.steps, 64) // per))
+    route_ms = time_per_call(lambda i: rs.qb_route(xs[i % nbuf], None, stream=stream), per, reps)
+    upd_ms = time_per_call(lambda i: B.idb_qb_update(rs.scores_t, rs.alpha, wl.K, args.rho, rs.state.bias, stream),
+                           per, reps)
+    log(f"router in QB mode (fused kernel + slice merge): {route_ms * 1000:.2f} us; update {upd_ms * 1000:.2f} us")
+    achieved = wl.flops / (route_ms * 1e-3) / 1e12
+    peak = PEAK_BF16_TFLOPS if wl.dtype == "bf16" else PEAK_F32_TFLOPS
+    upd_bytes = wl.E * wl.T * 4 + wl.T * 4 + 2 * wl.E * 4
+    upd_gbs = upd_bytes / (upd_ms * 1e-3) / 1e9
+    out = {
+        "metric": "routed tokens/sec for router + Quantile Balancing step (the paper's baseline controller)",
+        "value": round(wl.T / (ms_step * 1e-3), 1),
+        "unit": "routed tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": wl.dtype,
+        "data": "synthetic",
+        "config": {"workload": wl.name, "T": wl.T, "d": wl.d, "E": wl.E, "K": wl.K, "global_batch": wl.T,
+                   "parallelism": "single GPU", "variant": rs.info["variant"], "controller": "quantile-balancing",
+                   "rho": args.rho, "launch": f"hip-graph of {nbuf} steps", "input_buffers": nbuf},
+        "roofline": {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
+                     "frac": round(achieved / peak, 4), "traffic": None,
+                     "kernel": "router in Quantile Balancing mode: fused kernel (K+1 candidates, expert-major "
+                               "scores written) + slice merge",
+                     "kernel_us": round(route_ms * 1000, 2), "flops_per_launch": wl.flops},
+        "qb_update_roofline": {"bound": "hbm", "achieved": round(upd_gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                               "frac": round(upd_gbs / PEAK_HBM_GBS, 4), "kernel": "qb_update_kernel",
+                               "kernel_us": round(upd_ms * 1000, 2), "bytes_per_launch": upd_bytes},
+        "last_step": {"maxvio": stats[0], "minvio": stats[1]},
+    }
     print(json.dumps(out), flush=True)
     return 0
 
