@@ -16,6 +16,9 @@ readings of points the paper leaves open):
 * :func:`controller` -- one ID bias update (Alg. 1, Eq. rapid-update) or the
   DeepSeek sign rule (Eq. pid-deepseek)
 * :func:`load_stats` -- MaxVio / MinVio (Eq. vio)
+* :func:`controller_diag` -- one update plus its diagnostics (active-gate
+  fraction, busiest-10% share, inactive-expert ratio, mean |bias change|)
+* :func:`topk_entropy`, :func:`full_entropy` -- routing entropies (Sec. 4.3)
 * :func:`qb_alpha`, :func:`qb_update` -- Quantile Balancing's cutoffs and
   target bias, with the EMA variant (Eq. pid-quantile, Eq. pid-quantile-def)
 """
@@ -79,6 +82,12 @@ def _declare(lib):
     lib.oracle_load_stats.argtypes = [P, i32, P]
     lib.oracle_step_seconds.argtypes = [P, P, c_int, i64, i32, i32, i32, f32, f32, P, P, P, P, P, P, P, P]
     lib.oracle_step_seconds.restype = ctypes.c_double
+    lib.oracle_controller_diag.argtypes = [P, i32, f32, f32, c_int, c_int, P, P, P, P, P]
+    lib.oracle_controller_diag.restype = c_int
+    lib.oracle_topk_entropy.argtypes = [P, i64, i32]
+    lib.oracle_topk_entropy.restype = ctypes.c_double
+    lib.oracle_full_entropy.argtypes = [P, P, i64, i32]
+    lib.oracle_full_entropy.restype = ctypes.c_double
     lib.oracle_qb_alpha.argtypes = [P, P, i64, i32, i32, P]
     lib.oracle_qb_update.argtypes = [P, P, i64, i32, i32, f32, P]
     return lib
@@ -236,3 +245,29 @@ def qb_update(scores: np.ndarray, alpha: np.ndarray, K: int, rho: float, bias: n
     assert bias.flags.c_contiguous
     lib.oracle_qb_update(_ptr(s), _ptr(a), T, E, K, float(rho), _ptr(bias))
     return bias
+
+
+def controller_diag(counts: np.ndarray, state: ControllerState, Ki: float, Kd: float, mode: int = MODE_ERROR,
+                    center: bool = True):
+    """One bias update in place plus ``[active-gate fraction, busiest-10% share, inactive ratio, mean |db|]``."""
+    lib = _load()
+    c = np.ascontiguousarray(counts, dtype=np.int32)
+    E = len(c)
+    diag = np.empty(4, np.float64)
+    st = lib.oracle_controller_diag(_ptr(c), E, float(Ki), float(Kd), int(mode), int(bool(center)),
+                                    _ptr(state.bias), _ptr(state.e_prev), _ptr(state.step), _ptr(state.status),
+                                    _ptr(diag))
+    return int(st), diag
+
+
+def topk_entropy(w: np.ndarray) -> float:
+    """Mean over tokens of H_topK = -sum w log w (nats) for gate weights ``w`` [T][K]."""
+    a = np.ascontiguousarray(w, dtype=np.float32)
+    return float(_load().oracle_topk_entropy(_ptr(a), a.shape[0], a.shape[1]))
+
+
+def full_entropy(scores: np.ndarray, bias: np.ndarray) -> float:
+    """Mean over tokens of H_full over the clamped biased scores max(s + b, 0), normalised (nats)."""
+    s = np.ascontiguousarray(scores, dtype=np.float32)
+    b = np.ascontiguousarray(bias, dtype=np.float32)
+    return float(_load().oracle_full_entropy(_ptr(s), _ptr(b), s.shape[0], s.shape[1]))

@@ -23,6 +23,10 @@
  *                                                            rapid-update)
  *   SIGN mode: DeepSeek's fixed-step integral rule         (Eq. pid-deepseek)
  *   S1  MaxVio / MinVio                                    (Sec. 4.1, Eq. vio)
+ *   D1..D4 controller diagnostics: active-gate fraction,  (Sec. 3 text after Eq.
+ *          busiest-10% share, inactive-expert ratio, mean    rapid-gate and its figure;
+ *          absolute bias change                              Sec. 4.3; Sec. 3 bias drift)
+ *   H1, H2 top-K and full-pool score entropy               (Sec. 4.3)
  *   Q1..Q4 Quantile Balancing's target bias, with the EMA   (Eq. pid-quantile,
  *          variant used as a diagnostic                      Eq. pid-quantile-def; Sec. 3,
  *                                                            EMA smoothing of the target)
@@ -44,6 +48,17 @@
  *     power of two P >= E, then a_j <- a_j + a_{j+h} for h = P/2, ..., 1.
  *   - an empty batch (sum of counts == 0) leaves the state untouched and
  *     reports status 3; a negative count reports status 1.
+ *   - Diagnostics of one update: the active-gate fraction is #{g_i = 1} / E;
+ *     the busiest-10% share is the sum of the m = ceil(E / 10) largest counts
+ *     over S; the inactive-expert ratio is #{n_i = 0} / E; the mean absolute
+ *     bias change is (1/E) sum |fl32(b_new - b_old)| summed in fp64 over the
+ *     fixed pairwise tree (padded with +0 to a power of two); each ratio is one
+ *     fp64 division.  All four are NaN when the update does not run.
+ *   - Entropies in nats with natural logarithms in fp64: H_topK = -sum_r w_r
+ *     log w_r over a token's gate weights (0 log 0 = 0); H_full = -sum_e p_e
+ *     log p_e with p_e = max(s_e + b_e, 0) / sum of those (the biased sigmoid
+ *     score clamped at zero, normalised; H_full = 0 when the sum is 0); both
+ *     averaged over the tokens in fp64, tokens in order.
  *   - Quantile Balancing: the cutoff alpha_i is the (K+1)-th largest biased
  *     score fl32(s + b) of token i; margins are fl32(s_ij - alpha_i) with -0
  *     read as +0; quantile_{1-K/E} over the m tokens of a batch is the
@@ -271,6 +286,103 @@ int oracle_controller(const int32_t* counts, int32_t E, float Ki, float Kd, int 
     free(e);
     free(bt);
     return *status;
+}
+
+static int cmp_int_desc(const void* a, const void* b) {
+    int32_t x = *(const int32_t*)a, y = *(const int32_t*)b;
+    return (x < y) - (x > y);
+}
+
+/* One controller call (as oracle_controller) plus its diagnostics D1-D4:
+ * diag[0] active-gate fraction (Eq. rapid-gate; Sec. 3 reports its
+ * trajectory), diag[1] share of the assignments on the busiest 10% of
+ * experts, diag[2] inactive-expert ratio (Sec. 4.3), diag[3] mean absolute
+ * bias change of this update.  NaN x 4 when the update does not run. */
+int oracle_controller_diag(const int32_t* counts, int32_t E, float Ki, float Kd, int mode, int center, float* bias,
+                           float* e_prev, int64_t* step, int32_t* status, double* diag) {
+    float* b_old = (float*)malloc(sizeof(float) * (size_t)E);
+    float* ep_old = (float*)malloc(sizeof(float) * (size_t)E);
+    memcpy(b_old, bias, sizeof(float) * (size_t)E);
+    memcpy(ep_old, e_prev, sizeof(float) * (size_t)E);
+    int st = oracle_controller(counts, E, Ki, Kd, mode, center, bias, e_prev, step, status);
+    if (st != ORACLE_STATUS_OK) {
+        for (int q = 0; q < 4; ++q) diag[q] = NAN;
+        free(b_old);
+        free(ep_old);
+        return st;
+    }
+    int64_t S = 0;
+    int32_t gates = 0, zeros = 0;
+    for (int32_t i = 0; i < E; ++i) S += counts[i];
+    for (int32_t i = 0; i < E; ++i) {
+        /* D1: the gate of this update, from the error it used (C2-C4) */
+        int64_t num = S - (int64_t)E * (int64_t)counts[i];
+        float e = (float)((double)num / (double)S);
+        float de = e - ep_old[i];
+        gates += (ep_old[i] > 0.0f && de > 0.0f) || (ep_old[i] < 0.0f && de < 0.0f);
+        zeros += counts[i] == 0; /* D3 */
+    }
+    /* D2: the m = ceil(E / 10) largest counts */
+    int32_t* sorted = (int32_t*)malloc(sizeof(int32_t) * (size_t)E);
+    memcpy(sorted, counts, sizeof(int32_t) * (size_t)E);
+    qsort(sorted, (size_t)E, sizeof(int32_t), cmp_int_desc);
+    const int32_t m = (E + 9) / 10;
+    int64_t top = 0;
+    for (int32_t i = 0; i < m; ++i) top += sorted[i];
+    /* D4: mean |b_new - b_old|, fp64 pairwise tree */
+    int32_t P = 1;
+    while (P < E) P *= 2;
+    double* a = (double*)malloc(sizeof(double) * (size_t)P);
+    for (int32_t j = 0; j < P; ++j) a[j] = (j < E) ? (double)fabsf(bias[j] - b_old[j]) : 0.0;
+    for (int32_t h = P / 2; h >= 1; h /= 2)
+        for (int32_t j = 0; j < h; ++j) a[j] = a[j] + a[j + h];
+    diag[0] = (double)gates / (double)E;
+    diag[1] = (double)top / (double)S;
+    diag[2] = (double)zeros / (double)E;
+    diag[3] = a[0] / (double)E;
+    free(a);
+    free(sorted);
+    free(b_old);
+    free(ep_old);
+    return st;
+}
+
+/* H1: mean over T tokens of H_topK = -sum_r w_r log w_r (nats), w [T][K]. */
+double oracle_topk_entropy(const float* w, int64_t T, int32_t K) {
+    double acc = 0.0;
+    for (int64_t t = 0; t < T; ++t) {
+        double h = 0.0;
+        for (int32_t r = 0; r < K; ++r) {
+            double x = (double)w[t * (int64_t)K + r];
+            if (x > 0.0) h -= x * log(x);
+        }
+        acc += h;
+    }
+    return acc / (double)T;
+}
+
+/* H2: mean over T tokens of H_full = -sum_e p_e log p_e, p_e = c_e / sum c,
+ * c_e = max(fl32(s_e + b_e), 0) (the clamped biased sigmoid score). */
+double oracle_full_entropy(const float* s, const float* bias, int64_t T, int32_t E) {
+    double acc = 0.0;
+    for (int64_t t = 0; t < T; ++t) {
+        double C = 0.0;
+        for (int32_t e = 0; e < E; ++e) {
+            float v = s[t * (int64_t)E + e] + bias[e];
+            if (v > 0.0f) C += (double)v;
+        }
+        double h = 0.0;
+        if (C > 0.0)
+            for (int32_t e = 0; e < E; ++e) {
+                float v = s[t * (int64_t)E + e] + bias[e];
+                if (v > 0.0f) {
+                    double p = (double)v / C;
+                    h -= p * log(p);
+                }
+            }
+        acc += h;
+    }
+    return acc / (double)T;
 }
 
 /* S1: MaxVio = (max n - nbar)/nbar, MinVio = (nbar - min n)/nbar (Eq. vio),

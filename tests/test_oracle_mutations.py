@@ -28,6 +28,10 @@ MUTANTS = {
     "sigmoid-sign": ("exp(-z)", "exp(z)"),
     "maxvio-uses-min": ("(int64_t)E * mx - S", "(int64_t)E * mn - S"),
     "mean-over-P": ("tree_sum(bt, E) / (float)E", "tree_sum(bt, E) / (float)(E + 1)"),
+    "diag-m-floor": ("const int32_t m = (E + 9) / 10;", "const int32_t m = E / 10;"),
+    "diag-gate-new-eprev": ("float de = e - ep_old[i];", "float de = e - e_prev[i];"),
+    "entropy-log2": ("if (x > 0.0) h -= x * log(x);", "if (x > 0.0) h -= x * log2(x);"),
+    "full-entropy-unclamped": ("if (v > 0.0f) C += (double)v;", "C += (double)v;"),
     "qb-alpha-kth": ("for (int32_t r = 0; r <= K; ++r) {", "for (int32_t r = 0; r < K; ++r) {"),
     "qb-quantile-level": ("const int64_t k = (T * (int64_t)(E - K) + E - 1) / E;",
                           "const int64_t k = (T * (int64_t)K + E - 1) / E;"),

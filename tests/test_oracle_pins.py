@@ -505,3 +505,89 @@ def test_qb_ema_blends_previous_bias_and_target():
         want = [Fraction(rho) * Fraction(float(b[j])) + (1 - Fraction(rho)) * Fraction(float(target[j]))
                 for j in range(E)]
         np.testing.assert_array_equal(got, np.array([frac_to_f32(v) for v in want], F32))
+
+
+# ------------------------------------------------------------------ controller diagnostics and entropies
+
+
+def test_controller_diagnostics_worked_example(golden):
+    g = golden("controller_worked_example.txt")
+    E = int(g["E"][0][0])
+    Ki, Kd = float(g["Ki"][0][0]), float(g["Kd"][0][0])
+    st = oracle.ControllerState(E)
+    for row in g["counts"]:
+        t, counts = int(row[0]), np.array([int(v) for v in row[1:]], np.int32)
+        status, diag = oracle.controller_diag(counts, st, Ki, Kd)
+        assert status == oracle.STATUS_OK
+        assert diag.tolist() == [float(v) for v in g["diag"][t][1:]]
+
+
+def test_busiest_share_and_inactive_ratio_by_sorting():
+    rng = np.random.default_rng(3)
+    for E in (768, 64, 100, 7):
+        counts = rng.integers(0, 40, size=E).astype(np.int32)
+        counts[rng.integers(0, E, size=max(1, E // 10))] = 0
+        _, diag = oracle.controller_diag(counts, oracle.ControllerState(E), 6e-3, 6e-3)
+        m = -(-E // 10)
+        top = np.sort(counts)[::-1][:m].sum()
+        assert diag[1] == float(Fraction(int(top), int(counts.sum())))
+        assert diag[2] == float(Fraction(int((counts == 0).sum()), E))
+
+
+def test_busiest_share_closed_forms():
+    E = 768
+    _, diag = oracle.controller_diag(np.full(E, 10, np.int32), oracle.ControllerState(E), 6e-3, 6e-3)
+    assert diag[1] == 77 / 768 and diag[2] == 0.0  # uniform load: m/E
+    one = np.zeros(E, np.int32)
+    one[5] = 1000
+    _, diag = oracle.controller_diag(one, oracle.ControllerState(E), 6e-3, 6e-3)
+    assert diag[1] == 1.0 and diag[2] == (E - 1) / E
+
+
+def test_gate_fraction_closed_after_constant_counts_and_bias_change_matches_numpy():
+    rng = np.random.default_rng(9)
+    E = 256
+    counts = rng.integers(1, 50, size=E).astype(np.int32)
+    st = oracle.ControllerState(E)
+    before = st.bias.copy()
+    _, d0 = oracle.controller_diag(counts, st, 6e-3, 6e-3)
+    assert d0[0] == 0.0  # first step: every gate closed
+    np.testing.assert_allclose(d0[3], np.mean(np.abs(st.bias.astype(np.float64) - before)), rtol=1e-14)
+    _, d1 = oracle.controller_diag(counts, st, 6e-3, 6e-3)
+    assert d1[0] == 0.0  # unchanged counts: every error unchanged, every gate closed
+
+
+def test_diagnostics_nan_when_the_update_does_not_run():
+    st = oracle.ControllerState(8)
+    status, diag = oracle.controller_diag(np.zeros(8, np.int32), st, 6e-3, 6e-3)
+    assert status == oracle.STATUS_EMPTY and np.isnan(diag).all()
+
+
+def test_topk_entropy_closed_forms_and_scipy():
+    from scipy.stats import entropy
+    K = 10
+    assert abs(oracle.topk_entropy(np.full((3, K), 1 / K, F32)) - np.log(K)) < 1e-7
+    onehot = np.zeros((2, K), F32)
+    onehot[:, 3] = 1.0
+    assert oracle.topk_entropy(onehot) == 0.0
+    w = np.random.default_rng(1).random((50, K)).astype(F32)
+    w /= w.sum(1, keepdims=True)
+    # scipy renormalises each row, whose fp32 sum is 1 within a few ulps
+    want = np.mean([entropy(row.astype(np.float64)) for row in w])
+    np.testing.assert_allclose(oracle.topk_entropy(w), want, rtol=1e-6)
+
+
+def test_full_entropy_closed_forms_and_scipy():
+    from scipy.stats import entropy
+    E = 64
+    s = np.full((4, E), 0.5, F32)
+    assert abs(oracle.full_entropy(s, np.zeros(E, F32)) - np.log(E)) < 1e-12
+    # negative biased scores are clamped to zero and drop out
+    b = np.zeros(E, F32)
+    b[32:] = -1.0
+    assert abs(oracle.full_entropy(s, b) - np.log(32)) < 1e-12
+    s = synth.scores(40, E, "beta", seed=2)
+    b = synth.bias(E, "small", seed=3)
+    v = np.maximum((s + b).astype(F32), 0).astype(np.float64)
+    want = np.mean([entropy(row) for row in v])
+    np.testing.assert_allclose(oracle.full_entropy(s, b), want, rtol=1e-9)
