@@ -230,6 +230,48 @@ idb_status idb_router_step(const void* x, const void* W_g, idb_dtype dtype, idb_
                            size_t workspace_bytes, int32_t variant, hipStream_t stream);
 
 /* ---------------------------------------------------------------------------
+ * All MoE layers' controller updates of one iteration in one launch (Alg. 1
+ * runs per layer; one workgroup per layer), with the load statistics and the
+ * update's diagnostics.
+ *   counts    [L][E] int32, the layers' summed loads.
+ *   state     bias and e_prev [L][E] fp32, step [L] int64, status [L] int32.
+ *   out_stats nullable [L][2]: MaxVio, MinVio per layer (as idb_load_stats).
+ *   out_diag  nullable [L][4] fp64 per layer:
+ *     [0] active-gate fraction #{g_i = 1} / E of this update (Eq. rapid-gate;
+ *         Sec. 3 reports its trajectory);
+ *     [1] share of the assignments on the busiest 10% of experts, the
+ *         m = ceil(E / 10) largest counts over S (balanced: m / E);
+ *     [2] inactive-expert ratio #{n_i = 0} / E (Sec. 4.3);
+ *     [3] mean |b_new - b_old| of this update (the bias drift of Sec. 3 is
+ *         the same mean between checkpoints; fp64 over the fixed pairwise
+ *         tree);
+ *     each ratio one fp64 division; NaN x 4 for a layer whose update did not
+ *     run (empty or invalid batch).
+ * Each layer's bias, e_prev, step and status are exactly those of
+ * idb_controller_update on that layer.  1 <= L <= 65535, cfg as for
+ * idb_controller_update.
+ * ------------------------------------------------------------------------- */
+idb_status idb_controller_update_layers(const int32_t* counts, int32_t L, const idb_controller_cfg* cfg,
+                                        const idb_controller_state* state, double* out_stats, double* out_diag,
+                                        hipStream_t stream);
+
+/* ---------------------------------------------------------------------------
+ * Routing entropies (Sec. 4.3), in nats, averaged over the T tokens:
+ *   out[0] = mean H_topK, H_topK = -sum_r w_r log w_r over gate_w [T][K]
+ *            (0 log 0 = 0);
+ *   out[1] = mean H_full, H_full = -sum_e p_e log p_e, p_e = c_e / sum c,
+ *            c_e = max(fl32(s_e + b_e), 0) over scores [T][E] and bias [E]
+ *            (0 when every c_e is 0); NaN when scores is NULL.
+ * Natural logarithms in fp64; deterministic (fixed partial sums in the
+ * workspace, idb_routing_entropy_workspace_bytes() bytes, then added in
+ * order).  out is a device double[2].  1 <= T <= 2^26, 1 <= K <= 32,
+ * E <= 1024.
+ * ------------------------------------------------------------------------- */
+size_t idb_routing_entropy_workspace_bytes(void);
+idb_status idb_routing_entropy(const float* gate_w, int64_t T, int32_t K, const float* scores, const float* bias,
+                               int32_t E, void* workspace, size_t workspace_bytes, double* out, hipStream_t stream);
+
+/* ---------------------------------------------------------------------------
  * Quantile Balancing (Eq. pid-quantile, Eq. pid-quantile-def): the paper's
  * strongest baseline controller, on the same fused router.
  *

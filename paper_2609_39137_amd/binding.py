@@ -34,7 +34,7 @@ EXPORTED = (
     "idb_router_variant_info", "idb_select_from_scores", "idb_controller_update", "idb_load_stats",
     "idb_status_string", "idb_last_error", "idb_router_packed_weight_bytes", "idb_router_pack_weight",
     "idb_controller_step", "idb_router_step", "idb_qb_router_workspace_bytes", "idb_qb_router_forward",
-    "idb_qb_update",
+    "idb_qb_update", "idb_controller_update_layers", "idb_routing_entropy_workspace_bytes", "idb_routing_entropy",
 )
 
 
@@ -98,6 +98,13 @@ def lib() -> ctypes.CDLL:
     L.idb_qb_router_forward.restype = ctypes.c_int
     L.idb_qb_update.argtypes = [P, P, i64, i32, i32, ctypes.c_float, P, P]
     L.idb_qb_update.restype = ctypes.c_int
+    L.idb_controller_update_layers.argtypes = [P, i32, ctypes.POINTER(idb_controller_cfg),
+                                               ctypes.POINTER(idb_controller_state), P, P, P]
+    L.idb_controller_update_layers.restype = ctypes.c_int
+    L.idb_routing_entropy_workspace_bytes.argtypes = []
+    L.idb_routing_entropy_workspace_bytes.restype = sz
+    L.idb_routing_entropy.argtypes = [P, i64, i32, P, P, i32, P, sz, P, P]
+    L.idb_routing_entropy.restype = ctypes.c_int
     L.idb_status_string.argtypes = [ctypes.c_int]
     L.idb_status_string.restype = ctypes.c_char_p
     L.idb_last_error.argtypes = []
@@ -233,13 +240,15 @@ class ControllerCfg:
 
 
 class ControllerState:
-    """Device-resident controller state (bias, e_prev, step, status), zero-initialised."""
+    """Device-resident controller state (bias, e_prev, step, status), zero-initialised; with ``layers``, the
+    state of that many MoE layers ([L][E] and [L])."""
 
-    def __init__(self, E: int, device="cuda"):
-        self.bias = torch.zeros(E, dtype=torch.float32, device=device)
-        self.e_prev = torch.zeros(E, dtype=torch.float32, device=device)
-        self.step = torch.zeros(1, dtype=torch.int64, device=device)
-        self.status = torch.zeros(1, dtype=torch.int32, device=device)
+    def __init__(self, E: int, device="cuda", layers: int | None = None):
+        lead = () if layers is None else (layers,)
+        self.bias = torch.zeros(lead + (E,), dtype=torch.float32, device=device)
+        self.e_prev = torch.zeros(lead + (E,), dtype=torch.float32, device=device)
+        self.step = torch.zeros(layers or 1, dtype=torch.int64, device=device)
+        self.status = torch.zeros(layers or 1, dtype=torch.int32, device=device)
 
     def c(self) -> idb_controller_state:
         return idb_controller_state(_ptr(self.bias), _ptr(self.e_prev), _ptr(self.step), _ptr(self.status))
@@ -326,3 +335,37 @@ def idb_qb_update(scores_t, alpha, K, rho, bias, stream=None):
         raise ValueError("Quantile Balancing operands have the wrong shape or dtype")
     st = lib().idb_qb_update(_ptr(scores_t), _ptr(alpha), T, E, K, float(rho), _ptr(bias), _stream(stream))
     _check("idb_qb_update", st)
+
+
+# ---------------------------------------------------------------------------- layers and diagnostics
+
+
+def idb_controller_update_layers(counts, cfg: ControllerCfg, state: ControllerState, stats=None, diag=None,
+                                 stream=None):
+    """All layers' updates in one launch: ``counts`` [L][E]; optional ``stats`` [L][2] and ``diag`` [L][4]."""
+    L, E = counts.shape
+    if E != cfg.E or state.bias.shape != (L, E) or state.step.shape != (L,):
+        raise ValueError("layer state does not match counts")
+    for t, n in ((stats, 2), (diag, 4)):
+        if t is not None and (t.dtype != torch.float64 or t.shape != (L, n)):
+            raise ValueError("stats must be float64 [L][2] and diag float64 [L][4]")
+    c_cfg, c_state = cfg.c(), state.c()
+    st = lib().idb_controller_update_layers(_ptr(counts), L, ctypes.byref(c_cfg), ctypes.byref(c_state), _ptr(stats),
+                                            _ptr(diag), _stream(stream))
+    _check("idb_controller_update_layers", st)
+
+
+def idb_routing_entropy(gate_w, out, scores=None, bias=None, workspace=None, stream=None):
+    """Mean top-K and full-pool routing entropies (nats) into the device double[2] ``out``."""
+    T, K = gate_w.shape
+    E = 0 if scores is None else scores.shape[1]
+    if out.dtype != torch.float64 or out.numel() != 2:
+        raise ValueError("out must be a float64 tensor of 2 elements")
+    if scores is not None and (scores.shape[0] != T or bias is None or bias.shape != (E,)):
+        raise ValueError("scores must be [T][E] with a bias of E")
+    if workspace is None:
+        workspace = torch.empty(int(lib().idb_routing_entropy_workspace_bytes()), dtype=torch.uint8,
+                                device=gate_w.device)
+    st = lib().idb_routing_entropy(_ptr(gate_w), T, K, _ptr(scores), _ptr(bias), E, _ptr(workspace),
+                                   workspace.numel(), _ptr(out), _stream(stream))
+    _check("idb_routing_entropy", st)

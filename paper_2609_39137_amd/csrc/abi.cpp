@@ -384,6 +384,40 @@ idb_status idb_qb_update(const float* scores_t, const float* alpha, int64_t T, i
     return hip_result(idb::launch_qb_update(scores_t, alpha, T, E, K, rho, bias, stream), "Quantile Balancing launch");
 }
 
+idb_status idb_controller_update_layers(const int32_t* counts, int32_t L, const idb_controller_cfg* cfg,
+                                        const idb_controller_state* state, double* out_stats, double* out_diag,
+                                        hipStream_t stream) {
+    if (!counts) return fail(IDB_ERR_INVALID_ARG, "null pointer");
+    if (L < 1 || L > 65535) return fail(IDB_ERR_INVALID_ARG, "L=%d out of [1, 65535]", L);
+    idb_status st = check_controller(cfg, state, out_stats);
+    if (st != IDB_OK) return st;
+    if (!aligned(counts, 4) || (out_diag && !aligned(out_diag, 8))) return fail(IDB_ERR_INVALID_ARG, "misaligned buffer");
+    return hip_result(idb::launch_controller_layers(counts, L, cfg->E, cfg->Ki, cfg->Kd,
+                                                    cfg->integral_mode == IDB_INTEGRAL_SIGN, cfg->center, state->bias,
+                                                    state->e_prev, state->step, state->status, out_stats, out_diag,
+                                                    stream),
+                      "controller layers launch");
+}
+
+size_t idb_routing_entropy_workspace_bytes(void) { return (size_t)idb::kEntropyBlocks * 2 * sizeof(double); }
+
+idb_status idb_routing_entropy(const float* gate_w, int64_t T, int32_t K, const float* scores, const float* bias,
+                               int32_t E, void* workspace, size_t workspace_bytes, double* out, hipStream_t stream) {
+    if (!gate_w || !out || !workspace) return fail(IDB_ERR_INVALID_ARG, "null pointer");
+    if (T < 1 || T > kMaxTokens) return fail(IDB_ERR_INVALID_ARG, "T=%lld out of [1, 2^26]", (long long)T);
+    if (K < 1 || K > kMaxKGpu) return fail(IDB_ERR_INVALID_ARG, "K=%d out of [1, %d]", K, kMaxKGpu);
+    if (scores && (!bias || E < 1 || E > kMaxExperts))
+        return fail(IDB_ERR_INVALID_ARG, "scores need a bias and 1 <= E <= %d", kMaxExperts);
+    if (workspace_bytes < idb_routing_entropy_workspace_bytes())
+        return fail(IDB_ERR_INVALID_ARG, "workspace of %zu bytes needed", idb_routing_entropy_workspace_bytes());
+    if (!aligned(gate_w, 4) || !aligned(out, 8) || !aligned(workspace, 8) || (scores && !aligned(scores, 4)) ||
+        (bias && !aligned(bias, 4)))
+        return fail(IDB_ERR_INVALID_ARG, "misaligned buffer");
+    return hip_result(idb::launch_routing_entropy(gate_w, T, K, scores, bias, E, static_cast<double*>(workspace), out,
+                                                  stream),
+                      "routing entropy launch");
+}
+
 idb_status idb_load_stats(const int32_t* counts, int32_t E, double* out_maxvio_minvio, hipStream_t stream) {
     if (!counts || !out_maxvio_minvio) return fail(IDB_ERR_INVALID_ARG, "null pointer");
     if (E < 1 || E > (1 << 20)) return fail(IDB_ERR_INVALID_ARG, "E=%d out of [1, 2^20]", E);

@@ -64,6 +64,24 @@ __global__ __launch_bounds__(1024) void load_stats_kernel(const int32_t* __restr
     }
 }
 
+// L layers' updates in one launch, one workgroup per layer (Alg. 1 runs once
+// per MoE layer and iteration): counts, bias and e_prev [L][E], step and
+// status [L], stats [L][2] and diag [L][4] (both nullable).
+__global__ __launch_bounds__(1024) void controller_layers_kernel(const int32_t* __restrict__ counts, int E, int P,
+                                                                 float Ki, float Kd, int sign_mode, int center,
+                                                                 float* __restrict__ bias,
+                                                                 float* __restrict__ e_prev,
+                                                                 int64_t* __restrict__ step,
+                                                                 int32_t* __restrict__ status,
+                                                                 double* __restrict__ stats,
+                                                                 double* __restrict__ diag) {
+    __shared__ CtrlScratch sh;
+    __shared__ DiagScratch dsh;
+    const int64_t l = blockIdx.x;
+    controller_block<1>(counts + l * E, E, P, Ki, Kd, sign_mode, center, bias + l * E, e_prev + l * E, step + l,
+                        status + l, stats ? stats + 2 * l : nullptr, sh, diag ? diag + 4 * l : nullptr, &dsh);
+}
+
 hipError_t launch_controller_update(const int32_t* counts, int E, float Ki, float Kd, int sign_mode, int center,
                                     float* bias, float* e_prev, int64_t* step, int32_t* status, double* stats,
                                     hipStream_t stream) {
@@ -71,6 +89,16 @@ hipError_t launch_controller_update(const int32_t* counts, int E, float Ki, floa
     const int threads = P < 64 ? 64 : P;
     hipLaunchKernelGGL(controller_update_kernel, dim3(1), dim3(threads), 0, stream, counts, E, P, Ki, Kd,
                        sign_mode, center, bias, e_prev, step, status, stats);
+    return hipGetLastError();
+}
+
+hipError_t launch_controller_layers(const int32_t* counts, int L, int E, float Ki, float Kd, int sign_mode,
+                                    int center, float* bias, float* e_prev, int64_t* step, int32_t* status,
+                                    double* stats, double* diag, hipStream_t stream) {
+    const int P = ctrl_tree_size(E);
+    const int threads = P < 64 ? 64 : P;
+    hipLaunchKernelGGL(controller_layers_kernel, dim3((unsigned)L), dim3(threads), 0, stream, counts, E, P, Ki, Kd,
+                       sign_mode, center, bias, e_prev, step, status, stats, diag);
     return hipGetLastError();
 }
 

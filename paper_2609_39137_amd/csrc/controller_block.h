@@ -15,6 +15,25 @@ struct CtrlScratch {
     float tree[1024];
 };
 
+// LDS scratch of the diagnostics (controller_block with a diag pointer).
+struct DiagScratch {
+    int cnt[1024];
+    double tree[1024];
+};
+
+// Sum of one value per thread over the workgroup (exact for integers).
+__device__ inline long long block_sum(long long v, CtrlScratch& sh) {
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6, nw = blockDim.x >> 6;
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
+    __syncthreads();  // w_sum is free
+    if (lane == 0) sh.w_sum[wv] = v;
+    __syncthreads();
+    long long t = 0;
+    for (int w = 0; w < nw; ++w) t += sh.w_sum[w];
+    return t;
+}
+
 // Leaves of the centering tree: the next power of two >= E.
 __host__ __device__ inline int ctrl_tree_size(int E) {
     int P = 1;
@@ -25,7 +44,13 @@ __host__ __device__ inline int ctrl_tree_size(int E) {
 // The whole O(E) update on one workgroup whose size is a multiple of 64, each
 // thread taking experts i, i + blockDim, ... (kPer of them): needs
 // kPer * blockDim >= P, the centering tree's size below, and E <= 1024.  With a
-// non-null stats pointer it also writes MaxVio/MinVio of the same counts.
+// non-null stats pointer it also writes MaxVio/MinVio of the same counts;
+// with a non-null diag pointer (and dsh), the update's diagnostics: diag[0]
+// the active-gate fraction #{g_i = 1}/E, diag[1] the share of the assignments
+// on the m = ceil(E/10) busiest experts (an expert's rank: the experts with a
+// larger count or an equal count and a lower index before it), diag[2] the
+// inactive-expert ratio #{n_i = 0}/E, diag[3] the mean |b_new - b_old| summed
+// in fp64 over the same pairwise tree; NaN x 4 when the update does not run.
 // Reductions: exact integer sums/extrema across waves (order-free); the
 // centering mean with the fixed pairwise tree (level h adds a_{j+h} into a_j
 // for j < h, P = next power of two >= E), levels h >= 64 in LDS, the last
@@ -35,7 +60,8 @@ __device__ inline void controller_block(const int32_t* __restrict__ counts, int 
                                         int sign_mode, int center, float* __restrict__ bias,
                                         float* __restrict__ e_prev, int64_t* __restrict__ step,
                                         int32_t* __restrict__ status, double* __restrict__ stats,
-                                        CtrlScratch& sh) {
+                                        CtrlScratch& sh, double* __restrict__ diag = nullptr,
+                                        DiagScratch* dsh = nullptr) {
 #pragma clang fp contract(off)
     const int i0 = threadIdx.x, nt = blockDim.x;
     const int lane = i0 & 63, wv = i0 >> 6, nw = nt >> 6;
@@ -98,10 +124,15 @@ __device__ inline void controller_block(const int32_t* __restrict__ counts, int 
     }
     if (any_negative || S == 0) {
         // Invalid or empty batch: report it and leave the state untouched.
-        if (i0 == 0) *status = any_negative ? kStatusInvalid : kStatusEmpty;
+        if (i0 == 0) {
+            *status = any_negative ? kStatusInvalid : kStatusEmpty;
+            if (diag)
+                for (int q = 0; q < 4; ++q) diag[q] = __builtin_nan("");
+        }
         return;
     }
     float e[kPer], b[kPer];
+    int gates = 0;
 #pragma unroll
     for (int q = 0; q < kPer; ++q) {
         const int i = i0 + q * nt;
@@ -129,6 +160,7 @@ __device__ inline void controller_block(const int32_t* __restrict__ counts, int 
                 const float dterm = Kd * de;  // gated, accumulated derivative
                 b[q] = b[q] + dterm;
             }
+            gates += g ? 1 : 0;
         }
     }
     // Zero-mean centering (second line of Eq. rapid-update).
@@ -167,6 +199,56 @@ __device__ inline void controller_block(const int32_t* __restrict__ counts, int 
     if (i0 == 0) {
         *step = *step + 1;
         *status = kStatusOk;
+    }
+    if (!diag) return;
+    // diagnostics of this update
+    int zeros = 0;
+#pragma unroll
+    for (int q = 0; q < kPer; ++q) {
+        const int i = i0 + q * nt;
+        if (i < E) {
+            dsh->cnt[i] = n[q];
+            zeros += n[q] == 0 ? 1 : 0;
+        }
+        if (i < P) {
+            const float nb = (i < E) ? (center ? (b[q] - m) : b[q]) : 0.0f;
+            dsh->tree[i] = (i < E) ? (double)fabsf(nb - b0[q]) : 0.0;
+        }
+    }
+    const long long G = block_sum(gates, sh);  // its barriers also publish cnt[] and tree[]
+    const long long Z = block_sum(zeros, sh);
+    const int mtop = (E + 9) / 10;
+    long long top = 0;
+#pragma unroll
+    for (int q = 0; q < kPer; ++q) {
+        const int i = i0 + q * nt;
+        if (i < E) {
+            int rank = 0;
+            for (int jj = 0; jj < E; ++jj) {
+                const int c = dsh->cnt[jj];
+                rank += (c > n[q] || (c == n[q] && jj < i)) ? 1 : 0;
+            }
+            top += rank < mtop ? n[q] : 0;
+        }
+    }
+    const long long TOP = block_sum(top, sh);
+    int h = P >> 1;
+    for (; h >= 64; h >>= 1) {
+        for (int i = i0; i < h; i += nt) dsh->tree[i] = dsh->tree[i] + dsh->tree[i + h];
+        __syncthreads();
+    }
+    if (wv == 0) {
+        double a = (lane < P) ? dsh->tree[lane] : 0.0;
+        for (; h >= 1; h >>= 1) {
+            const double up = __shfl_down(a, h);
+            if (lane < h) a = a + up;
+        }
+        if (lane == 0) {
+            diag[0] = (double)G / (double)E;
+            diag[1] = (double)TOP / (double)S;
+            diag[2] = (double)Z / (double)E;
+            diag[3] = a / (double)E;
+        }
     }
 }
 

@@ -13,6 +13,14 @@ hipError_t launch_controller_update(const int32_t* counts, int E, float Ki, floa
                                     float* bias, float* e_prev, int64_t* step, int32_t* status, double* stats,
                                     hipStream_t stream);
 hipError_t launch_load_stats(const int32_t* counts, int E, double* out, hipStream_t stream);
+// L layers' controller updates in one launch; stats [L][2], diag [L][4] nullable.
+hipError_t launch_controller_layers(const int32_t* counts, int L, int E, float Ki, float Kd, int sign_mode,
+                                    int center, float* bias, float* e_prev, int64_t* step, int32_t* status,
+                                    double* stats, double* diag, hipStream_t stream);
+// Routing entropies: partial sums into workspace [kEntropyBlocks][2], then the means into out[2].
+constexpr int kEntropyBlocks = 512;
+hipError_t launch_routing_entropy(const float* gate_w, int64_t T, int K, const float* scores, const float* bias,
+                                  int E, double* partial, double* out, hipStream_t stream);
 
 hipError_t launch_fill_i32(int32_t* p, int32_t value, int64_t n, hipStream_t stream);
 // Quantile Balancing's bias update from expert-major scores and cutoffs.

@@ -260,3 +260,25 @@ def test_qb_workspace_holds_k_plus_one_candidates():
         B.idb_router_workspace_bytes(16384, 2048, 768, 11, B.IDB_DTYPE_BF16, 0)
     assert B.idb_qb_router_workspace_bytes(16384, 2048, 768, 32, B.IDB_DTYPE_BF16, 0) == 0
     assert B.idb_qb_router_workspace_bytes(16384, 2048, 768, 10, B.IDB_DTYPE_BF16, 7) == 0  # one slice
+
+
+def test_layers_and_entropy_reject_invalid_arguments():
+    L = B.lib()
+    ccfg = B.idb_controller_cfg(768, 6e-3, 6e-3, 0, 1)
+    st = _state()
+    assert L.idb_controller_update_layers(None, 4, ctypes.byref(ccfg), ctypes.byref(st), None, None, None) == \
+        B.IDB_ERR_INVALID_ARG
+    assert L.idb_controller_update_layers(A16, 0, ctypes.byref(ccfg), ctypes.byref(st), None, None, None) == \
+        B.IDB_ERR_INVALID_ARG
+    bad = B.idb_controller_cfg(768, -1.0, 6e-3, 0, 1)
+    assert L.idb_controller_update_layers(A16, 4, ctypes.byref(bad), ctypes.byref(st), None, None, None) == \
+        B.IDB_ERR_INVALID_ARG
+    assert L.idb_controller_update_layers(A16, 4, ctypes.byref(ccfg), ctypes.byref(st), None, A16 + 4, None) == \
+        B.IDB_ERR_INVALID_ARG
+    ws = int(L.idb_routing_entropy_workspace_bytes())
+    assert ws == 512 * 2 * 8
+    assert L.idb_routing_entropy(A16, 0, 10, None, None, 0, A16, ws, A16, None) == B.IDB_ERR_INVALID_ARG
+    assert L.idb_routing_entropy(A16, 100, 0, None, None, 0, A16, ws, A16, None) == B.IDB_ERR_INVALID_ARG
+    assert L.idb_routing_entropy(A16, 100, 10, None, None, 0, A16, ws - 8, A16, None) == B.IDB_ERR_INVALID_ARG
+    assert L.idb_routing_entropy(A16, 100, 10, A16, None, 768, A16, ws, A16, None) == B.IDB_ERR_INVALID_ARG
+    assert L.idb_routing_entropy(None, 100, 10, None, None, 0, A16, ws, A16, None) == B.IDB_ERR_INVALID_ARG
