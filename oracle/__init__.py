@@ -21,6 +21,8 @@ readings of points the paper leaves open):
 * :func:`topk_entropy`, :func:`full_entropy` -- routing entropies (Sec. 4.3)
 * :func:`qb_alpha`, :func:`qb_update` -- Quantile Balancing's cutoffs and
   target bias, with the EMA variant (Eq. pid-quantile, Eq. pid-quantile-def)
+* :func:`aux_stats`, :func:`aux_router` -- the auxiliary-loss router's
+  forward statistics f_i, P_i and the loss (Eq. pid-auxloss)
 """
 from __future__ import annotations
 
@@ -90,6 +92,7 @@ def _declare(lib):
     lib.oracle_full_entropy.restype = ctypes.c_double
     lib.oracle_qb_alpha.argtypes = [P, P, i64, i32, i32, P]
     lib.oracle_qb_update.argtypes = [P, P, i64, i32, i32, f32, P]
+    lib.oracle_aux_stats.argtypes = [P, i64, i32, i32, ctypes.c_double, P, P, P, P, P, P]
     return lib
 
 
@@ -271,3 +274,32 @@ def full_entropy(scores: np.ndarray, bias: np.ndarray) -> float:
     s = np.ascontiguousarray(scores, dtype=np.float32)
     b = np.ascontiguousarray(bias, dtype=np.float32)
     return float(_load().oracle_full_entropy(_ptr(s), _ptr(b), s.shape[0], s.shape[1]))
+
+
+def aux_stats(z: np.ndarray, K: int, alpha: float):
+    """Auxiliary-loss forward statistics (Eq. pid-auxloss) from logits z [T][E].
+
+    p = softmax(z) per token (fp64); Top-K ranked on the fp32-rounded logits,
+    lowest index among equals; gate weights = selected p renormalised.
+    Returns ``(idx [T][K] int32, w [T][K] float32, counts [E] int32,
+    f [E] float64, P [E] float64, loss float)``.
+    """
+    lib = _load()
+    zz = np.ascontiguousarray(z, dtype=np.float64)
+    T, E = zz.shape
+    assert 1 <= K <= E and T >= 1
+    idx = np.empty((T, K), np.int32)
+    w = np.empty((T, K), np.float32)
+    c = np.empty(E, np.int32)
+    f = np.empty(E, np.float64)
+    P = np.empty(E, np.float64)
+    loss = np.zeros(1, np.float64)
+    lib.oracle_aux_stats(_ptr(zz), T, E, K, float(alpha), _ptr(idx), _ptr(w), _ptr(c), _ptr(f), _ptr(P),
+                         _ptr(loss))
+    return idx, w, c, f, P, float(loss[0])
+
+
+def aux_router(x: np.ndarray, W: np.ndarray, K: int, alpha: float, rows: np.ndarray | None = None):
+    """Logits from hidden states (R1), then :func:`aux_stats` of those rows."""
+    _, z = router_scores(x, W, rows=rows, want_z=True)
+    return aux_stats(z, K, alpha)

@@ -30,6 +30,9 @@
  *   Q1..Q4 Quantile Balancing's target bias, with the EMA   (Eq. pid-quantile,
  *          variant used as a diagnostic                      Eq. pid-quantile-def; Sec. 3,
  *                                                            EMA smoothing of the target)
+ *   X1..X5 auxiliary-loss balancing, forward statistics:   (Eq. pid-auxloss)
+ *          softmax router probabilities, Top-K, assigned
+ *          fractions f_i, mean probabilities P_i, the loss
  *
  * Readings of points the paper leaves open (each is listed in the design
  * notes of the repository):
@@ -66,6 +69,13 @@
  *     k = ceil(m (E - K) / E) computed in exact integers; the target is its
  *     negation.  The EMA variant is fl32(fl32(rho b) + fl32(fl32(1 - rho) Q)),
  *     and rho == 0 is the plain target b = Q.
+ *   - Auxiliary-loss routers keep no bias: p = softmax(z) over all E experts
+ *     in fp64 (max subtracted first); T(x) = the K largest p, ranked on the
+ *     logits rounded to fp32 (softmax preserves their order; fp32 is the
+ *     precision the GPU decides in) with ties to the lowest index; gate
+ *     weights w_r = p_r / sum of the selected p in rank order, in fp64, then
+ *     fp32; f_i = n_i / T; P_i = (1/T) sum over tokens of p_i, tokens in
+ *     order; the loss alpha * sum_i f_i P_i, experts in order.
  *
  * Build: gcc -O2 -ffp-contract=off -fopenmp -shared -fPIC (never -ffast-math:
  * the fp32 steps must round exactly as written).
@@ -473,6 +483,70 @@ void oracle_qb_update(const float* s, const float* alpha, int64_t T, int32_t E, 
 
 /* Wall-clock seconds of one whole oracle step (R1-R6, C1-C7, S1) on the host,
  * for the CPU baseline.  Uses the OpenMP thread count in effect. */
+/* X1-X5 from logits z [T][E] (fp64): the auxiliary-loss router's forward
+ * statistics (Eq. pid-auxloss).  idx, w [T][K] in rank order; counts [E];
+ * f, P [E]; *loss = alpha sum_i f_i P_i. */
+void oracle_aux_stats(const double* z, int64_t T, int32_t E, int32_t K, double alpha, int32_t* idx, float* w,
+                      int32_t* counts, double* f, double* P, double* loss) {
+    double* p = (double*)malloc((size_t)T * E * sizeof(double));
+#pragma omp parallel
+    {
+        unsigned char* taken = (unsigned char*)malloc((size_t)E);
+#pragma omp for schedule(static)
+        for (int64_t t = 0; t < T; ++t) {
+            const double* zt = z + t * (int64_t)E;
+            double* pt = p + t * (int64_t)E;
+            /* X1: softmax, the largest logit subtracted so exp cannot overflow */
+            double m = zt[0];
+            for (int32_t i = 1; i < E; ++i)
+                if (zt[i] > m) m = zt[i];
+            double Z = 0.0;
+            for (int32_t i = 0; i < E; ++i) {
+                pt[i] = exp(zt[i] - m);
+                Z = Z + pt[i];
+            }
+            for (int32_t i = 0; i < E; ++i) pt[i] = pt[i] / Z;
+            /* X2: Top-K on the fp32 logits, lowest index first among equals */
+            memset(taken, 0, (size_t)E);
+            int32_t* it = idx + t * (int64_t)K;
+            for (int32_t r = 0; r < K; ++r) {
+                int32_t best = -1;
+                float best_v = 0.0f;
+                for (int32_t i = 0; i < E; ++i) {
+                    if (taken[i]) continue;
+                    const float v = (float)zt[i];
+                    if (best < 0 || ranks_above(v, i, best_v, best)) {
+                        best = i;
+                        best_v = v;
+                    }
+                }
+                taken[best] = 1;
+                it[r] = best;
+            }
+            /* X3: gate weights, the selected probabilities renormalised */
+            double den = 0.0;
+            for (int32_t r = 0; r < K; ++r) den = den + pt[it[r]];
+            for (int32_t r = 0; r < K; ++r) w[t * (int64_t)K + r] = (float)(pt[it[r]] / den);
+        }
+        free(taken);
+    }
+    /* X4: assignment counts and fractions */
+    for (int32_t i = 0; i < E; ++i) counts[i] = 0;
+    for (int64_t t = 0; t < T; ++t)
+        for (int32_t r = 0; r < K; ++r) counts[idx[t * (int64_t)K + r]] += 1;
+    /* X5: mean probabilities and the loss */
+    for (int32_t i = 0; i < E; ++i) {
+        double acc = 0.0;
+        for (int64_t t = 0; t < T; ++t) acc = acc + p[t * (int64_t)E + i];
+        P[i] = acc / (double)T;
+        f[i] = (double)counts[i] / (double)T;
+    }
+    double L = 0.0;
+    for (int32_t i = 0; i < E; ++i) L = L + f[i] * P[i];
+    *loss = alpha * L;
+    free(p);
+}
+
 double oracle_step_seconds(const void* x, const void* W, int dtype, int64_t T, int32_t d, int32_t E, int32_t K,
                            float Ki, float Kd, float* bias, float* e_prev, int64_t* step, int32_t* status,
                            int32_t* idx, float* w, int32_t* counts, double* stats) {

@@ -41,6 +41,12 @@ MUTANTS = {
     "qb-ema-weights": ("const float take = (1.0f - rho) * Q;", "const float take = rho * Q;"),
     "qb-biased-margin": ("d[t] = (s[t * (int64_t)E + j] - alpha[t]) + 0.0f;",
                          "d[t] = (s[t * (int64_t)E + j] + bias[j] - alpha[t]) + 0.0f;"),
+    "aux-no-max-shift": ("pt[i] = exp(zt[i] - m);", "pt[i] = exp(zt[i]);"),
+    "aux-unnormalised-p": ("for (int32_t i = 0; i < E; ++i) pt[i] = pt[i] / Z;", "(void)Z;"),
+    "aux-raw-gate-weights": ("(float)(pt[it[r]] / den)", "(float)pt[it[r]]"),
+    "aux-f-over-tk": ("f[i] = (double)counts[i] / (double)T;", "f[i] = (double)counts[i] / (double)(T * K);"),
+    "aux-loss-misaligned": ("L = L + f[i] * P[i];", "L = L + f[i] * P[E - 1 - i];"),
+    "aux-rank-ascending": ("const float v = (float)zt[i];", "const float v = -(float)zt[i];"),
 }
 
 

@@ -591,3 +591,95 @@ def test_full_entropy_closed_forms_and_scipy():
     v = np.maximum((s + b).astype(F32), 0).astype(np.float64)
     want = np.mean([entropy(row) for row in v])
     np.testing.assert_allclose(oracle.full_entropy(s, b), want, rtol=1e-9)
+
+
+# ------------------------------------------------- auxiliary-loss statistics
+
+
+def _softmax_ref(z):
+    from scipy.special import softmax
+
+    return softmax(np.asarray(z, np.float64), axis=1)
+
+
+def test_aux_worked_example(golden):
+    g = golden("aux_worked_example.txt")
+    K = int(g["K"][0][0])
+    alpha = float(g["alpha"][0][0])
+    z = np.array([[float(v) for v in g[f"z{t}"][0]] for t in range(3)])
+    idx, w, c, f, P, loss = oracle.aux_stats(z, K, alpha)
+    np.testing.assert_array_equal(idx, np.array([[int(v) for v in g[f"idx{t}"][0]] for t in range(3)]))
+    np.testing.assert_allclose(w, np.array([[float(v) for v in g[f"w{t}"][0]] for t in range(3)]), rtol=1e-7)
+    np.testing.assert_array_equal(c, np.array([int(v) for v in g["counts"][0]]))
+    np.testing.assert_allclose(f, [float(v) for v in g["f"][0]], rtol=1e-15)
+    np.testing.assert_allclose(P, [float(v) for v in g["P"][0]], rtol=1e-14)
+    assert loss == pytest.approx(float(g["loss"][0][0]), rel=1e-14)
+
+
+def test_aux_equal_logits_closed_form():
+    # all logits equal: p = 1/E, the K lowest indices win every token,
+    # f = 1 on them, P = 1/E, loss = alpha K / E
+    T, E, K, alpha = 50, 32, 4, 0.05
+    z = np.full((T, E), 0.75)
+    idx, w, c, f, P, loss = oracle.aux_stats(z, K, alpha)
+    np.testing.assert_array_equal(idx, np.tile(np.arange(K, dtype=np.int32), (T, 1)))
+    np.testing.assert_array_equal(w, np.full((T, K), F32(1.0 / K)))
+    np.testing.assert_array_equal(c, np.where(np.arange(E) < K, T, 0))
+    np.testing.assert_array_equal(f, np.where(np.arange(E) < K, 1.0, 0.0))
+    np.testing.assert_allclose(P, np.full(E, 1.0 / E), rtol=1e-15)
+    assert loss == pytest.approx(alpha * K / E, rel=1e-14)
+
+
+@pytest.mark.parametrize("T,E,K", [(200, 64, 6), (97, 48, 1), (64, 32, 32)])
+def test_aux_matches_scipy_softmax(T, E, K):
+    r = synth.rng(T, E, K)
+    z = r.normal(0.0, 2.0, (T, E))
+    alpha = 0.1
+    idx, w, c, f, P, loss = oracle.aux_stats(z, K, alpha)
+    p = _softmax_ref(z)
+    np.testing.assert_allclose(P, p.mean(axis=0), rtol=1e-12)
+    np.testing.assert_array_equal(f, np.bincount(idx.ravel(), minlength=E) / T)
+    np.testing.assert_array_equal(c, np.bincount(idx.ravel(), minlength=E))
+    psel = np.take_along_axis(p, idx.astype(np.int64), 1)
+    np.testing.assert_allclose(w, psel / psel.sum(axis=1, keepdims=True), rtol=1e-6)
+    assert loss == pytest.approx(alpha * float(np.dot(f, p.mean(axis=0))), rel=1e-12)
+
+
+def test_aux_selection_is_a_stable_sort_of_the_fp32_logits():
+    # quarter-integer logits tie often; the order is v descending, index ascending
+    T, E, K = 300, 40, 7
+    r = synth.rng(7, 40)
+    z = r.integers(-6, 7, (T, E)) / 4.0
+    idx, *_ = oracle.aux_stats(z, K, 0.0)
+    v = z.astype(F32)
+    order = np.argsort(-v, axis=1, kind="stable")[:, :K]
+    np.testing.assert_array_equal(idx, order)
+
+
+def test_aux_invariants_and_shift_invariance():
+    # sum f = K, sum P = 1; adding a per-token constant to the logits changes
+    # nothing (integer logits and shifts keep every value exact)
+    T, E, K = 128, 64, 5
+    r = synth.rng(128, 64)
+    z = r.integers(-8, 9, (T, E)).astype(np.float64)
+    idx, w, c, f, P, loss = oracle.aux_stats(z, K, 0.3)
+    assert f.sum() == pytest.approx(K, rel=1e-15)
+    assert P.sum() == pytest.approx(1.0, rel=1e-13)
+    assert c.sum() == T * K
+    shift = r.integers(-40, 41, (T, 1)).astype(np.float64)
+    idx2, w2, c2, f2, P2, loss2 = oracle.aux_stats(z + shift, K, 0.3)
+    np.testing.assert_array_equal(idx2, idx)
+    np.testing.assert_array_equal(c2, c)
+    np.testing.assert_allclose(w2, w, rtol=1e-7)
+    np.testing.assert_allclose(P2, P, rtol=1e-13)
+    assert loss2 == pytest.approx(loss, rel=1e-13)
+
+
+def test_aux_large_logits_do_not_overflow():
+    # softmax is shift-invariant, so logits near 1000 give the same p as near 0
+    # (the gap ln 3 is held to the fp64 spacing at 1000, about 1e-13)
+    z = np.array([[1000.0, 1000.0 + np.log(3.0)], [-1000.0, -1000.0 + np.log(3.0)]])
+    idx, w, c, f, P, loss = oracle.aux_stats(z, 1, 1.0)
+    np.testing.assert_array_equal(idx, [[1], [1]])
+    np.testing.assert_allclose(P, [0.25, 0.75], rtol=1e-12)
+    assert loss == pytest.approx(0.75, rel=1e-12)
