@@ -104,8 +104,11 @@ def main() -> int:
                     help="eager copy calibration + a few router launches, for rocprofv3 counter passes")
     ap.add_argument("--copy-mib", type=int, default=512, help="size of the calibration copy of --pmc-pass")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--controller", choices=("id", "qb"), default="id",
-                    help="id: ID Balancing (the headline step); qb: Quantile Balancing, the paper's baseline")
+    ap.add_argument("--controller", choices=("id", "qb", "aux"), default="id",
+                    help="id: ID Balancing (the headline step); qb: Quantile Balancing, the paper's baseline; "
+                         "aux: auxiliary-loss balancing's forward statistics (softmax router, no bias)")
+    ap.add_argument("--aux-alpha", type=float, default=0.05, help="auxiliary-loss coefficient")
+    ap.add_argument("--aux-variant", type=int, default=0, help="one-slice router tiling of --controller aux")
     ap.add_argument("--rho", type=float, default=0.0, help="Quantile Balancing EMA weight (0: the plain target)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="wall-clock target of the CPU oracle sample")
     args = ap.parse_args()
@@ -150,11 +153,16 @@ def main() -> int:
     torch.cuda.synchronize()
 
     qb = args.controller == "qb"
+    aux = args.controller == "aux"
+    if aux:
+        rs.aux_buffers(args.aux_variant)
 
     def one_step(i):
         rs.pack(W, stream=stream)
         if qb:
             rs.qb_step(xs[i % nbuf], None, rho=args.rho, stream=stream)
+        elif aux:
+            rs.aux_step(xs[i % nbuf], None, alpha=args.aux_alpha, stream=stream)
         else:
             rs.step(xs[i % nbuf], None, stream=stream)
 
@@ -227,6 +235,8 @@ def main() -> int:
     stats = rs.stats.cpu().tolist()
     if qb:
         return qb_report(args, wl, rs, xs, nbuf, stream, capture, ms_step, stats)
+    if aux:
+        return aux_report(args, wl, rs, xs, nbuf, stream, capture, ms_step, stats)
 
     # live timing of the dominant kernel: back-to-back launches of the fused
     # router kernel alone, on the stream the steps run on, between HIP events
@@ -330,6 +340,73 @@ def main() -> int:
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on a bounded sample")
         out["cpu_baseline"] = cpu_baseline(wl, W_np, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+def graph_time_per_call(fn, per, reps, stream, capture):
+    """Average duration of fn on the stream: graph replays of per calls, reps times, between HIP events."""
+    import torch
+
+    g = capture(fn, per)
+    with torch.cuda.stream(stream):
+        g.replay()
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    with torch.cuda.stream(stream):
+        for _ in range(reps):
+            g.replay()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / (reps * per)
+
+
+def aux_report(args, wl, rs, xs, nbuf, stream, capture, ms_step, stats) -> int:
+    """JSON line of the auxiliary-loss statistics step (softmax router + f, P, loss; MaxVio/MinVio)."""
+    from paper_2609_39137_amd import binding as B
+
+    per = nbuf * max(1, 16 // nbuf)
+    reps = max(1, -(-max(args.steps, 64) // per))
+
+    def aux_call(i):
+        B.idb_aux_router_forward(xs[i % nbuf], rs.W_packed, wl.K, args.aux_alpha, rs.idx, rs.w, rs.counts, rs.aux_f,
+                                 rs.aux_P, rs.aux_loss, rs.aux_workspace, None, rs.aux_variant, stream,
+                                 B.IDB_WEIGHT_PACKED, stats=rs.stats)
+
+    route_ms = graph_time_per_call(aux_call, per, reps, stream, capture)
+    info = B.idb_router_variant_info(wl.T, wl.d, wl.E, wl.K, rs.dtype_code, rs.aux_variant) if rs.aux_variant \
+        else None
+    log(f"softmax router + auxiliary-loss statistics: {route_ms * 1000:.2f} us per call")
+    achieved = wl.flops / (route_ms * 1e-3) / 1e12
+    peak = PEAK_BF16_TFLOPS if wl.dtype == "bf16" else PEAK_F32_TFLOPS
+    loss = float(rs.aux_loss.item())
+    out = {
+        "metric": "routed tokens/sec for the auxiliary-loss router step (softmax Top-K, f_i, P_i, loss; the paper's "
+                  "baseline, forward statistics)",
+        "value": round(wl.T / (ms_step * 1e-3), 1),
+        "unit": "routed tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": wl.dtype,
+        "data": "synthetic",
+        "config": {"workload": wl.name, "T": wl.T, "d": wl.d, "E": wl.E, "K": wl.K, "global_batch": wl.T,
+                   "parallelism": "single GPU", "variant": info["variant"] if info else "auto (one slice)",
+                   "controller": "auxiliary-loss statistics", "alpha": args.aux_alpha,
+                   "launch": f"hip-graph of {nbuf} steps", "input_buffers": nbuf},
+        "roofline": {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
+                     "frac": round(achieved / peak, 4), "traffic": None,
+                     "kernel": "fused router kernel in softmax mode (one slice of all experts, per-tile softmax "
+                               "column sums) + the statistics kernel",
+                     "kernel_us": round(route_ms * 1000, 2), "flops_per_launch": wl.flops},
+        "last_step": {"maxvio": stats[0], "minvio": stats[1], "aux_loss": loss},
+    }
     print(json.dumps(out), flush=True)
     return 0
 

@@ -302,6 +302,43 @@ idb_status idb_qb_router_forward(const void* x, const void* W_g, idb_dtype dtype
 idb_status idb_qb_update(const float* scores_t, const float* alpha, int64_t T, int32_t E, int32_t K, float rho,
                          float* bias, hipStream_t stream);
 
+/* ---------------------------------------------------------------------------
+ * Auxiliary-loss balancing's forward statistics (Eq. pid-auxloss), on the
+ * fused router.  The router keeps no bias: with logits z = W_g x (as
+ * idb_router_forward) and p = softmax(z) over all E experts,
+ *   expert_idx [T][K] int32 out: the K largest z per token in rank order
+ *              (softmax preserves the order; equal logits: lowest index
+ *              first), decided on the fp32 logits;
+ *   gate_w     [T][K] fp32 out: the selected p renormalised,
+ *              exp(z_r - z_top) / (fp32 sum of those in rank order);
+ *   counts     [E] int32 out: assignments per expert;
+ *   f          [E] fp64 out: f_i = n_i / T;
+ *   P          [E] fp64 out: P_i = (1/T) sum over the tokens of p_i, from
+ *              per-tile fp32 column sums (M = the token's largest logit,
+ *              p = exp(z - M) / sum exp(z - M)) added in fp64 in a fixed
+ *              order, so repeated calls give identical bits;
+ *   loss       fp64 out (device scalar): alpha * sum_i f_i P_i.
+ *   out_maxvio_minvio nullable fp64 [2] out: MaxVio, MinVio of the counts
+ *              (as idb_load_stats).
+ *   logits_dump nullable [T][E] fp32 out: the logits the selection ranked.
+ * counts, f, P and the loss are written by the second launch from per-tile
+ * rows (no atomics: identical bits on every call).
+ * Only tilings whose workgroups cover all E experts run this (the statistics
+ * need each token's whole softmax in one workgroup): E <= 768 for bf16, E <=
+ * 128 for fp32; other shapes or variants return IDB_ERR_UNSUPPORTED.  Other
+ * limits as for idb_router_forward; alpha finite.  The workspace (at least
+ * idb_aux_router_workspace_bytes(), 16-byte aligned) holds the per-tile rows
+ * and a ticket; it must not be shared with a call still running on another
+ * stream.  Two launches: the fused router kernel, then the statistics kernel.
+ * ------------------------------------------------------------------------- */
+size_t idb_aux_router_workspace_bytes(int64_t T, int32_t d, int32_t E, int32_t K, idb_dtype dtype,
+                                      int32_t variant);
+idb_status idb_aux_router_forward(const void* x, const void* W_g, idb_dtype dtype, idb_weight_layout weight_layout,
+                                  int64_t T, int32_t d, int32_t E, int32_t K, double alpha, int32_t* expert_idx,
+                                  float* gate_w, int32_t* counts, double* f, double* P, double* loss,
+                                  double* out_maxvio_minvio, float* logits_dump, void* workspace,
+                                  size_t workspace_bytes, int32_t variant, hipStream_t stream);
+
 /* Static description of a status code; message of the last failing call on
  * this thread (empty string if none). */
 const char* idb_status_string(idb_status s);

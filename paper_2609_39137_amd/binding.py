@@ -35,6 +35,7 @@ EXPORTED = (
     "idb_status_string", "idb_last_error", "idb_router_packed_weight_bytes", "idb_router_pack_weight",
     "idb_controller_step", "idb_router_step", "idb_qb_router_workspace_bytes", "idb_qb_router_forward",
     "idb_qb_update", "idb_controller_update_layers", "idb_routing_entropy_workspace_bytes", "idb_routing_entropy",
+    "idb_aux_router_workspace_bytes", "idb_aux_router_forward",
 )
 
 
@@ -105,6 +106,11 @@ def lib() -> ctypes.CDLL:
     L.idb_routing_entropy_workspace_bytes.restype = sz
     L.idb_routing_entropy.argtypes = [P, i64, i32, P, P, i32, P, sz, P, P]
     L.idb_routing_entropy.restype = ctypes.c_int
+    L.idb_aux_router_workspace_bytes.argtypes = [i64, i32, i32, i32, i32, i32]
+    L.idb_aux_router_workspace_bytes.restype = sz
+    L.idb_aux_router_forward.argtypes = [P, P, i32, i32, i64, i32, i32, i32, ctypes.c_double, P, P, P, P, P, P, P,
+                                         P, P, sz, i32, P]
+    L.idb_aux_router_forward.restype = ctypes.c_int
     L.idb_status_string.argtypes = [ctypes.c_int]
     L.idb_status_string.restype = ctypes.c_char_p
     L.idb_last_error.argtypes = []
@@ -335,6 +341,38 @@ def idb_qb_update(scores_t, alpha, K, rho, bias, stream=None):
         raise ValueError("Quantile Balancing operands have the wrong shape or dtype")
     st = lib().idb_qb_update(_ptr(scores_t), _ptr(alpha), T, E, K, float(rho), _ptr(bias), _stream(stream))
     _check("idb_qb_update", st)
+
+
+# ---------------------------------------------------------------------------- auxiliary-loss statistics
+
+
+def idb_aux_router_workspace_bytes(T, d, E, K, dtype=IDB_DTYPE_BF16, variant=0) -> int:
+    return int(lib().idb_aux_router_workspace_bytes(T, d, E, K, dtype, variant))
+
+
+def idb_aux_router_forward(x, W_g, K, alpha, expert_idx, gate_w, counts, f, P, loss, workspace, logits_dump=None,
+                           variant=0, stream=None, weight_layout=IDB_WEIGHT_ROW_MAJOR, stats=None):
+    """Softmax router without bias and its auxiliary-loss statistics f, P and the loss (Eq. pid-auxloss);
+    ``stats`` (float64 [2], optional) receives MaxVio/MinVio."""
+    T, d = x.shape
+    E = W_g.shape[0]
+    if W_g.shape[1] != d or W_g.dtype != x.dtype:
+        raise ValueError("router operands disagree in shape or dtype")
+    if expert_idx.shape != (T, K) or gate_w.shape != (T, K) or counts.shape != (E,):
+        raise ValueError("router outputs have the wrong shape")
+    for name, t, shape in (("f", f, (E,)), ("P", P, (E,)), ("loss", loss, (1,))):
+        if t.shape != shape or t.dtype != torch.float64:
+            raise ValueError(f"{name} must be float64 of shape {shape}")
+    if logits_dump is not None and (logits_dump.shape != (T, E) or logits_dump.dtype != torch.float32):
+        raise ValueError("logits_dump must be float32 [T][E]")
+    if stats is not None and (stats.shape != (2,) or stats.dtype != torch.float64):
+        raise ValueError("stats must be float64 [2]")
+    ws_bytes = workspace.numel() * workspace.element_size()
+    st = lib().idb_aux_router_forward(_ptr(x), _ptr(W_g), _dtype_code(x), int(weight_layout), T, d, E, K,
+                                      float(alpha), _ptr(expert_idx), _ptr(gate_w), _ptr(counts), _ptr(f), _ptr(P),
+                                      _ptr(loss), _ptr(stats), _ptr(logits_dump), _ptr(workspace), ws_bytes,
+                                      int(variant), _stream(stream))
+    _check("idb_aux_router_forward", st)
 
 
 # ---------------------------------------------------------------------------- layers and diagnostics

@@ -36,16 +36,23 @@ constexpr int kMaxKGpu = 32;
 size_t round_up(size_t n) { return (n + 255) & ~size_t(255); }
 
 // Resolve a router variant for a shape; returns IDB_OK and the tiling, or an error.
-idb_status resolve_tiling(int32_t E, idb_dtype dtype, int32_t variant, idb::RouterTiling* out) {
+// one_slice: only tilings whose workgroups cover all E experts and that have
+// the softmax mode (the auxiliary-loss statistics need each token's whole
+// softmax in one workgroup).
+idb_status resolve_tiling(int32_t E, idb_dtype dtype, int32_t variant, idb::RouterTiling* out,
+                          bool one_slice = false) {
     const int n = idb::router_tiling_count();
     const int want_f32 = dtype == IDB_DTYPE_F32;
+    const int max_slices = one_slice ? 1 : kMaxSlices;
     if (variant != 0) {
         if (variant < 1 || variant > n) return fail(IDB_ERR_INVALID_ARG, "router variant %d out of range", variant);
         idb::RouterTiling t = idb::router_tiling(variant - 1);
         if (t.is_f32 != want_f32) return fail(IDB_ERR_UNSUPPORTED, "router variant %d is for another dtype", variant);
-        if (idb::router_slices(t, E) > kMaxSlices)
-            return fail(IDB_ERR_UNSUPPORTED, "router variant %d needs more than %d expert slices", variant,
-                        kMaxSlices);
+        if (idb::router_slices(t, E) > max_slices)
+            return fail(IDB_ERR_UNSUPPORTED, "router variant %d needs more than %d expert slice(s) for E=%d",
+                        variant, max_slices, E);
+        if (one_slice && !t.softmax)
+            return fail(IDB_ERR_UNSUPPORTED, "router variant %d has no softmax mode", variant);
         *out = t;
         return IDB_OK;
     }
@@ -58,7 +65,7 @@ idb_status resolve_tiling(int32_t E, idb_dtype dtype, int32_t variant, idb::Rout
         idb::RouterTiling t = idb::router_tiling(i);
         if (t.is_f32 != want_f32) continue;
         const int ns = idb::router_slices(t, E);
-        if (ns > kMaxSlices) continue;
+        if (ns > max_slices || (one_slice && !t.softmax)) continue;
         const long waste = (long)ns * t.waves * t.we - E;
         if (!found || waste < best_waste || (waste == best_waste && t.rank < best.rank)) {
             best = t;
@@ -66,7 +73,9 @@ idb_status resolve_tiling(int32_t E, idb_dtype dtype, int32_t variant, idb::Rout
             found = true;
         }
     }
-    if (!found) return fail(IDB_ERR_UNSUPPORTED, "no router tiling for E=%d", E);
+    if (!found)
+        return fail(IDB_ERR_UNSUPPORTED, one_slice ? "no one-slice router tiling for E=%d" : "no router tiling for E=%d",
+                    E);
     *out = best;
     return IDB_OK;
 }
@@ -93,17 +102,28 @@ size_t router_ws_bytes(int64_t T, int32_t E, int32_t K, const idb::RouterTiling&
     return 3 * round_up((size_t)T * ns * K * 4) + 256;
 }
 
+// Auxiliary-loss statistics: per-tile softmax column sums [tiles][E] fp32,
+// per-tile counts [tiles][E] int32, kAuxMaxBlocks block records, the ticket.
+size_t aux_rows_bytes(int64_t T, int32_t E, const idb::RouterTiling& t) {
+    return round_up((size_t)((T + t.bt - 1) / t.bt) * E * 4);
+}
+size_t aux_ws_bytes(int64_t T, int32_t E, const idb::RouterTiling& t) {
+    return 2 * aux_rows_bytes(T, E, t) + round_up(idb::kAuxMaxBlocks * sizeof(idb::AuxPartial)) + 256;
+}
+
 struct RouterCall {
     idb::RouterTiling tiling;
     idb::RouterArgs args;
-    unsigned* ticket;  // the merge's ticket in the workspace (multi-slice tilings)
+    unsigned* ticket;  // the merge's (multi-slice tilings) or the statistics kernel's ticket
+    idb::AuxPartial* aux_partial;  // auxiliary-loss statistics: block records
 };
 
 idb_status prepare_router(const void* x, const void* W_g, idb_dtype dtype, idb_weight_layout layout,
                           const float* bias, int64_t T, int32_t d,
                           int32_t E, int32_t K, int32_t* expert_idx, float* gate_w, int32_t* counts,
                           int32_t accumulate_counts, float* scores_dump, void* workspace, size_t workspace_bytes,
-                          int32_t variant, bool need_inputs, RouterCall* call, bool qb = false) {
+                          int32_t variant, bool need_inputs, RouterCall* call, bool qb = false,
+                          bool aux = false) {
     // Quantile Balancing keeps K + 1 candidates per token (the (K+1)-th is the cutoff)
     const int32_t KL = qb ? K + 1 : K;
     idb_status st = check_router_shape(T, d, E, KL, dtype);
@@ -111,18 +131,18 @@ idb_status prepare_router(const void* x, const void* W_g, idb_dtype dtype, idb_w
     if (layout != IDB_WEIGHT_ROW_MAJOR && layout != IDB_WEIGHT_PACKED)
         return fail(IDB_ERR_INVALID_ARG, "unknown weight layout %d", layout);
     if (need_inputs) {
-        if (!x || !W_g || !bias) return fail(IDB_ERR_INVALID_ARG, "null input pointer");
+        if (!x || !W_g || (!bias && !aux)) return fail(IDB_ERR_INVALID_ARG, "null input pointer");
         if (!aligned(x, 16) || !aligned(W_g, 16)) return fail(IDB_ERR_INVALID_ARG, "x and W_g must be 16-byte aligned");
-        if (!aligned(bias, 4)) return fail(IDB_ERR_INVALID_ARG, "bias must be 4-byte aligned");
+        if (bias && !aligned(bias, 4)) return fail(IDB_ERR_INVALID_ARG, "bias must be 4-byte aligned");
         if (scores_dump && !aligned(scores_dump, 16))
             return fail(IDB_ERR_INVALID_ARG, "scores_dump must be 16-byte aligned");
     }
     if (!expert_idx || !gate_w || !counts) return fail(IDB_ERR_INVALID_ARG, "null output pointer");
     if (!aligned(expert_idx, 4) || !aligned(gate_w, 4) || !aligned(counts, 4))
         return fail(IDB_ERR_INVALID_ARG, "outputs must be 4-byte aligned");
-    st = resolve_tiling(E, dtype, variant, &call->tiling);
+    st = resolve_tiling(E, dtype, variant, &call->tiling, aux);
     if (st != IDB_OK) return st;
-    const size_t need = router_ws_bytes(T, E, KL, call->tiling);
+    const size_t need = aux ? aux_ws_bytes(T, E, call->tiling) : router_ws_bytes(T, E, KL, call->tiling);
     if (need > 0) {
         if (!workspace || workspace_bytes < need)
             return fail(IDB_ERR_INVALID_ARG, "workspace of %zu bytes needed, %zu given", need, workspace_bytes);
@@ -151,13 +171,30 @@ idb_status prepare_router(const void* x, const void* W_g, idb_dtype dtype, idb_w
     a.ticket = nullptr;
     a.alpha = nullptr;
     a.scores_t = nullptr;
+    a.softmax = aux ? 1 : 0;
+    a.prob_part = nullptr;
+    a.cnt_part = nullptr;
     call->ticket = need ? reinterpret_cast<unsigned*>(ws + 3 * part) : nullptr;
+    call->aux_partial = nullptr;
+    if (aux) {
+        // one slice: no candidates; the statistics' per-tile rows instead
+        const size_t rows = aux_rows_bytes(T, E, call->tiling);
+        a.bias = nullptr;
+        a.cand_v = a.cand_s = nullptr;
+        a.cand_i = nullptr;
+        a.prob_part = reinterpret_cast<float*>(ws);
+        a.cnt_part = reinterpret_cast<int32_t*>(ws + rows);
+        call->aux_partial = reinterpret_cast<idb::AuxPartial*>(ws + 2 * rows);
+        call->ticket =
+            reinterpret_cast<unsigned*>(ws + 2 * rows + round_up(idb::kAuxMaxBlocks * sizeof(idb::AuxPartial)));
+        a.ticket = call->ticket;  // zeroed by the router kernel, taken by the statistics kernel
+    }
     return IDB_OK;
 }
 
 idb_status enqueue_score_select(const RouterCall& c, int32_t accumulate_counts, hipStream_t stream) {
     const int ns = idb::router_slices(c.tiling, c.args.E);
-    if (ns <= 1 && !accumulate_counts) {
+    if (ns <= 1 && !accumulate_counts && !c.args.cnt_part) {
         idb_status st = hip_result(idb::launch_fill_i32(c.args.counts, 0, c.args.E, stream), "zero counts");
         if (st != IDB_OK) return st;
     }
@@ -382,6 +419,36 @@ idb_status idb_qb_update(const float* scores_t, const float* alpha, int64_t T, i
     if (!aligned(scores_t, 4) || !aligned(alpha, 4) || !aligned(bias, 4))
         return fail(IDB_ERR_INVALID_ARG, "misaligned buffer");
     return hip_result(idb::launch_qb_update(scores_t, alpha, T, E, K, rho, bias, stream), "Quantile Balancing launch");
+}
+
+size_t idb_aux_router_workspace_bytes(int64_t T, int32_t d, int32_t E, int32_t K, idb_dtype dtype,
+                                      int32_t variant) {
+    if (check_router_shape(T, d, E, K, dtype) != IDB_OK) return 0;
+    idb::RouterTiling t;
+    if (resolve_tiling(E, dtype, variant, &t, true) != IDB_OK) return 0;
+    return aux_ws_bytes(T, E, t);
+}
+
+idb_status idb_aux_router_forward(const void* x, const void* W_g, idb_dtype dtype, idb_weight_layout weight_layout,
+                                  int64_t T, int32_t d, int32_t E, int32_t K, double alpha, int32_t* expert_idx,
+                                  float* gate_w, int32_t* counts, double* f, double* P, double* loss,
+                                  double* out_maxvio_minvio, float* logits_dump, void* workspace,
+                                  size_t workspace_bytes, int32_t variant, hipStream_t stream) {
+    if (!f || !P || !loss) return fail(IDB_ERR_INVALID_ARG, "null statistics output");
+    if (!aligned(f, 8) || !aligned(P, 8) || !aligned(loss, 8) ||
+        (out_maxvio_minvio && !aligned(out_maxvio_minvio, 8)))
+        return fail(IDB_ERR_INVALID_ARG, "statistics outputs must be 8-byte aligned");
+    if (!isfinite(alpha)) return fail(IDB_ERR_INVALID_ARG, "alpha must be finite");
+    RouterCall c;
+    idb_status st = prepare_router(x, W_g, dtype, weight_layout, nullptr, T, d, E, K, expert_idx, gate_w, counts, 0,
+                                   logits_dump, workspace, workspace_bytes, variant, true, &c, false, true);
+    if (st != IDB_OK) return st;
+    st = enqueue_score_select(c, 0, stream);
+    if (st != IDB_OK) return st;
+    const int64_t tiles = (T + c.tiling.bt - 1) / c.tiling.bt;  // <= 2^26 / 64
+    return hip_result(idb::launch_aux_stats(c.args.prob_part, c.args.cnt_part, (int)tiles, T, E, alpha, counts, f, P,
+                                            loss, out_maxvio_minvio, c.aux_partial, c.ticket, stream),
+                      "auxiliary-loss statistics launch");
 }
 
 idb_status idb_controller_update_layers(const int32_t* counts, int32_t L, const idb_controller_cfg* cfg,

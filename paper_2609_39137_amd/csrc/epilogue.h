@@ -26,6 +26,11 @@
 // C-G and the biased value of rank K (the cutoff alpha of Eq.
 // pid-quantile-def) is written per token; with a.scores_t set, the scores are
 // also written expert-major after step A.
+// In softmax mode (SM; auxiliary-loss routing, one slice) the LDS matrix holds
+// logits and the bias is zero: step C also finds each token's largest logit
+// M and Z = sum exp(z - M), the gate weights are exp(z_r - z_top) over their
+// sum, and with a.prob_part set the tile's column sums of exp(z - M) / Z go
+// out per token tile.
 #pragma once
 
 #include "common.h"
@@ -35,6 +40,10 @@ namespace idb {
 namespace {
 
 constexpr int kCap = 32;      // candidate list capacity per token and slice
+constexpr float kLog2e = 1.4426950408889634f;
+
+// exp(x) as 2^(x log2 e) with the hardware exp2 (about 1 ulp; exp(-inf) = 0).
+__device__ __forceinline__ float exp_fast(float x) { return __builtin_amdgcn_exp2f(x * kLog2e); }
 constexpr int kScoreLds = 100000;  // LDS budget of the epilogue's score matrix
 
 // Epilogue layout for NT threads, BT tokens, BE experts per workgroup; the
@@ -96,12 +105,13 @@ __device__ __forceinline__ void flush_hist(const int* hist, int32_t* counts, int
 
 // Loads the slice's bias into registers (issued before the contraction, so
 // it arrives meanwhile); the epilogue moves it to LDS.
-template <class EC>
+template <class EC, bool SM = false>
 __device__ __forceinline__ void prefetch_bias(const RouterArgs& a, int sbase, float (&breg)[EC::NBIAS]) {
 #pragma unroll
     for (int i = 0; i < EC::NBIAS; ++i) {
         const int c = threadIdx.x + EC::NT * i;
-        breg[i] = (c < EC::BE && sbase + c < a.E) ? a.bias[sbase + c] : 0.0f;
+        // softmax mode (auxiliary-loss routing) keeps no bias
+        breg[i] = (!SM && c < EC::BE && sbase + c < a.E) ? a.bias[sbase + c] : 0.0f;
     }
 }
 
@@ -124,7 +134,7 @@ __device__ __forceinline__ void epi_begin(unsigned char* smem, const float (&bre
 // 0..TPP-1 of the LDS score matrix sc (padding experts: -inf).  One slice:
 // outputs and the LDS histogram; several: the slice's candidates.  Ends with a
 // barrier.
-template <class EC, class StoreFn>
+template <class EC, bool SM, class StoreFn>
 __device__ __forceinline__ void epi_tile(const RouterArgs& a, int NS, int slice, int64_t tok0, unsigned char* smem,
                                          StoreFn&& store_pass) {
     using C = EC;
@@ -160,6 +170,10 @@ __device__ __forceinline__ void epi_tile(const RouterArgs& a, int NS, int slice,
             valid[m >> 1] |= bits << (16 * (m & 1));
         }
     }
+
+    float pacc[C::NBIAS];  // softmax column sums of the tile (prob_part)
+#pragma unroll
+    for (int i = 0; i < C::NBIAS; ++i) pacc[i] = 0.0f;
 
 #pragma unroll
     for (int pass = 0; pass < C::NPASS; ++pass) {
@@ -220,6 +234,7 @@ __device__ __forceinline__ void epi_tile(const RouterArgs& a, int NS, int slice,
         // tests its own maxima against all 32, a max over the token's lanes
         // combines them.
         float tau = -INFINITY;
+        float zmax = 0.0f, zsum = 0.0f;  // softmax mode
         {
             float g[C::NG];
 #pragma unroll
@@ -239,6 +254,19 @@ __device__ __forceinline__ void epi_tile(const RouterArgs& a, int NS, int slice,
             }
 #pragma unroll
             for (int o = 1; o < C::TPT; o <<= 1) tau = fmaxf(tau, __shfl_xor(tau, o));
+            if constexpr (SM) {
+                // the token's largest logit and Z = sum exp(z - M): each
+                // thread over its columns in order (padding: exp(-inf) = 0),
+                // then a butterfly over the token's threads (every lane ends
+                // with the same bits: fp32 addition commutes)
+                zmax = g[0];
+#pragma unroll
+                for (int j = 1; j < C::NG; ++j) zmax = fmaxf(zmax, g[j]);
+#pragma unroll
+                for (int j = 0; j < C::VPT; ++j) zsum = zsum + exp_fast(v[j] - zmax);
+#pragma unroll
+                for (int o = 1; o < C::TPT; o <<= 1) zsum = zsum + __shfl_xor(zsum, o);
+            }
         }
         // Bit j: v_j >= tau, read off the sign of v_j - tau (a difference of
         // two finite floats is +0 only when they are equal, and -inf - tau is
@@ -266,6 +294,11 @@ __device__ __forceinline__ void epi_tile(const RouterArgs& a, int NS, int slice,
             const int m = cnt[tl * C::CNS + o];
             off += (o < q) ? m : 0;
             n += m;
+        }
+        if (SM && q == 0) {
+            // the group maxima are no longer read: the row keeps M and 1/Z
+            gm[tl * C::GMS + 0] = zmax;
+            gm[tl * C::GMS + 1] = 1.0f / zsum;
         }
         const bool listed = n <= kCap;
         if (!listed) {
@@ -355,6 +388,22 @@ __device__ __forceinline__ void epi_tile(const RouterArgs& a, int NS, int slice,
                         a.cand_i[base + r] = e;
                     }
                 } else {
+                    if constexpr (SM) {
+                        // gate weights: the selected probabilities
+                        // renormalised, exp(z_r - z_top) over their fp32 sum
+                        // in rank order (the first term is exactly 1)
+                        const float ztop = sc[tl * C::RS + (si[tl * C::LSS + 0] - sbase)];
+                        float den = 0.0f;
+#pragma unroll 8
+                        for (int r = 0; r < K; ++r)
+                            den = den + exp_fast(sc[tl * C::RS + (si[tl * C::LSS + r] - sbase)] - ztop);
+                        for (int r = q; r < K; r += C::TPT) {
+                            const int e = si[tl * C::LSS + r];
+                            a.idx[tok * K + r] = e;
+                            a.w[tok * K + r] = exp_fast(sc[tl * C::RS + (e - sbase)] - ztop) / den;
+                            atomicAdd(&hist[e], 1);
+                        }
+                    } else {
                     // gate weights: den is the fp32 sum of the selected
                     // unbiased scores in rank order
                     float den = 0.0f;
@@ -367,6 +416,7 @@ __device__ __forceinline__ void epi_tile(const RouterArgs& a, int NS, int slice,
                         a.w[tok * K + r] = (den == 0.0f) ? 1.0f / (float)K : s / den;
                         atomicAdd(&hist[e], 1);
                     }
+                    }
                     if (a.alpha && q == 0) {
                         // cutoff: the biased value of rank K
                         const int e = si[tl * C::LSS + K];
@@ -375,18 +425,51 @@ __device__ __forceinline__ void epi_tile(const RouterArgs& a, int NS, int slice,
                 }
             }
         }
+        if (SM && NS == 1 && a.prob_part) {
+            // column sums of the pass's probabilities p = exp(z - M) / Z,
+            // tokens in order; a thread owns columns tid, tid + NT, ...
+            const int64_t left = T - (tok0 + pass * C::TPP);
+            const int rows = left < C::TPP ? (int)left : C::TPP;
+#pragma unroll
+            for (int i = 0; i < C::NBIAS; ++i) {
+                const int c = tid + C::NT * i;
+                if (c < C::BE && sbase + c < E) {
+                    float s = 0.0f;
+                    for (int row = 0; row < rows; ++row)
+                        s = s + exp_fast(sc[row * C::RS + c] - gm[row * C::GMS + 0]) * gm[row * C::GMS + 1];
+                    pacc[i] = pacc[i] + s;
+                }
+            }
+        }
         __syncthreads();
+    }
+    if (SM && NS == 1 && a.prob_part) {
+        float* out = a.prob_part + (tok0 / C::BT) * (int64_t)E + sbase;
+#pragma unroll
+        for (int i = 0; i < C::NBIAS; ++i) {
+            const int c = tid + C::NT * i;
+            if (c < C::BE && sbase + c < E) out[c] = pacc[i];
+        }
     }
 }
 
-// The whole epilogue of one workgroup tile (the fused router kernels).
-template <class EC, class StoreFn>
+// The whole epilogue of one workgroup tile (the fused router kernels); SM:
+// the softmax mode of auxiliary-loss routing.
+template <class EC, bool SM, class StoreFn>
 __device__ __forceinline__ void select_epilogue(const RouterArgs& a, int NS, int slice, int64_t tok0,
                                                 unsigned char* smem, const float (&breg)[EC::NBIAS],
                                                 StoreFn&& store_pass) {
     epi_begin<EC>(smem, breg);
-    epi_tile<EC>(a, NS, slice, tok0, smem, store_pass);
-    if (NS == 1) flush_hist(reinterpret_cast<const int*>(smem + EC::OFF_HIST), a.counts, a.E);
+    epi_tile<EC, SM>(a, NS, slice, tok0, smem, store_pass);
+    if (NS != 1) return;
+    const int* hist = reinterpret_cast<const int*>(smem + EC::OFF_HIST);
+    if (SM && a.cnt_part) {
+        // the tile's counts as one row (summed in order by the statistics kernel)
+        int32_t* row = a.cnt_part + (tok0 / EC::BT) * (int64_t)a.E;
+        for (int e = threadIdx.x; e < a.E; e += EC::NT) row[e] = hist[e];
+    } else {
+        flush_hist(hist, a.counts, a.E);
+    }
 }
 
 }  // namespace

@@ -22,6 +22,21 @@ constexpr int kEntropyBlocks = 512;
 hipError_t launch_routing_entropy(const float* gate_w, int64_t T, int K, const float* scores, const float* bias,
                                   int E, double* partial, double* out, hipStream_t stream);
 
+// Auxiliary-loss statistics from the router's per-tile softmax column sums
+// prob_part [tiles][E] and counts cnt_part [tiles][E]: counts [E], f [E],
+// P [E], loss, and (stats nullable) MaxVio/MinVio.  partial holds
+// kAuxMaxBlocks block records; the ticket must be zero (the router kernel
+// zeroes it).
+constexpr int kAuxMaxBlocks = 16;  // expert blocks of 64 for E <= 1024
+struct AuxPartial {
+    double fp;  // sum of f_i P_i over the block's experts
+    long long sum;
+    int max, min;
+};
+hipError_t launch_aux_stats(const float* prob_part, const int32_t* cnt_part, int tiles, int64_t T, int E,
+                            double alpha, int32_t* counts, double* f, double* P, double* loss, double* stats,
+                            AuxPartial* partial, unsigned* ticket, hipStream_t stream);
+
 hipError_t launch_fill_i32(int32_t* p, int32_t value, int64_t n, hipStream_t stream);
 // Quantile Balancing's bias update from expert-major scores and cutoffs.
 hipError_t launch_qb_update(const float* scores_t, const float* alpha, int64_t T, int E, int K, float rho,
@@ -38,6 +53,7 @@ struct RouterTiling {
     int bt;       // tokens per workgroup
     int we;       // experts per wave (a workgroup's slice is waves * we experts)
     int rank;     // preference among tilings with equally few padded experts (lower first)
+    int softmax;  // the softmax mode (auxiliary-loss routing) is compiled for this tiling
 };
 
 // Number of known tilings and the i-th one (0-based).
@@ -68,6 +84,15 @@ struct RouterArgs {
     // (K+1)-th largest biased score per token; scores_t [E][T] the scores.
     float* alpha;
     float* scores_t;
+    // Auxiliary-loss routing (Eq. pid-auxloss; one-slice tilings only): the
+    // logits themselves are ranked (bias null: no bias), the gate weights are
+    // the selected softmax probabilities renormalised, and with prob_part set
+    // each token tile's column sums of the full softmax go to [tiles][E].
+    int softmax;
+    float* prob_part;
+    // softmax mode: each token tile's expert counts go to cnt_part [tiles][E]
+    // (no atomics; the statistics kernel sums them into counts)
+    int32_t* cnt_part;
 };
 
 // Slices of E covered by one workgroup column for tiling t.

@@ -92,7 +92,7 @@ struct Cfg32 {
     static_assert(PPT * NT == BT * 8, "token-tile pieces must split evenly over threads");
 };
 
-template <bool F32, bool PACKED, int WAVES, int TBW, int NBLK>
+template <bool F32, bool PACKED, int WAVES, int TBW, int NBLK, bool SM>
 __global__ __launch_bounds__(WAVES * 64) void router32_kernel(RouterArgs a, int NS) {
     using C = Cfg32<F32, WAVES, TBW, NBLK>;
     using EC = typename C::Epi;
@@ -116,10 +116,10 @@ __global__ __launch_bounds__(WAVES * 64) void router32_kernel(RouterArgs a, int 
 
     if (a.zero_counts && blockIdx.x == 0)
         for (int e = tid; e < E; e += C::NT) a.counts[e] = 0;
-    if (a.ticket && blockIdx.x == 0 && tid == 0) *a.ticket = 0u;
+    if (a.ticket && blockIdx.x == 0 && tid == 0) *a.ticket = 0u;  // the merge's or the statistics kernel's
     const int sbase = slice * C::BE;
     float breg[EC::NBIAS];
-    prefetch_bias<EC>(a, sbase, breg);
+    prefetch_bias<EC, SM>(a, sbase, breg);
 
     // ---------------------------------------------------------------- contraction
     // Operands are fetched with buffer loads: a scalar resource per operand
@@ -244,6 +244,11 @@ __global__ __launch_bounds__(WAVES * 64) void router32_kernel(RouterArgs a, int 
     // (r%4).  E is a multiple of 32, so a whole 32-expert block is real or
     // padding.
     const int ccol = wave * C::WE + 4 * h;
+    // score activation; auxiliary-loss routing (SM) ranks the logits themselves
+    auto act = [&](float z) {
+        if constexpr (SM) return z;
+        else return sigmoid_fast(z);
+    };
     auto store_pass = [&](int pass, float* sc) {
         constexpr int PB = EC::TPP / 32;
 #pragma unroll
@@ -257,10 +262,10 @@ __global__ __launch_bounds__(WAVES * 64) void router32_kernel(RouterArgs a, int 
 #pragma unroll
                 for (int r4 = 0; r4 < 4; ++r4) {
                     float4 s4;
-                    s4.x = real ? sigmoid_fast(acc[tb][nbk][4 * r4 + 0]) : -INFINITY;
-                    s4.y = real ? sigmoid_fast(acc[tb][nbk][4 * r4 + 1]) : -INFINITY;
-                    s4.z = real ? sigmoid_fast(acc[tb][nbk][4 * r4 + 2]) : -INFINITY;
-                    s4.w = real ? sigmoid_fast(acc[tb][nbk][4 * r4 + 3]) : -INFINITY;
+                    s4.x = real ? act(acc[tb][nbk][4 * r4 + 0]) : -INFINITY;
+                    s4.y = real ? act(acc[tb][nbk][4 * r4 + 1]) : -INFINITY;
+                    s4.z = real ? act(acc[tb][nbk][4 * r4 + 2]) : -INFINITY;
+                    s4.w = real ? act(acc[tb][nbk][4 * r4 + 3]) : -INFINITY;
                     const int col = ccol + nbk * 32 + 8 * r4;
                     *reinterpret_cast<float4*>(sc + row * EC::RS + col) = s4;
                     if (a.dump && real && tok < T) *reinterpret_cast<float4*>(a.dump + tok * E + sbase + col) = s4;
@@ -268,7 +273,7 @@ __global__ __launch_bounds__(WAVES * 64) void router32_kernel(RouterArgs a, int 
             }
         }
     };
-    select_epilogue<EC>(a, NS, slice, tok0, smem, breg, store_pass);
+    select_epilogue<EC, SM>(a, NS, slice, tok0, smem, breg, store_pass);
 }
 
 template <int WAVES, int TT, int ET>
@@ -284,7 +289,7 @@ struct Cfg16 {
     static_assert(PPT * NT == BT * 8, "token-tile pieces must split evenly over threads");
 };
 
-template <bool PACKED, int WAVES, int TT, int ET>
+template <bool PACKED, int WAVES, int TT, int ET, bool SM>
 __global__ __launch_bounds__(WAVES * 64) void router16_kernel(RouterArgs a, int NS) {
     using C = Cfg16<WAVES, TT, ET>;
     using EC = typename C::Epi;
@@ -307,10 +312,10 @@ __global__ __launch_bounds__(WAVES * 64) void router16_kernel(RouterArgs a, int 
 
     if (a.zero_counts && blockIdx.x == 0)
         for (int e = tid; e < E; e += C::NT) a.counts[e] = 0;
-    if (a.ticket && blockIdx.x == 0 && tid == 0) *a.ticket = 0u;
+    if (a.ticket && blockIdx.x == 0 && tid == 0) *a.ticket = 0u;  // the merge's or the statistics kernel's
     const int sbase = slice * C::BE;
     float breg[EC::NBIAS];
-    prefetch_bias<EC>(a, sbase, breg);
+    prefetch_bias<EC, SM>(a, sbase, breg);
 
     // ---------------------------------------------------------------- contraction
     // Buffer loads as in router32_kernel.  A operand of expert tile et, chunk
@@ -426,6 +431,11 @@ __global__ __launch_bounds__(WAVES * 64) void router16_kernel(RouterArgs a, int 
     // ---------------------------------------------------------------- selection
     // Slice column of accumulator (et, r): wave*WE + 16 et + 4 (l/16) + r.
     // E is a multiple of 32, so a whole 16-expert tile is real or padding.
+    // score activation; auxiliary-loss routing (SM) ranks the logits themselves
+    auto act = [&](float z) {
+        if constexpr (SM) return z;
+        else return sigmoid_fast(z);
+    };
     auto store_pass = [&](int pass, float* sc) {
         constexpr int PT = EC::TPP / 16;  // token tiles per pass
 #pragma unroll
@@ -437,17 +447,17 @@ __global__ __launch_bounds__(WAVES * 64) void router16_kernel(RouterArgs a, int 
             for (int et = 0; et < ET; ++et) {
                 const bool real = sbase + wave * C::WE + et * 16 < E;
                 float4 s4;
-                s4.x = real ? sigmoid_fast(acc[tt][et][0]) : -INFINITY;
-                s4.y = real ? sigmoid_fast(acc[tt][et][1]) : -INFINITY;
-                s4.z = real ? sigmoid_fast(acc[tt][et][2]) : -INFINITY;
-                s4.w = real ? sigmoid_fast(acc[tt][et][3]) : -INFINITY;
+                s4.x = real ? act(acc[tt][et][0]) : -INFINITY;
+                s4.y = real ? act(acc[tt][et][1]) : -INFINITY;
+                s4.z = real ? act(acc[tt][et][2]) : -INFINITY;
+                s4.w = real ? act(acc[tt][et][3]) : -INFINITY;
                 const int col = wave * C::WE + et * 16 + 4 * g4;
                 *reinterpret_cast<float4*>(sc + row * EC::RS + col) = s4;
                 if (a.dump && real && tok < T) *reinterpret_cast<float4*>(a.dump + tok * E + sbase + col) = s4;
             }
         }
     };
-    select_epilogue<EC>(a, NS, slice, tok0, smem, breg, store_pass);
+    select_epilogue<EC, SM>(a, NS, slice, tok0, smem, breg, store_pass);
 }
 
 // Merge the slices' rank-ordered candidate lists into the final Top-K, compute
@@ -668,26 +678,36 @@ __global__ void pack_weight_kernel(const char* __restrict__ W, char* __restrict_
     }
 }
 
-template <bool F32, bool PACKED, int WAVES, int TBW, int NBLK>
+template <bool F32, bool PACKED, int WAVES, int TBW, int NBLK, bool SM = false>
 hipError_t launch32(const RouterArgs& a, int NS, hipStream_t stream) {
     using C = Cfg32<F32, WAVES, TBW, NBLK>;
     const int64_t blocks = (a.T + C::BT - 1) / C::BT * NS;
-    hipLaunchKernelGGL((router32_kernel<F32, PACKED, WAVES, TBW, NBLK>), dim3((unsigned)blocks), dim3(C::NT), 0,
+    hipLaunchKernelGGL((router32_kernel<F32, PACKED, WAVES, TBW, NBLK, SM>), dim3((unsigned)blocks), dim3(C::NT), 0,
                        stream, a, NS);
     return hipGetLastError();
 }
 
-template <bool PACKED, int WAVES, int TT, int ET>
+template <bool PACKED, int WAVES, int TT, int ET, bool SM = false>
 hipError_t launch16(const RouterArgs& a, int NS, hipStream_t stream) {
     using C = Cfg16<WAVES, TT, ET>;
     const int64_t blocks = (a.T + C::BT - 1) / C::BT * NS;
-    hipLaunchKernelGGL((router16_kernel<PACKED, WAVES, TT, ET>), dim3((unsigned)blocks), dim3(C::NT), 0, stream, a,
-                       NS);
+    hipLaunchKernelGGL((router16_kernel<PACKED, WAVES, TT, ET, SM>), dim3((unsigned)blocks), dim3(C::NT), 0, stream,
+                       a, NS);
     return hipGetLastError();
 }
 
 template <bool PACKED>
 hipError_t launch_layout(const RouterTiling& t, const RouterArgs& a, int NS, hipStream_t stream) {
+    if (a.softmax) {
+        // softmax mode: compiled for the tilings marked in kTilings only
+        switch (t.id) {
+            case 2: return launch32<false, PACKED, 8, 2, 3, true>(a, NS, stream);
+            case 4: return launch32<false, PACKED, 4, 4, 1, true>(a, NS, stream);
+            case 5: return launch32<true, PACKED, 4, 4, 1, true>(a, NS, stream);
+            case 7: return launch16<PACKED, 8, 4, 6, true>(a, NS, stream);
+            default: return hipErrorInvalidValue;
+        }
+    }
     switch (t.id) {
         case 1: return launch32<false, PACKED, 4, 4, 3>(a, NS, stream);
         case 2: return launch32<false, PACKED, 8, 2, 3>(a, NS, stream);
@@ -701,15 +721,16 @@ hipError_t launch_layout(const RouterTiling& t, const RouterArgs& a, int NS, hip
 }
 
 // id, fp32 input, waves, tokens per workgroup, experts per wave, preference
-// among tilings with equally few padded experts (lower first).
+// among tilings with equally few padded experts (lower first), softmax mode
+// compiled.
 const RouterTiling kTilings[] = {
-    {1, 0, 4, 128, 96, 2},  // bf16 32x32 tiles: 128 tokens x 384 experts per workgroup
-    {2, 0, 8, 64, 96, 1},   // bf16 32x32 tiles: 64 tokens x 768 experts
-    {3, 0, 4, 128, 64, 3},  // bf16 32x32 tiles: 128 tokens x 256 experts
-    {4, 0, 4, 128, 32, 4},  // bf16 32x32 tiles: 128 tokens x 128 experts
-    {5, 1, 4, 128, 32, 0},  // fp32 32x32 tiles: 128 tokens x 128 experts
-    {6, 0, 8, 128, 48, 0},  // bf16 16x16 tiles: 128 tokens x 384 experts, two waves per SIMD
-    {7, 0, 8, 64, 96, 5},   // bf16 16x16 tiles: 64 tokens x 768 experts, two waves per SIMD
+    {1, 0, 4, 128, 96, 2, 0},  // bf16 32x32 tiles: 128 tokens x 384 experts per workgroup
+    {2, 0, 8, 64, 96, 5, 1},   // bf16 32x32 tiles: 64 tokens x 768 experts
+    {3, 0, 4, 128, 64, 3, 0},  // bf16 32x32 tiles: 128 tokens x 256 experts
+    {4, 0, 4, 128, 32, 4, 1},  // bf16 32x32 tiles: 128 tokens x 128 experts
+    {5, 1, 4, 128, 32, 0, 1},  // fp32 32x32 tiles: 128 tokens x 128 experts
+    {6, 0, 8, 128, 48, 0, 0},  // bf16 16x16 tiles: 128 tokens x 384 experts, two waves per SIMD
+    {7, 0, 8, 64, 96, 1, 1},   // bf16 16x16 tiles: 64 tokens x 768 experts, two waves per SIMD
 };
 
 }  // namespace

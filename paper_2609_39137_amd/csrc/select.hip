@@ -85,7 +85,7 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(RouterArgs a, const
             }
             if (next < ntiles) load(next);
         };
-        epi_tile<EC>(a, 1, 0, tile * kSelTile, smem, store_pass);
+        epi_tile<EC, false>(a, 1, 0, tile * kSelTile, smem, store_pass);
     }
     flush_hist(reinterpret_cast<const int*>(smem + EC::OFF_HIST), a.counts, E);
 }

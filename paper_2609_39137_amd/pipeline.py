@@ -100,3 +100,30 @@ class RouterStep:
         self.qb_route(x, W, stream=stream)
         B.idb_load_stats(self.counts, self.stats, stream)
         B.idb_qb_update(self.scores_t, self.alpha, self.K, rho, self.state.bias, stream)
+
+    # ------------------------------------------------------------ auxiliary-loss statistics
+
+    def aux_buffers(self, variant: int = 0):
+        """Allocate (once) the auxiliary-loss outputs f, P, loss and their workspace (one-slice tiling)."""
+        if getattr(self, "aux_P", None) is None:
+            dev = self.idx.device
+            self.aux_variant = variant
+            self.aux_f = torch.empty(self.E, dtype=torch.float64, device=dev)
+            self.aux_P = torch.empty(self.E, dtype=torch.float64, device=dev)
+            self.aux_loss = torch.empty(1, dtype=torch.float64, device=dev)
+            n = B.idb_aux_router_workspace_bytes(self.T, self.d, self.E, self.K, self.dtype_code, variant)
+            if n == 0:
+                raise B.IdbError("idb_aux_router_workspace_bytes", B.IDB_ERR_UNSUPPORTED,
+                                 f"no one-slice router tiling for E={self.E} (variant {variant})")
+            self.aux_workspace = torch.empty(n, dtype=torch.uint8, device=dev)
+            self.aux_info = B.idb_router_variant_info(self.T, self.d, self.E, self.K, self.dtype_code, variant) \
+                if variant else None
+
+    def aux_step(self, x, W=None, alpha: float = 0.05, stream=None):
+        """Softmax routing without bias, the auxiliary-loss statistics f, P and alpha sum f P
+        (Eq. pid-auxloss) and MaxVio/MinVio of the counts (two launches)."""
+        self.aux_buffers()
+        Wt, layout = self._weights(W)
+        B.idb_aux_router_forward(x, Wt, self.K, alpha, self.idx, self.w, self.counts, self.aux_f, self.aux_P,
+                                 self.aux_loss, self.aux_workspace, None, self.aux_variant, stream, layout,
+                                 stats=self.stats)

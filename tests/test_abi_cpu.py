@@ -282,3 +282,42 @@ def test_layers_and_entropy_reject_invalid_arguments():
     assert L.idb_routing_entropy(A16, 100, 10, None, None, 0, A16, ws - 8, A16, None) == B.IDB_ERR_INVALID_ARG
     assert L.idb_routing_entropy(A16, 100, 10, A16, None, 768, A16, ws, A16, None) == B.IDB_ERR_INVALID_ARG
     assert L.idb_routing_entropy(None, 100, 10, None, None, 0, A16, ws, A16, None) == B.IDB_ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(f=None), B.IDB_ERR_INVALID_ARG),
+    (dict(P=None), B.IDB_ERR_INVALID_ARG),
+    (dict(loss=None), B.IDB_ERR_INVALID_ARG),
+    (dict(loss=A16 + 4), B.IDB_ERR_INVALID_ARG),          # fp64 output misaligned
+    (dict(stats=A16 + 4), B.IDB_ERR_INVALID_ARG),
+    (dict(variant=1), B.IDB_ERR_UNSUPPORTED),             # one slice at E <= 384, but no softmax mode
+    (dict(alpha=float("inf")), B.IDB_ERR_INVALID_ARG),
+    (dict(E=1024), B.IDB_ERR_UNSUPPORTED),                # no tiling covers 1024 experts in one slice
+    (dict(variant=6), B.IDB_ERR_UNSUPPORTED),             # two 384-expert slices
+    (dict(variant=5), B.IDB_ERR_UNSUPPORTED),             # fp32 tiling for bf16 inputs
+    (dict(dtype=B.IDB_DTYPE_F32, E=256), B.IDB_ERR_UNSUPPORTED),  # fp32 tiling covers 128 experts
+    (dict(ws_bytes=1024), B.IDB_ERR_INVALID_ARG),
+    (dict(ws=None), B.IDB_ERR_INVALID_ARG),
+    (dict(x=None), B.IDB_ERR_INVALID_ARG),
+    (dict(K=0), B.IDB_ERR_INVALID_ARG),
+    (dict(K=33), B.IDB_ERR_UNSUPPORTED),
+])
+def test_aux_router_rejects_invalid_arguments(kw, code):
+    a = dict(x=A16, W=A16, dtype=B.IDB_DTYPE_BF16, T=128, d=256, E=768, K=10, alpha=0.05, f=A16, P=A16, loss=A16,
+             stats=None, ws=A16, ws_bytes=1 << 30, variant=0)
+    a.update(kw)
+    st = B.lib().idb_aux_router_forward(a["x"], a["W"], a["dtype"], 0, a["T"], a["d"], a["E"], a["K"], a["alpha"],
+                                        A16, A16, A16, a["f"], a["P"], a["loss"], a["stats"], None, a["ws"],
+                                        a["ws_bytes"], a["variant"], None)
+    assert st == code
+    assert B.idb_last_error() != ""
+
+
+def test_aux_workspace_and_tiling():
+    # one-slice tilings only: 64 tokens x 768 experts per workgroup at the headline shape
+    T, E = 16384, 768
+    n = B.idb_aux_router_workspace_bytes(T, 2048, E, 10, B.IDB_DTYPE_BF16, 0)
+    assert n >= 2 * (T // 64) * E * 4 + 16 * 24 + 4
+    assert B.idb_aux_router_workspace_bytes(T, 2048, E, 10, B.IDB_DTYPE_BF16, 6) == 0
+    assert B.idb_aux_router_workspace_bytes(T, 2048, 1024, 10, B.IDB_DTYPE_BF16, 0) == 0
+    assert B.idb_aux_router_workspace_bytes(4096, 256, 64, 4, B.IDB_DTYPE_F32, 0) >= 32 * 64 * 4
