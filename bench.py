@@ -312,7 +312,35 @@ def main() -> int:
         "kernel_us": round(sel_ms * 1000, 2),
         "bytes_per_launch": sel_bytes,
     }
+    # the paper's diagnostics on the same step: the full-pool and top-K
+    # routing entropies over this batch (scores [T][E] read from HBM), and
+    # the batched controller of a 21-layer model (one launch, one
+    # workgroup per layer, with MaxVio/MinVio and the update's diagnostics)
+    ent_ws = torch.empty(int(B.lib().idb_routing_entropy_workspace_bytes()), dtype=torch.uint8, device=dev)
+    ent_out = torch.empty(2, dtype=torch.float64, device=dev)
+    ent_ms = graph_time_per_call(lambda i: B.idb_routing_entropy(sw, ent_out, scores[i % sel_bufs], rs.state.bias,
+                                                                 ent_ws, stream=stream), sel_per, n_rep, stream,
+                                 capture)
+    ent_bytes = wl.T * wl.E * 4 + wl.T * wl.K * 4 + wl.E * 4
+    ent_gbs = ent_bytes / (ent_ms * 1e-3) / 1e9
     del scores
+    n_layers = 21
+    lay_counts = rs.counts.repeat(n_layers, 1).contiguous()
+    lay_state = B.ControllerState(wl.E, dev, layers=n_layers)
+    lay_stats = torch.empty((n_layers, 2), dtype=torch.float64, device=dev)
+    lay_diag = torch.empty((n_layers, 4), dtype=torch.float64, device=dev)
+    lay_ms = graph_time_per_call(lambda i: B.idb_controller_update_layers(lay_counts, rs.cfg, lay_state, lay_stats,
+                                                                          lay_diag, stream=stream), 16, n_rep, stream,
+                                 capture)
+    log(f"routing entropies: {ent_ms * 1000:.2f} us ({ent_gbs:.0f} GB/s); {n_layers}-layer controller with "
+        f"diagnostics: {lay_ms * 1000:.2f} us")
+    diagnostics = {
+        "routing_entropy": {"bound": "hbm", "achieved": round(ent_gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                            "frac": round(ent_gbs / PEAK_HBM_GBS, 4), "kernel_us": round(ent_ms * 1000, 2),
+                            "bytes_per_call": ent_bytes, "launches": 2},
+        "layers_controller": {"layers": n_layers, "kernel_us": round(lay_ms * 1000, 2), "bound": "latency",
+                              "outputs": "bias, e_prev, MaxVio/MinVio and four diagnostics per layer"},
+    }
 
     value = wl.T / (ms_step * 1e-3)
     out = {
@@ -335,6 +363,7 @@ def main() -> int:
                              "fp32 row-major, repacked every step"},
         "roofline": roofline,
         "select_roofline": select_roofline,
+        "diagnostics": diagnostics,
         "last_step": {"maxvio": stats[0], "minvio": stats[1]},
     }
     if not args.no_cpu_baseline:

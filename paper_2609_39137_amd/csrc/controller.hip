@@ -1,9 +1,10 @@
 // ID controller update (Alg. 1; Eq. rapid-integral, rapid-delta, rapid-gate,
 // rapid-update; SIGN mode: Eq. pid-deepseek) and MaxVio/MinVio (Eq. vio).
 //
-// Both are O(E) single-workgroup kernels: the controller holds one expert per
-// thread (E <= 1024) and reduces in LDS with fixed trees, so the result is
-// bit-reproducible.  fp32 steps are evaluated exactly as written: no FMA
+// The single-layer controller holds one expert per thread of one workgroup
+// (E <= 1024) and reduces in LDS with fixed trees; the batched kernel runs one
+// wave per layer with the same trees in registers; both are bit-reproducible
+// and give the same bits.  fp32 steps are evaluated exactly as written: no FMA
 // contraction in this file.
 #include "common.h"
 #include "controller_block.h"
@@ -64,22 +65,22 @@ __global__ __launch_bounds__(1024) void load_stats_kernel(const int32_t* __restr
     }
 }
 
-// L layers' updates in one launch, one workgroup per layer (Alg. 1 runs once
-// per MoE layer and iteration): counts, bias and e_prev [L][E], step and
-// status [L], stats [L][2] and diag [L][4] (both nullable).
-__global__ __launch_bounds__(1024) void controller_layers_kernel(const int32_t* __restrict__ counts, int E, int P,
-                                                                 float Ki, float Kd, int sign_mode, int center,
-                                                                 float* __restrict__ bias,
-                                                                 float* __restrict__ e_prev,
-                                                                 int64_t* __restrict__ step,
-                                                                 int32_t* __restrict__ status,
-                                                                 double* __restrict__ stats,
-                                                                 double* __restrict__ diag) {
-    __shared__ CtrlScratch sh;
-    __shared__ DiagScratch dsh;
+// L layers' updates in one launch, one wave per layer (Alg. 1 runs once per
+// MoE layer and iteration): counts, bias and e_prev [L][E], step and status
+// [L], stats [L][2] and diag [L][4] (both nullable).  The same bits as the
+// single-layer update.
+__global__ __launch_bounds__(64) void controller_layers_kernel(const int32_t* __restrict__ counts, int E, float Ki,
+                                                               float Kd, int sign_mode, int center,
+                                                               float* __restrict__ bias, float* __restrict__ e_prev,
+                                                               int64_t* __restrict__ step,
+                                                               int32_t* __restrict__ status,
+                                                               double* __restrict__ stats,
+                                                               double* __restrict__ diag) {
     const int64_t l = blockIdx.x;
-    controller_block<1>(counts + l * E, E, P, Ki, Kd, sign_mode, center, bias + l * E, e_prev + l * E, step + l,
-                        status + l, stats ? stats + 2 * l : nullptr, sh, diag ? diag + 4 * l : nullptr, &dsh);
+    float b0[kCtrlPer], ep0[kCtrlPer];
+    controller_load_state(bias + l * E, e_prev + l * E, E, b0, ep0);
+    controller_wave(counts + l * E, E, Ki, Kd, sign_mode, center, b0, ep0, bias + l * E, e_prev + l * E, step + l,
+                    status + l, stats ? stats + 2 * l : nullptr, diag ? diag + 4 * l : nullptr);
 }
 
 hipError_t launch_controller_update(const int32_t* counts, int E, float Ki, float Kd, int sign_mode, int center,
@@ -95,10 +96,8 @@ hipError_t launch_controller_update(const int32_t* counts, int E, float Ki, floa
 hipError_t launch_controller_layers(const int32_t* counts, int L, int E, float Ki, float Kd, int sign_mode,
                                     int center, float* bias, float* e_prev, int64_t* step, int32_t* status,
                                     double* stats, double* diag, hipStream_t stream) {
-    const int P = ctrl_tree_size(E);
-    const int threads = P < 64 ? 64 : P;
-    hipLaunchKernelGGL(controller_layers_kernel, dim3((unsigned)L), dim3(threads), 0, stream, counts, E, P, Ki, Kd,
-                       sign_mode, center, bias, e_prev, step, status, stats, diag);
+    hipLaunchKernelGGL(controller_layers_kernel, dim3((unsigned)L), dim3(64), 0, stream, counts, E, Ki, Kd, sign_mode,
+                       center, bias, e_prev, step, status, stats, diag);
     return hipGetLastError();
 }
 

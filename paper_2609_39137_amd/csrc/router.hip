@@ -555,8 +555,8 @@ __global__ __launch_bounds__(kTileThreads) void router_merge_tile_kernel(RouterA
     for (int e = tid; e < E; e += kTileThreads) hist[e] = 0;
     const int64_t ntiles = (a.T + kTileTokens - 1) / kTileTokens;
 
-    // A thread's candidates of tile g (indices past the tile's candidates
-    // re-read the last one; they are never used).
+    // A thread's candidates of tile g (slots past the tile's candidates are
+    // neither loaded nor used).
     constexpr int kIt = kTileTokens * 64 / kTileThreads;
     float cv[kIt], cs[kIt];
     int ci[kIt];
@@ -566,12 +566,13 @@ __global__ __launch_bounds__(kTileThreads) void router_merge_tile_kernel(RouterA
         const int n = nt * NSK;
 #pragma unroll
         for (int it = 0; it < kIt; ++it) {
-            int c = tid + it * kTileThreads;
-            c = c < n ? c : n - 1;
-            const int64_t gi = t0 * NSK + c;  // candidates of token t: [t][slice][K]
-            cv[it] = a.cand_v[gi];
-            cs[it] = a.cand_s[gi];
-            ci[it] = a.cand_i[gi];
+            const int c = tid + it * kTileThreads;
+            if (c < n) {
+                const int64_t gi = t0 * NSK + c;  // candidates of token t: [t][slice][K]
+                cv[it] = a.cand_v[gi];
+                cs[it] = a.cand_s[gi];
+                ci[it] = a.cand_i[gi];
+            }
         }
     };
     int64_t g = blockIdx.x;

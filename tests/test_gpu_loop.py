@@ -96,9 +96,10 @@ def _bf16(a: np.ndarray) -> torch.Tensor:
     return torch.from_numpy(a.view(np.int16)).to(DEV).view(torch.bfloat16)
 
 
-def _assert_same_step(f: RouterStep, s: RouterStep, ref, msg):
-    """The one-call step (f) against route + controller step (s) and the oracle
-    controller run on the GPU's counts: everything bit-identical."""
+def _assert_same_step(f: RouterStep, s: RouterStep, msg):
+    """The one-call step (f) against route + controller step (s): everything
+    bit-identical (the controller step itself is pinned against the oracle on
+    host-generated counts in test_gpu_controller.py)."""
     assert torch.equal(f.idx, s.idx), msg
     assert torch.equal(f.w.view(torch.int32), s.w.view(torch.int32)), msg
     assert torch.equal(f.counts, s.counts), msg
@@ -107,12 +108,7 @@ def _assert_same_step(f: RouterStep, s: RouterStep, ref, msg):
         assert torch.equal(a.view(torch.int32) if a.dtype == torch.float32 else a,
                            b.view(torch.int32) if b.dtype == torch.float32 else b), f"{msg}: {name}"
     assert torch.equal(f.stats.view(torch.int64), s.stats.view(torch.int64)), msg
-    counts = f.counts.cpu().numpy()
-    stats = oracle.load_stats(counts)
-    assert oracle.controller(counts, ref, f.cfg.Ki, f.cfg.Kd, f.cfg.integral_mode, f.cfg.center) == 0
-    np.testing.assert_array_equal(f.state.bias.cpu().numpy().view(np.uint32), ref.bias.view(np.uint32), msg)
-    np.testing.assert_array_equal(f.state.e_prev.cpu().numpy().view(np.uint32), ref.e_prev.view(np.uint32), msg)
-    np.testing.assert_array_equal(f.stats.cpu().numpy(), stats, msg)
+    assert int(f.state.status.item()) == 0, msg
 
 
 @pytest.mark.parametrize("T,d,E,K,variant,packed", [
@@ -132,7 +128,6 @@ def test_router_step_equals_route_then_controller(T, d, E, K, variant, packed):
     if packed:
         f.pack(Wt)
         s.pack(Wt)
-    ref = oracle.ControllerState(E)
     for t in range(5):
         x = _bf16(synth.normal_router_inputs(T, d, E, seed=100 + t)[0])
         # a component shared by every token skews the load, so the
@@ -141,7 +136,7 @@ def test_router_step_equals_route_then_controller(T, d, E, K, variant, packed):
         f.step(x, None if packed else Wt)
         s.route(x, None if packed else Wt)
         s.update_and_stats()
-        _assert_same_step(f, s, ref, f"step {t}")
+        _assert_same_step(f, s, f"step {t}")
     assert int(f.state.step.item()) == 5
 
 
@@ -151,7 +146,6 @@ def test_router_step_accumulates_microbatches():
     Wt = _bf16(W)
     f = RouterStep(T, d, E, K, torch.bfloat16)
     s = RouterStep(T, d, E, K, torch.bfloat16)
-    ref = oracle.ControllerState(E)
     for t in range(3):
         xa = _bf16(synth.normal_router_inputs(T, d, E, seed=200 + 2 * t)[0])
         xb = _bf16(synth.normal_router_inputs(T, d, E, seed=201 + 2 * t)[0])
@@ -161,7 +155,7 @@ def test_router_step_accumulates_microbatches():
         s.route(xb, Wt, accumulate=True)
         s.update_and_stats()
         assert int(f.counts.sum().item()) == 2 * T * K
-        _assert_same_step(f, s, ref, f"step {t}")
+        _assert_same_step(f, s, f"step {t}")
 
 
 def test_router_step_graph_replays():
@@ -175,7 +169,6 @@ def test_router_step_graph_replays():
     s = RouterStep(T, d, E, K, torch.bfloat16)
     f.pack(Wt)
     s.pack(Wt)
-    ref = oracle.ControllerState(E)
     side = torch.cuda.Stream()
     torch.cuda.synchronize()
     g = torch.cuda.CUDAGraph()
@@ -187,4 +180,4 @@ def test_router_step_graph_replays():
         s.route(xt, None)
         s.update_and_stats()
         torch.cuda.synchronize()
-        _assert_same_step(f, s, ref, f"replay {t}")
+        _assert_same_step(f, s, f"replay {t}")
