@@ -80,6 +80,13 @@ def cpu_baseline(wl, W, target_s: float):
     total = 0.0
     for _ in range(reps):
         total += oracle.step_seconds(x, W, wl.K, 6e-3, 6e-3, st)
+    # one thread on 1024 tokens
+    x1 = synth.hidden_states(wl, step=0, rows=np.arange(min(1024, wl.T)))
+    oracle.set_num_threads(1)
+    try:
+        t1 = oracle.step_seconds(x1, W, wl.K, 6e-3, 6e-3, oracle.ControllerState(wl.E))
+    finally:
+        oracle.set_num_threads(threads)
     return {
         "value": n * reps / total,
         "unit": "routed tokens/s",
@@ -88,14 +95,28 @@ def cpu_baseline(wl, W, target_s: float):
         "sample": f"{reps} oracle steps (router + ID update + MaxVio/MinVio, controller state carried over) on the "
                   f"first {n} of the {wl.T} tokens of batch 0 of {wl.name}: {total:.2f} s wall on {threads} "
                   f"OpenMP threads",
+        "cpu_model": cpu_model(),
+        "single_thread_value": round(len(x1) / t1, 1),
+        "single_thread_sample": f"one oracle step on the first {len(x1)} tokens, one thread",
     }
+
+
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
 
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
-    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=200)
     ap.add_argument("--workload", default=None, help="synthetic workload name (default: the Top-10-of-768 shape)")
     ap.add_argument("--variant", type=int, default=0, help="router tiling (0 = automatic)")
     ap.add_argument("--buffers", type=int, default=0, help="distinct hidden-state buffers to rotate (0 = auto)")
@@ -227,6 +248,18 @@ def main() -> int:
     ms_total = ev0.elapsed_time(ev1)
     ms_step = ms_total / args.steps
     log(f"timed {args.steps} steps: {ms_step * 1000:.2f} us/step")
+    # spread: 5 more timed blocks of 100 steps each (outside the timed region above)
+    reps_us = []
+    for _ in range(5):
+        torch.cuda.synchronize()
+        ev0.record(stream)
+        run_steps(100)
+        ev1.record(stream)
+        torch.cuda.synchronize()
+        reps_us.append(ev0.elapsed_time(ev1) * 1000 / 100)
+    spread = {"blocks": 5, "steps_per_block": 100, "p10": round(float(np.percentile(reps_us, 10)), 2),
+              "median": round(float(np.median(reps_us)), 2), "p90": round(float(np.percentile(reps_us, 90)), 2),
+              "unit": "us/step"}
 
     # sanity of the last step's outputs
     counts = rs.counts.cpu()
@@ -234,9 +267,9 @@ def main() -> int:
     assert int(rs.state.status.item()) == 0
     stats = rs.stats.cpu().tolist()
     if qb:
-        return qb_report(args, wl, rs, xs, nbuf, stream, capture, ms_step, stats)
+        return qb_report(args, wl, rs, xs, nbuf, stream, capture, ms_step, stats, spread)
     if aux:
-        return aux_report(args, wl, rs, xs, nbuf, stream, capture, ms_step, stats)
+        return aux_report(args, wl, rs, xs, nbuf, stream, capture, ms_step, stats, spread)
 
     # live timing of the dominant kernel: back-to-back launches of the fused
     # router kernel alone, on the stream the steps run on, between HIP events
@@ -364,6 +397,8 @@ def main() -> int:
         "roofline": roofline,
         "select_roofline": select_roofline,
         "diagnostics": diagnostics,
+        "step_spread": spread,
+        "assignments_per_s": round(wl.T * wl.K / (ms_step * 1e-3), 1),
         "last_step": {"maxvio": stats[0], "minvio": stats[1]},
     }
     if not args.no_cpu_baseline:
@@ -392,7 +427,7 @@ def graph_time_per_call(fn, per, reps, stream, capture):
     return e0.elapsed_time(e1) / (reps * per)
 
 
-def aux_report(args, wl, rs, xs, nbuf, stream, capture, ms_step, stats) -> int:
+def aux_report(args, wl, rs, xs, nbuf, stream, capture, ms_step, stats, spread) -> int:
     """JSON line of the auxiliary-loss statistics step (softmax router + f, P, loss; MaxVio/MinVio)."""
     from paper_2609_39137_amd import binding as B
 
@@ -435,12 +470,13 @@ def aux_report(args, wl, rs, xs, nbuf, stream, capture, ms_step, stats) -> int:
                                "column sums) + the statistics kernel",
                      "kernel_us": round(route_ms * 1000, 2), "flops_per_launch": wl.flops},
         "last_step": {"maxvio": stats[0], "minvio": stats[1], "aux_loss": loss},
+        "step_spread": spread,
     }
     print(json.dumps(out), flush=True)
     return 0
 
 
-def qb_report(args, wl, rs, xs, nbuf, stream, capture, ms_step, stats) -> int:
+def qb_report(args, wl, rs, xs, nbuf, stream, capture, ms_step, stats, spread) -> int:
     """JSON line of the Quantile Balancing step (router in its QB mode, MaxVio/MinVio, the update)."""
     import torch
 
@@ -496,6 +532,7 @@ def qb_report(args, wl, rs, xs, nbuf, stream, capture, ms_step, stats) -> int:
                                "frac": round(upd_gbs / PEAK_HBM_GBS, 4), "kernel": "qb_update_kernel",
                                "kernel_us": round(upd_ms * 1000, 2), "bytes_per_launch": upd_bytes},
         "last_step": {"maxvio": stats[0], "minvio": stats[1]},
+        "step_spread": spread,
     }
     print(json.dumps(out), flush=True)
     return 0

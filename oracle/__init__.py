@@ -76,6 +76,7 @@ def _declare(lib):
     P = ctypes.c_void_p
     i64, i32, f32, c_int = ctypes.c_int64, ctypes.c_int32, ctypes.c_float, ctypes.c_int
     lib.oracle_num_threads.restype = c_int
+    lib.oracle_set_num_threads.argtypes = [c_int]
     lib.oracle_router_scores.argtypes = [P, P, c_int, i64, i32, i32, P, i64, P, P]
     lib.oracle_select.argtypes = [P, P, i64, i32, i32, P, P, P, c_int]
     lib.oracle_router.argtypes = [P, P, c_int, P, i64, i32, i32, i32, P, P, P, c_int, P]
@@ -110,6 +111,11 @@ def _dtype_code(x: np.ndarray) -> int:
 
 def num_threads() -> int:
     return int(_load().oracle_num_threads())
+
+
+def set_num_threads(n: int) -> None:
+    """Threads of the oracle's OpenMP loops from now on (timing only)."""
+    _load().oracle_set_num_threads(int(n))
 
 
 def router_scores(x: np.ndarray, W: np.ndarray, rows: np.ndarray | None = None, want_z: bool = False):

@@ -107,6 +107,15 @@ int oracle_num_threads(void) {
 #endif
 }
 
+/* Threads of the following OpenMP loops (timing a single-thread rate). */
+void oracle_set_num_threads(int n) {
+#ifdef _OPENMP
+    omp_set_num_threads(n);
+#else
+    (void)n;
+#endif
+}
+
 /* Exact widening of one input element to double.  bf16 is the upper half of
  * an IEEE binary32, so shifting its 16 bits up gives the same value. */
 static double load_elem(const void* base, int dtype, int64_t i) {

@@ -5,6 +5,9 @@ Two commands, both run on the CPU over files a profiled run wrote:
 ``stats``: a ``*_kernel_stats.csv`` of ``rocprofv3 --kernel-trace --stats``
 becomes a short markdown table (calls, average/min/max duration, share).
 
+``counters``: per-dispatch means of the fused router kernel's counters from
+one ``--pmc`` pass (MFMA busy cycles, wait cycles, LDS bank conflicts).
+
 ``traffic``: the ``*_counter_collection.csv`` of a ``FETCH_SIZE`` pass and of
 a ``WRITE_SIZE`` pass over ``bench.py --pmc-pass`` become the HBM bytes per
 launch of the fused router kernel.  Both counters are read in KiB per
@@ -109,6 +112,35 @@ def traffic(args) -> None:
                       "write_factor": w["factor"]}))
 
 
+def counters(args) -> None:
+    """Per-dispatch means of the fused router kernel's counters in one --pmc pass."""
+    per = {}
+    for r in csv.DictReader(open(args.csv)):
+        if _is_router(r["Kernel_Name"]):
+            per.setdefault(r["Counter_Name"], {}).setdefault(r["Dispatch_Id"], 0.0)
+            per[r["Counter_Name"]][r["Dispatch_Id"]] += float(r["Counter_Value"])
+    if not per:
+        raise SystemExit(f"{args.csv}: no readings for the router kernel")
+    mean = {c: statistics.mean(v.values()) for c, v in per.items()}
+    n = max(len(v) for v in per.values())
+    md = [f"# {args.title}", "", "Command:", "", "```", args.cmd, "```", "",
+          f"Per-dispatch values (mean over {n} dispatches of the fused router kernel), summed over the chip.", "",
+          "| counter | per dispatch |", "|---|---:|"]
+    for c in sorted(mean):
+        md.append(f"| {c} | {mean[c]:.4g} |")
+    if "SQ_VALU_MFMA_BUSY_CYCLES" in mean and "SQ_INSTS_VALU_MFMA_MOPS_BF16" not in mean:
+        md += ["", f"MFMA busy cycles per SIMD ({args.simds} SIMDs): "
+               f"{mean['SQ_VALU_MFMA_BUSY_CYCLES'] / args.simds:.4g}"]
+    if "SQ_WAIT_INST_ANY" in mean and "SQ_WAVE_CYCLES" in mean:
+        md.append(f"Share of wave cycles waiting for an instruction to issue: "
+                  f"{mean['SQ_WAIT_INST_ANY'] / mean['SQ_WAVE_CYCLES']:.3f}")
+    if "SQ_WAIT_INST_LDS" in mean and "SQ_WAVE_CYCLES" in mean:
+        md.append(f"Share of wave cycles waiting on LDS: {mean['SQ_WAIT_INST_LDS'] / mean['SQ_WAVE_CYCLES']:.3f}")
+    md.append("")
+    with open(args.out, "w") as fh:
+        fh.write("\n".join(md))
+
+
 def main(argv=None) -> int:
     ap = argparse.ArgumentParser()
     sub = ap.add_subparsers(dest="action", required=True)
@@ -126,10 +158,18 @@ def main(argv=None) -> int:
     b.add_argument("--cmd-fetch", required=True)
     b.add_argument("--cmd-write", required=True)
     b.add_argument("--out", required=True, help="output path without extension (.json and .md are written)")
+    c = sub.add_parser("counters")
+    c.add_argument("csv")
+    c.add_argument("--cmd", required=True)
+    c.add_argument("--title", default="Hardware counters")
+    c.add_argument("--simds", type=int, default=1024)
+    c.add_argument("--out", required=True)
     args = ap.parse_args(argv)
     if args.action == "stats":
         with open(args.out, "w") as fh:
             fh.write(stats_markdown(args.csv, args.cmd, args.title))
+    elif args.action == "counters":
+        counters(args)
     else:
         traffic(args)
     return 0
