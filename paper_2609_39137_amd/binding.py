@@ -259,6 +259,23 @@ class ControllerState:
     def c(self) -> idb_controller_state:
         return idb_controller_state(_ptr(self.bias), _ptr(self.e_prev), _ptr(self.step), _ptr(self.status))
 
+    _FIELDS = ("bias", "e_prev", "step", "status")
+
+    def state_dict(self) -> dict:
+        """Host copies of the full controller state (bias, e_prev, step, status; Alg. 1): a checkpoint.
+        Synchronises with the device; restoring it continues the trajectory bit for bit."""
+        return {k: getattr(self, k).detach().to("cpu", copy=True) for k in self._FIELDS}
+
+    def load_state_dict(self, d: dict) -> None:
+        """Restore a :meth:`state_dict` (same shapes and dtypes; copied into the existing device buffers, so
+        pointers held elsewhere, e.g. by captured graphs, stay valid)."""
+        for k in self._FIELDS:
+            src, dst = d[k], getattr(self, k)
+            if tuple(src.shape) != tuple(dst.shape) or src.dtype != dst.dtype:
+                raise ValueError(f"{k}: expected {tuple(dst.shape)} {dst.dtype}, got {tuple(src.shape)} {src.dtype}")
+        for k in self._FIELDS:
+            getattr(self, k).copy_(d[k])
+
 
 def idb_controller_update(counts, cfg: ControllerCfg, state: ControllerState, stream=None):
     """One ID controller update of ``state`` from ``counts`` on ``stream``."""

@@ -321,3 +321,26 @@ def test_aux_workspace_and_tiling():
     assert B.idb_aux_router_workspace_bytes(T, 2048, E, 10, B.IDB_DTYPE_BF16, 6) == 0
     assert B.idb_aux_router_workspace_bytes(T, 2048, 1024, 10, B.IDB_DTYPE_BF16, 0) == 0
     assert B.idb_aux_router_workspace_bytes(4096, 256, 64, 4, B.IDB_DTYPE_F32, 0) >= 32 * 64 * 4
+
+
+def test_controller_state_dict_round_trip():
+    # host-side checkpoint helpers (no kernel runs): exact bits, shape checks
+    import torch
+    a = B.ControllerState(768, "cpu", layers=3)
+    a.bias.copy_(torch.linspace(-1, 1, 3 * 768).view(3, 768))
+    a.bias[0, 5] = -0.0
+    a.e_prev.fill_(0.25)
+    a.step.fill_(7)
+    a.status.fill_(3)
+    d = a.state_dict()
+    b = B.ControllerState(768, "cpu", layers=3)
+    ptr = b.bias.data_ptr()
+    b.load_state_dict(d)
+    assert b.bias.data_ptr() == ptr  # restored in place
+    for k in ("bias", "e_prev", "step", "status"):
+        x, y = getattr(a, k), getattr(b, k)
+        assert torch.equal(x.view(torch.int32) if x.dtype == torch.float32 else x,
+                           y.view(torch.int32) if y.dtype == torch.float32 else y)
+    d["bias"] = d["bias"][:2]
+    with pytest.raises(ValueError, match="bias"):
+        b.load_state_dict(d)

@@ -92,10 +92,9 @@ def test_state_checkpoint_restore_continues_identically():
     a = B.ControllerState(E, DEV)
     for n in stream[:10]:
         B.idb_controller_update(torch.from_numpy(n).to(DEV), cfg, a)
-    saved = {k: getattr(a, k).cpu().clone() for k in ("bias", "e_prev", "step", "status")}
+    saved = a.state_dict()
     b = B.ControllerState(E, DEV)
-    for k, v in saved.items():
-        getattr(b, k).copy_(v.to(DEV))
+    b.load_state_dict(saved)
     for n in stream[10:]:
         c = torch.from_numpy(n).to(DEV)
         B.idb_controller_update(c, cfg, a)
