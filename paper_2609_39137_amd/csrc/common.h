@@ -43,6 +43,15 @@ __device__ __forceinline__ float rank_key_value(unsigned long long key) {
     return __uint_as_float((o & 0x80000000u) ? (o & 0x7fffffffu) : ~o);
 }
 
+// Orders a wave's LDS writes before the same wave's later LDS reads of what
+// other lanes wrote: one wave's LDS instructions execute in issue order, so
+// only the compiler has to be kept from moving memory operations across.
+__device__ __forceinline__ void wave_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
 // Score activation s = sigmoid(z) = 1 / (1 + 2^(-z log2 e)) with the hardware
 // exp2 and reciprocal (each about 1 ulp).  Saturates to exactly 0 and 1.
 __device__ __forceinline__ float sigmoid_fast(float z) {

@@ -5,11 +5,12 @@
 //
 // The scores of TPP tokens at a time are written token-major into LDS; TPT
 // adjacent threads then own one token, each every TPT-th block of 16 experts
-// (so a wave's LDS reads of the score rows hit distinct banks).  Exact for any
-// input:
+// (so a wave's LDS reads of the score rows hit distinct banks).  A token's
+// threads share one wave, so after step A only wave-level ordering is needed
+// between the steps.  Exact for any input:
 //   A. the scores into the LDS score matrix (the caller's store_pass; padding
 //      experts -inf).
-//   B. v = fl32(s + b) into registers; 32 group maxima per token.
+//   B. v = fl32(s + b) into registers; NG <= 32 group maxima per token.
 //   C. tau = the K-th largest group maximum, <= the token's K-th largest v;
 //      each thread marks its values >= tau in a bitmask and counts them.
 //   D. A prefix over the token's threads gives write offsets; the candidates
@@ -17,8 +18,8 @@
 //   E. Candidate rank = number of list keys above it; ranks < K are the
 //      slice's selection, in rank order.
 //   F. Tokens whose list would overflow (heavy ties, large K) are resolved by
-//      one wave each: K rounds of "best key strictly below the previous pick"
-//      over the token's LDS score row.
+//      their own wave, one at a time: K rounds of "best key strictly below
+//      the previous pick" over the token's LDS score row.
 //   G. One slice: gate weights, outputs and an LDS histogram flushed with one
 //      atomic per non-zero bin.  Several slices: the slice's K candidates go
 //      to the workspace for the slice merge.
@@ -40,6 +41,7 @@ namespace idb {
 namespace {
 
 constexpr int kCap = 32;      // candidate list capacity per token and slice
+constexpr int kShortList = 16;  // lists up to this length are ranked in one unrolled sweep
 constexpr float kLog2e = 1.4426950408889634f;
 
 // exp(x) as 2^(x log2 e) with the hardware exp2 (about 1 ulp; exp(-inf) = 0).
@@ -62,7 +64,9 @@ struct EpiCfg {
     static constexpr int TPT = NT / TPP;
     static constexpr int VPT = BE / TPT;  // slice columns per thread: every TPT-th 16-column block
     static constexpr int NBL = VPT / 16;  // 16-column blocks per thread
-    static constexpr int NG = 32;         // group maxima per token
+    // group maxima per token: one per 16-column block when that makes 24 to
+    // 32 of them (a multiple of 4), else 32
+    static constexpr int NG = (TPT * NBL >= 24 && TPT * NBL <= 32 && (TPT * NBL) % 4 == 0) ? TPT * NBL : 32;
     static constexpr int GPT = NG / TPT;  // group maxima per thread
     static constexpr int GSZ = VPT / GPT;
     static constexpr int MW = (VPT + 31) / 32;          // candidate mask words
@@ -78,15 +82,13 @@ struct EpiCfg {
     static constexpr int OFF_CNT = OFF_GM + TPP * GMS * 4;
     static constexpr int OFF_LK = (OFF_CNT + TPP * CNS * 4 + 15) / 16 * 16;
     static constexpr int OFF_SI = OFF_LK + TPP * LKS * 8;
-    static constexpr int OFF_OVF = OFF_SI + TPP * LSS * 4;
-    static constexpr int OFF_HIST = OFF_OVF + 16 * 4;
+    static constexpr int OFF_HIST = OFF_SI + TPP * LSS * 4;
     static constexpr int EPI_LDS = OFF_HIST + 1024 * 4;
     static constexpr int LDS = MAIN_LDS_ > EPI_LDS ? MAIN_LDS_ : EPI_LDS;
     static_assert(NPASS * TPP == BT && TPP % 16 == 0, "passes of whole 16-token groups");
     static_assert(TPT * TPP == NT && TPT <= 16 && 16 % TPT == 0, "a token's threads share one wave");
     static_assert(VPT * TPT == BE && VPT % 16 == 0 && GSZ * GPT == VPT && GPT * TPT == NG, "columns split evenly");
     static_assert(TPP * RS * 4 <= SCORE_LDS, "score rows of a pass fit");
-    static_assert(TPP <= 16 * 32, "overflow bitmask size");
     static_assert(NT % TPP == 0, "whole token rows per thread group");
     static_assert(LDS <= 160 * 1024, "LDS of one workgroup");
 };
@@ -153,7 +155,6 @@ __device__ __forceinline__ void epi_tile(const RouterArgs& a, int NS, int slice,
     int* cnt = reinterpret_cast<int*>(smem + C::OFF_CNT);
     unsigned long long* lk = reinterpret_cast<unsigned long long*>(smem + C::OFF_LK);
     int* si = reinterpret_cast<int*>(smem + C::OFF_SI);
-    unsigned* ovf = reinterpret_cast<unsigned*>(smem + C::OFF_OVF);
     int* hist = reinterpret_cast<int*>(smem + C::OFF_HIST);
 
     const int tl = tid / C::TPT, q = tid % C::TPT;  // token of the pass and part, in steps B-G
@@ -179,7 +180,6 @@ __device__ __forceinline__ void epi_tile(const RouterArgs& a, int NS, int slice,
     for (int pass = 0; pass < C::NPASS; ++pass) {
         // A. scores of the pass's tokens into the LDS score matrix
         store_pass(pass, sc);
-        if (tid < 16) ovf[tid] = 0;
         __syncthreads();
 
         // The scores also go out expert-major, [E][T] (Quantile Balancing's
@@ -226,12 +226,13 @@ __device__ __forceinline__ void epi_tile(const RouterArgs& a, int NS, int slice,
             own[g] = mx;
             gm[tl * C::GMS + q * C::GPT + g] = mx;
         }
-        __syncthreads();
+        wave_sync();
 
         // C. threshold; candidate masks and counts
-        // tau = the K-th largest of the token's 32 group maxima, i.e. the
-        // largest maximum m with #{maxima >= m} >= K (K <= 32): each thread
-        // tests its own maxima against all 32, a max over the token's lanes
+        // tau = the K-th largest of the token's NG group maxima, i.e. the
+        // largest maximum m with #{maxima >= m} >= K (for K > NG no maximum
+        // qualifies: tau = -inf and the token takes step F): each thread
+        // tests its own maxima against all NG, a max over the token's lanes
         // combines them.
         float tau = -INFINITY;
         float zmax = 0.0f, zsum = 0.0f;  // softmax mode
@@ -285,7 +286,7 @@ __device__ __forceinline__ void epi_tile(const RouterArgs& a, int NS, int slice,
             mine_n += __builtin_popcount(msk[w]);
         }
         cnt[tl * C::CNS + q] = mine_n;
-        __syncthreads();
+        wave_sync();
 
         // D. write offsets; candidate keys into the token's list
         int off = 0, n = 0;
@@ -301,9 +302,7 @@ __device__ __forceinline__ void epi_tile(const RouterArgs& a, int NS, int slice,
             gm[tl * C::GMS + 1] = 1.0f / zsum;
         }
         const bool listed = n <= kCap;
-        if (!listed) {
-            if (q == 0) atomicOr(&ovf[tl >> 5], 1u << (tl & 31));
-        } else {
+        if (listed) {
 #pragma unroll
             for (int w = 0; w < C::MW; ++w) {
                 unsigned m = msk[w];
@@ -314,12 +313,35 @@ __device__ __forceinline__ void epi_tile(const RouterArgs& a, int NS, int slice,
                     ++off;
                 }
             }
+            // short lists are padded with key 0 (below every key) to kShortList
+            for (int c = n + q; c < kShortList; c += C::TPT) lk[tl * C::LKS + c] = 0ull;
         }
-        __syncthreads();
+        wave_sync();
 
         // E. ranks of the listed candidates: thread q ranks entries q, q+TPT, ...
-        // against the n list keys, reading each list key once.
-        if (listed) {
+        // against the n list keys, reading each list key once.  When no list
+        // of the wave is longer than kShortList, one unrolled sweep over the
+        // padded kShortList keys (the padding ranks below every entry).
+        if (listed && __ballot(n > kShortList) == 0) {
+            constexpr int NSH = (kShortList + C::TPT - 1) / C::TPT;
+            unsigned long long mine[NSH];
+            int rank[NSH];
+#pragma unroll
+            for (int i = 0; i < NSH; ++i) {
+                const int c = q + C::TPT * i;
+                mine[i] = c < kShortList ? lk[tl * C::LKS + c] : 0ull;
+                rank[i] = 0;
+            }
+#pragma unroll
+            for (int o = 0; o < kShortList; ++o) {
+                const unsigned long long ko = lk[tl * C::LKS + o];
+#pragma unroll
+                for (int i = 0; i < NSH; ++i) rank[i] += (ko > mine[i]) ? 1 : 0;
+            }
+#pragma unroll
+            for (int i = 0; i < NSH; ++i)
+                if (q + C::TPT * i < n && rank[i] < KL) si[tl * C::LSS + rank[i]] = (int)~(unsigned)mine[i];
+        } else if (listed) {
             unsigned long long mine[C::NCI];
             int rank[C::NCI];
 #pragma unroll
@@ -339,39 +361,34 @@ __device__ __forceinline__ void epi_tile(const RouterArgs& a, int NS, int slice,
                 if (q + C::TPT * i < n && rank[i] < KL) si[tl * C::LSS + rank[i]] = (int)~(unsigned)mine[i];
         }
 
-        // F. overflowing tokens, one wave each (the bitmask is uniform: it was
-        // complete at the last barrier)
+        // F. this wave's overflowing tokens, one at a time by the whole wave
         {
-            int k = 0;
-            for (int word = 0; word < (C::TPP + 31) / 32; ++word) {
-                unsigned bits = ovf[word];
-                while (bits) {
-                    const int t = word * 32 + __builtin_ctz(bits);
-                    bits &= bits - 1u;
-                    if ((k++ % WAVES) != wave) continue;
-                    unsigned long long prev = ~0ull;
-                    for (int r = 0; r < KL; ++r) {
-                        unsigned long long best = 0ull;
-                        for (int c = lane; c < C::BE; c += 64) {
-                            if (sbase + c < E) {
-                                const unsigned long long kk = rank_key(sc[t * C::RS + c] + bias_s[c], sbase + c);
-                                if (kk < prev && kk > best) best = kk;
-                            }
+            unsigned long long lead = __ballot(!listed && q == 0);  // wave-uniform
+            while (lead) {
+                const int t = (wave * 64 + __builtin_ctzll(lead)) / C::TPT;
+                lead &= lead - 1ull;
+                unsigned long long prev = ~0ull;
+                for (int r = 0; r < KL; ++r) {
+                    unsigned long long best = 0ull;
+                    for (int c = lane; c < C::BE; c += 64) {
+                        if (sbase + c < E) {
+                            const unsigned long long kk = rank_key(sc[t * C::RS + c] + bias_s[c], sbase + c);
+                            if (kk < prev && kk > best) best = kk;
                         }
-#pragma unroll
-                        for (int o = 32; o >= 1; o >>= 1) {
-                            const unsigned lo = __shfl_xor((unsigned)best, o);
-                            const unsigned hi = __shfl_xor((unsigned)(best >> 32), o);
-                            const unsigned long long other = ((unsigned long long)hi << 32) | lo;
-                            best = other > best ? other : best;
-                        }
-                        prev = best;
-                        if (lane == 0) si[t * C::LSS + r] = (int)~(unsigned)best;
                     }
+#pragma unroll
+                    for (int o = 32; o >= 1; o >>= 1) {
+                        const unsigned lo = __shfl_xor((unsigned)best, o);
+                        const unsigned hi = __shfl_xor((unsigned)(best >> 32), o);
+                        const unsigned long long other = ((unsigned long long)hi << 32) | lo;
+                        best = other > best ? other : best;
+                    }
+                    prev = best;
+                    if (lane == 0) si[t * C::LSS + r] = (int)~(unsigned)best;
                 }
             }
         }
-        __syncthreads();
+        wave_sync();
 
         // G. outputs of the pass's tokens (selected scores read back from the
         // token's LDS score row)
@@ -428,6 +445,8 @@ __device__ __forceinline__ void epi_tile(const RouterArgs& a, int NS, int slice,
         if (SM && NS == 1 && a.prob_part) {
             // column sums of the pass's probabilities p = exp(z - M) / Z,
             // tokens in order; a thread owns columns tid, tid + NT, ...
+            // (every token's M and 1/Z row is complete after the barrier)
+            __syncthreads();
             const int64_t left = T - (tok0 + pass * C::TPP);
             const int rows = left < C::TPP ? (int)left : C::TPP;
 #pragma unroll
