@@ -535,7 +535,8 @@ __global__ __launch_bounds__(kMergeThreads) void router_merge_kernel(RouterArgs 
 // candidate's final rank is its position in its slice's list plus the other
 // slices' candidates above it (keys are distinct, as the experts are).  The
 // next tile's candidates are fetched into registers while the current one is
-// ranked, and the workgroup's histogram is flushed once at the end (few
+// ranked.  The workgroup's histogram is flushed once, right after its last
+// tile's ranking, so the count atomics overlap that tile's output stores (few
 // workgroups: few, spread-out flushes instead of a burst on the same
 // counters).
 constexpr int kTileThreads = 512;
@@ -548,6 +549,7 @@ __global__ __launch_bounds__(kTileThreads) void router_merge_tile_kernel(RouterA
     __shared__ float ms[kTileTokens * 64];
     __shared__ float msel[kTileTokens * kMaxK];
     __shared__ int midx[kTileTokens * kMaxK];
+    __shared__ float mden[kTileTokens];  // per token: the fp32 sum of its selected scores in rank order
     const int E = a.E, K = a.K;
     const int KL = a.alpha ? K + 1 : K;  // candidates per slice
     const int NSK = NS * KL;             // <= 64
@@ -594,8 +596,10 @@ __global__ __launch_bounds__(kTileThreads) void router_merge_tile_kernel(RouterA
         __syncthreads();
         if (NS == 2) {
             // Each slice's list is in rank order: a two-pointer merge per
-            // token (the lists hold K distinct keys each; key 0 marks an
-            // exhausted list).
+            // token (the lists hold KL distinct keys each; key 0 marks an
+            // exhausted list).  Each list's key after its head is read ahead,
+            // and the gate weights' denominator is summed in rank order on
+            // the way.
             for (int t = tid; t < ntok; t += kTileThreads) {
                 const unsigned long long* L0 = mk + t * NSK;
                 const unsigned long long* L1 = L0 + KL;
@@ -608,6 +612,7 @@ __global__ __launch_bounds__(kTileThreads) void router_merge_tile_kernel(RouterA
                     const unsigned long long k = take0 ? k0 : k1;
                     msel[t * kMaxK + r] = take0 ? S0[p0] : S1[p1];
                     midx[t * kMaxK + r] = (int)~(unsigned)k;
+                    atomicAdd(&hist[(int)~(unsigned)k], 1);
                     if (take0) {
                         ++p0;
                         k0 = p0 < KL ? L0[p0] : 0ull;
@@ -636,12 +641,22 @@ __global__ __launch_bounds__(kTileThreads) void router_merge_tile_kernel(RouterA
                 if (rank < K) {
                     msel[t * kMaxK + rank] = ms[c];
                     midx[t * kMaxK + rank] = (int)~(unsigned)k;
+                    atomicAdd(&hist[(int)~(unsigned)k], 1);
                 } else if (rank == K && a.alpha) {
                     a.alpha[tok0 + t] = rank_key_value(k);
                 }
             }
+            __syncthreads();
+            for (int t = tid; t < ntok; t += kTileThreads) {
+                float den = 0.0f;
+                for (int j = 0; j < K; ++j) den = den + msel[t * kMaxK + j];
+                mden[t] = den;
+            }
         }
         __syncthreads();
+        // The histogram is complete after the last tile's merge: its global
+        // flush overlaps the output stores below.
+        if (g + gridDim.x >= ntiles) flush_hist(hist, a.counts, E);
         // gate weights: den is the fp32 sum of the selected unbiased scores
         // in rank order
         for (int c = tid; c < ntok * K; c += kTileThreads) {
@@ -653,11 +668,8 @@ __global__ __launch_bounds__(kTileThreads) void router_merge_tile_kernel(RouterA
             const int64_t tok = tok0 + t;
             a.idx[tok * K + r] = e;
             a.w[tok * K + r] = (den == 0.0f) ? 1.0f / (float)K : msel[t * kMaxK + r] / den;
-            atomicAdd(&hist[e], 1);
         }
     }
-    __syncthreads();
-    flush_hist(hist, a.counts, E);
     if (c.ticket) {
         __shared__ CtrlScratch csh;
         controller_tail<1024 / kTileThreads>(a.counts, E, c.Ki, c.Kd, c.sign_mode, c.center, c.bias, c.e_prev,
