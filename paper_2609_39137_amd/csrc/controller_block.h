@@ -112,9 +112,10 @@ __device__ inline void controller_block(const int32_t* __restrict__ counts, int 
         mn = min(mn, sh.w_min[w]);
         any_negative |= sh.w_neg[w];
     }
-    if (stats && i0 == 0) {
+    if (stats && i0 == nt - 1) {
         // MaxVio, MinVio (Eq. vio): one fp64 division of an exact integer
-        // numerator each; NaN for an empty batch.
+        // numerator each; NaN for an empty batch.  (The last wave: wave 0
+        // has the centering tree's serial part.)
         if (S == 0) {
             stats[0] = __builtin_nan("");
             stats[1] = __builtin_nan("");
@@ -164,30 +165,49 @@ __device__ inline void controller_block(const int32_t* __restrict__ counts, int 
             gates += g ? 1 : 0;
         }
     }
-    // Zero-mean centering (second line of Eq. rapid-update).
+    // Zero-mean centering (second line of Eq. rapid-update): the fixed
+    // pairwise tree over the P leaves (level h adds leaf j + h into leaf j for
+    // j < h).  Levels h >= nt pair two leaves of one thread (registers);
+    // levels nt/2 .. 64 pair the same lane of two waves (one LDS exchange,
+    // then wave 0 in registers); the last six run inside wave 0 by shuffles.
     float m = 0.0f;
     if (center) {
+        float v[kPer];
 #pragma unroll
-        for (int q = 0; q < kPer; ++q) {
-            const int i = i0 + q * nt;
-            if (i < P) sh.tree[i] = (i < E) ? b[q] : 0.0f;
-        }
-        __syncthreads();
-        int h = P >> 1;
-        for (; h >= 64; h >>= 1) {
-            for (int i = i0; i < h; i += nt) sh.tree[i] = sh.tree[i] + sh.tree[i + h];
+        for (int q = 0; q < kPer; ++q) v[q] = (i0 + q * nt < E) ? b[q] : 0.0f;
+#pragma unroll
+        for (int d = kPer / 2; d >= 1; d >>= 1)
+            if (2 * d * nt <= P)
+#pragma unroll
+                for (int q = 0; q < d; ++q) v[q] = v[q] + v[q + d];
+        const int NP = P < nt ? P : nt;  // tree nodes left, node i0 in thread i0
+        float a = 0.0f;
+        if (NP > 64) {
+            if (i0 < NP) sh.tree[i0] = v[0];
             __syncthreads();
+            if (wv == 0) {
+                float r[16];  // node 64 w + lane, w < NP / 64 <= 16
+#pragma unroll
+                for (int w = 0; w < 16; ++w) r[w] = (w < NP / 64) ? sh.tree[64 * w + lane] : 0.0f;
+#pragma unroll
+                for (int hw = 8; hw >= 1; hw >>= 1)
+                    if (hw < NP / 64)
+#pragma unroll
+                        for (int w = 0; w < hw; ++w) r[w] = r[w] + r[w + hw];
+                a = r[0];
+            }
+        } else if (wv == 0) {
+            a = (lane < NP) ? v[0] : 0.0f;
         }
         if (wv == 0) {
-            float a = (lane < P) ? sh.tree[lane] : 0.0f;
-            for (; h >= 1; h >>= 1) {
+            for (int h = (NP < 64 ? NP : 64) >> 1; h >= 1; h >>= 1) {
                 const float up = __shfl_down(a, h);
                 if (lane < h) a = a + up;
             }
-            if (lane == 0) sh.tree[0] = a;
+            if (lane == 0) sh.tree[1024 - 1] = a;  // a slot no other thread reads before the barrier
         }
         __syncthreads();
-        m = sh.tree[0] / (float)E;
+        m = sh.tree[1024 - 1] / (float)E;
     }
 #pragma unroll
     for (int q = 0; q < kPer; ++q) {
