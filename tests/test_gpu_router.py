@@ -235,6 +235,23 @@ def test_tied_scores_fall_back_exactly():
     np.testing.assert_array_equal(c, r_c)
 
 
+def test_overflowing_and_listed_tokens_share_waves():
+    # every third token has x = 0, so all of its scores tie at 0.5 and its
+    # candidate list overflows, while its neighbours in the same wave take
+    # the list path; integer inputs keep every logit exact on both sides.
+    T, d, E, K = 400, 256, 768, 10
+    x, W = synth.integer_router_inputs(T, d, E, seed=31, dtype="bf16", w_shift=6)
+    x = x.copy()
+    x[::3] = 0
+    b = np.zeros(E, np.float32)
+    idx, w, c, s = run_router(x, W, b, K)
+    r_idx, r_w, r_c = oracle.router(x, W, b, K)
+    np.testing.assert_array_equal(idx, r_idx)
+    np.testing.assert_array_equal(c, r_c)
+    np.testing.assert_allclose(w, r_w, rtol=2e-5)
+    assert np.all(idx[::3] == np.arange(K)[None, :])
+
+
 def test_bias_steers_selection_but_not_weights():
     T, d, E, K = 256, 256, 768, 10
     x, W = synth.normal_router_inputs(T, d, E, seed=8, w_std=0.05)

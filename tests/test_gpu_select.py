@@ -53,6 +53,16 @@ def test_all_equal_scores_take_lowest_indices():
         assert np.all(idx == np.arange(K)[None, :])
 
 
+def test_overflowing_and_listed_tokens_share_waves():
+    # constant rows (every score tied: the list overflows) between rows of
+    # distinct scores, so both paths run inside one wave
+    s = synth.scores(200, 768, "beta", seed=12)
+    s[::4] = np.float32(0.25)
+    b = np.zeros(768, np.float32)
+    for K in (1, 10, 32):
+        check(s, b, K)
+
+
 def test_headline_shape_full_size():
     s = synth.scores(16384, 768, "beta", seed=1)
     b = synth.bias(768, "small", seed=2)
