@@ -541,7 +541,6 @@ __global__ __launch_bounds__(kMergeThreads) void router_merge_kernel(RouterArgs 
 // counters).
 constexpr int kTileThreads = 512;
 constexpr int kTileTokens = 128;
-constexpr int kTileBlocks = 4096;
 
 __global__ __launch_bounds__(kTileThreads) void router_merge_tile_kernel(RouterArgs a, int NS, CtrlArgs c) {
     __shared__ int hist[1024];
@@ -764,8 +763,15 @@ hipError_t launch_router_merge(const RouterTiling& t, const RouterArgs& a, const
     if (ctrl) c = *ctrl;
     const int KL = a.alpha ? a.K + 1 : a.K;
     if (NS * KL <= 64) {
+        // one workgroup per CU at most (its LDS takes most of one): larger
+        // batches walk several tiles per workgroup, each next tile's
+        // candidates fetched during the current one's merge
+        int cus = 0, dev = 0;
+        if (hipGetDevice(&dev) != hipSuccess ||
+            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1)
+            cus = 256;
         int64_t blocks = (a.T + kTileTokens - 1) / kTileTokens;
-        if (blocks > kTileBlocks) blocks = kTileBlocks;
+        if (blocks > cus) blocks = cus;
         hipLaunchKernelGGL(router_merge_tile_kernel, dim3((unsigned)blocks), dim3(kTileThreads), 0, stream, a, NS,
                            c);
         return hipGetLastError();
