@@ -236,7 +236,8 @@ __device__ unsigned wave_select_reg(const unsigned* vals, unsigned n, unsigned k
 // each pass).  Otherwise, or when the list would overflow, a full radix
 // select over the registers.
 template <int NT, int R, bool VEC>
-__global__ __launch_bounds__(NT) void qb_update_reg_kernel(const float* __restrict__ scores_t,
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(NT == 512 ? 6 : 1)))
+void qb_update_reg_kernel(const float* __restrict__ scores_t,
                                                            const float* __restrict__ alpha, int64_t T, int E, int K,
                                                            float rho, float* __restrict__ bias) {
     constexpr int NW = NT / 64;
