@@ -341,7 +341,8 @@ def main() -> int:
         "peak": PEAK_HBM_GBS,
         "unit": "GB/s",
         "frac": round(sel_gbs / PEAK_HBM_GBS, 4),
-        "kernel": "select_kernel (idb_select_from_scores, fp32 scores [T][E] read from HBM)",
+        "kernel": ("select_reg_kernel" if wl.K <= 10 and wl.E % 4 == 0 else "select_kernel")
+                  + " (idb_select_from_scores, fp32 scores [T][E] read from HBM)",
         "kernel_us": round(sel_ms * 1000, 2),
         "bytes_per_launch": sel_bytes,
     }

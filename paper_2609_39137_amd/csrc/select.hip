@@ -3,15 +3,27 @@
 // (Eq. pid-error): the router step without the gate contraction, an HBM-bound
 // pass over a materialised T x E score matrix.
 //
-// A workgroup of 512 threads walks tiles of 32 tokens (grid-stride, one
-// workgroup per CU: the score rows of a tile take most of the LDS).  A tile's scores go from registers into the LDS score
-// rows of the selection epilogue (epilogue.h, one slice of BE >= E experts,
-// padding -inf); right after, the next tile's scores are loaded into the same
-// registers, so their HBM reads overlap the selection of the current tile.
-// The LDS histogram is flushed once per workgroup.
+// Two kernels:
+//  * select_reg_kernel (K <= 10, E % 4 == 0, 16-byte aligned scores): 16 lanes
+//    (one DPP row) per token, each holding every 16th float4 of the row in
+//    registers.  The K-th largest of the 16 lane maxima is a lower bound tau of
+//    the token's K-th largest biased score; only the float4 chunks whose
+//    maximum reaches tau are read again, and their values >= tau go to a short
+//    LDS list whose entries are ranked by counting.  A token whose list would
+//    overflow takes K exact argmax rounds over its registers instead.
+//  * select_kernel (every other case): a workgroup of 512 threads walks tiles
+//    of 32 tokens (grid-stride, one workgroup per CU: the score rows of a tile
+//    take most of the LDS).  A tile's scores go from registers into the LDS
+//    score rows of the selection epilogue (epilogue.h, one slice of BE >= E
+//    experts, padding -inf); right after, the next tile's scores are loaded
+//    into the same registers, so their HBM reads overlap the selection of the
+//    current tile.
+// Both flush their LDS histogram once per workgroup.
 #include "common.h"
 #include "epilogue.h"
 #include "internal.h"
+
+#include <utility>
 
 #pragma clang fp contract(off)
 
@@ -107,6 +119,265 @@ hipError_t launch_select_be(const RouterArgs& a, const float* scores, hipStream_
     return hipGetLastError();
 }
 
+
+// ---------------------------------------------------------------------------
+// Register-resident selection.
+constexpr int kRegMaxK = 10;   // largest K of this kernel
+constexpr int kRegCap = 64;    // candidate list entries per token
+
+// DPP rotation by R lanes inside each 16-lane row.
+template <int R>
+__device__ __forceinline__ unsigned row_ror(unsigned x) {
+    return (unsigned)__builtin_amdgcn_update_dpp(0, (int)x, 0x120 + R, 0xF, 0xF, false);
+}
+template <int R>
+__device__ __forceinline__ float row_rorf(float x) {
+    return __uint_as_float(row_ror<R>(__float_as_uint(x)));
+}
+
+// Number of lanes of the row whose value is strictly greater than this lane's.
+template <int... R>
+__device__ __forceinline__ int row_count_greater(float m, std::integer_sequence<int, R...>) {
+    return ((row_rorf<R + 1>(m) > m ? 1 : 0) + ...);
+}
+
+__device__ __forceinline__ float row_min(float x) {
+    x = fminf(x, row_rorf<8>(x));
+    x = fminf(x, row_rorf<4>(x));
+    x = fminf(x, row_rorf<2>(x));
+    return fminf(x, row_rorf<1>(x));
+}
+
+// Row-wide best (v, i) under (v descending, i ascending); every lane of the
+// row gets it.
+template <int R>
+__device__ __forceinline__ void row_best_step(float& v, int& i) {
+    const float ov = row_rorf<R>(v);
+    const int oi = (int)row_ror<R>((unsigned)i);
+    if (ov > v || (ov == v && oi < i)) {
+        v = ov;
+        i = oi;
+    }
+}
+__device__ __forceinline__ void row_best(float& v, int& i) {
+    row_best_step<8>(v, i);
+    row_best_step<4>(v, i);
+    row_best_step<2>(v, i);
+    row_best_step<1>(v, i);
+}
+
+__device__ __forceinline__ float f4_at(const float4& v, int q) {
+    return q == 0 ? v.x : q == 1 ? v.y : q == 2 ? v.z : v.w;
+}
+
+// Heavy ties (a candidate list that would overflow): K argmax rounds over the
+// row's biased scores in registers, by the token's 16 lanes (one DPP row, all
+// active).  Round r finds the element ranked next after the previous round's
+// (pv, pi); a lane visits its columns in ascending order, so among equal
+// values it keeps the first, i.e. the lowest index.  Not inlined: the main
+// path's register count (and occupancy) does not carry this rare path's.
+template <int NV>
+__device__ __attribute__((noinline)) void overflow_select(const float* row, const float* bias_s, unsigned vmask, int j,
+                                                          int K, int* sel_i, float* sel_s) {
+    float4 vv[NV];
+#pragma unroll
+    for (int c = 0; c < NV; ++c) {
+        vv[c] = make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY);
+        if ((vmask >> c) & 1u) {
+            const float4 s4 = *reinterpret_cast<const float4*>(row + 4 * (16 * c + j));
+            const float4 b4 = *reinterpret_cast<const float4*>(bias_s + 4 * (16 * c + j));
+            vv[c] = make_float4(s4.x + b4.x, s4.y + b4.y, s4.z + b4.z, s4.w + b4.w);
+        }
+    }
+    float pv = INFINITY;
+    int pi = -1, mine = 0;
+    for (int r = 0; r < K; ++r) {
+        float bv = -INFINITY;
+        int bi = 0x7fffffff;
+#pragma unroll
+        for (int c = 0; c < NV; ++c) {
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const float v = f4_at(vv[c], q);
+                const int i = 4 * (16 * c + j) + q;
+                const bool after = v < pv || (v == pv && i > pi);
+                if (((vmask >> c) & 1u) && after && v > bv) {
+                    bv = v;
+                    bi = i;
+                }
+            }
+        }
+        row_best(bv, bi);
+        pv = bv;
+        pi = bi;
+        if (j == r) mine = bi;
+    }
+    if (j < K) {
+        sel_i[j] = mine;
+        sel_s[j] = row[mine];
+    }
+}
+
+// NV: float4 chunks per lane (64 NV >= E).  Lane j of a token's row owns the
+// columns 4 (16 c + j) .. +3 for c < NV.
+template <int NV, int WAVES>
+__global__ __launch_bounds__(64 * WAVES) void select_reg_kernel(RouterArgs a, const float* __restrict__ scores) {
+    constexpr int BE = 64 * NV;
+    constexpr int TPB = 4 * WAVES;  // tokens per workgroup tile (4 per wave)
+    __shared__ __attribute__((aligned(16))) float bias_s[BE];
+    __shared__ int hist[BE];
+    __shared__ int cnt[TPB];
+    __shared__ unsigned long long lkey[TPB][kRegCap];
+    __shared__ float lsc[TPB][kRegCap];
+    __shared__ int sel_i[TPB][kRegMaxK];
+    __shared__ float sel_s[TPB][kRegMaxK];
+
+    const int tid = threadIdx.x;
+    const int E = a.E, K = a.K;
+    const int64_t T = a.T;
+    for (int i = tid; i < BE; i += blockDim.x) {
+        bias_s[i] = i < E ? a.bias[i] : 0.0f;
+        hist[i] = 0;
+    }
+    __syncthreads();
+
+    const int lane = tid & 63;
+    const int j = lane & 15;
+    const int slot = (tid >> 6) * 4 + (lane >> 4);  // token of the tile
+    unsigned vmask = 0;                              // chunks holding real columns
+#pragma unroll
+    for (int c = 0; c < NV; ++c) vmask |= (4 * (16 * c + j) < E ? 1u : 0u) << c;
+
+    const int64_t ntiles = (T + TPB - 1) / TPB;
+    for (int64_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
+        const int64_t t = tile * TPB + slot;
+        const bool valid = t < T;  // uniform over the row
+        const float* row = scores + (valid ? t : 0) * (int64_t)E;
+
+        float4 sv[NV];
+#pragma unroll
+        for (int c = 0; c < NV; ++c) {
+            sv[c] = make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY);
+            if (valid && ((vmask >> c) & 1u)) sv[c] = *reinterpret_cast<const float4*>(row + 4 * (16 * c + j));
+        }
+        // chunk and lane maxima of v = s + b
+        float cm[NV];
+        float m = -INFINITY;
+#pragma unroll
+        for (int c = 0; c < NV; ++c) {
+            const float4 b4 = *reinterpret_cast<const float4*>(bias_s + 4 * (16 * c + j));
+            const float v0 = sv[c].x + b4.x, v1 = sv[c].y + b4.y, v2 = sv[c].z + b4.z, v3 = sv[c].w + b4.w;
+            cm[c] = fmaxf(fmaxf(v0, v1), fmaxf(v2, v3));
+            m = fmaxf(m, cm[c]);
+        }
+        // tau = the K-th largest lane maximum: K distinct elements reach it, so
+        // every element of the top-K does.  Padding lanes (-inf) make tau -inf
+        // when fewer than K lanes hold real columns.
+        const int gt = row_count_greater(m, std::make_integer_sequence<int, 15>{});
+        const float tau = row_min(gt < K ? m : INFINITY);
+
+        unsigned cmask = 0;
+#pragma unroll
+        for (int c = 0; c < NV; ++c) cmask |= (cm[c] >= tau ? 1u : 0u) << c;
+        cmask &= valid ? vmask : 0u;
+
+        if (j == 0) cnt[slot] = 0;
+        wave_sync();
+        // candidates: the values >= tau of the marked chunks, appended to the
+        // token's list (list order is irrelevant: ranks are counted below)
+        while (__ballot(cmask != 0u) != 0) {
+            if (cmask != 0u) {
+                const int c = __ffs(cmask) - 1;
+                cmask &= cmask - 1u;
+                const int col0 = 4 * (16 * c + j);
+                const float4 s4 = *reinterpret_cast<const float4*>(row + col0);
+                const float4 b4 = *reinterpret_cast<const float4*>(bias_s + col0);
+                const float4 v4 = make_float4(s4.x + b4.x, s4.y + b4.y, s4.z + b4.z, s4.w + b4.w);
+                const int n4 = (v4.x >= tau) + (v4.y >= tau) + (v4.z >= tau) + (v4.w >= tau);
+                int p = atomicAdd(&cnt[slot], n4);
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    if (f4_at(v4, q) >= tau) {
+                        if (p < kRegCap) {
+                            lkey[slot][p] = rank_key(f4_at(v4, q), col0 + q);
+                            lsc[slot][p] = f4_at(s4, q);
+                        }
+                        ++p;
+                    }
+                }
+            }
+        }
+        wave_sync();
+
+        const int n = cnt[slot];
+        const bool over = n > kRegCap;  // uniform over the row
+        const int nl = over ? 0 : n;
+        int nmax = __builtin_amdgcn_readlane(nl, 0);
+        nmax = max(nmax, __builtin_amdgcn_readlane(nl, 16));
+        nmax = max(nmax, __builtin_amdgcn_readlane(nl, 32));
+        nmax = max(nmax, __builtin_amdgcn_readlane(nl, 48));
+        // rank of each listed candidate = the number of list keys above it;
+        // the lanes take the entries in groups of 16
+        for (int base = 0; base < nmax; base += 16) {
+            const int me = base + j;
+            const unsigned long long km = me < nl ? lkey[slot][me] : 0ull;
+            int rk = 0;
+            int e = 0;
+            for (; e + 4 <= nmax; e += 4) {
+                const unsigned long long q0 = lkey[slot][e], q1 = lkey[slot][e + 1];
+                const unsigned long long q2 = lkey[slot][e + 2], q3 = lkey[slot][e + 3];
+                rk += (e < nl && q0 > km) ? 1 : 0;
+                rk += (e + 1 < nl && q1 > km) ? 1 : 0;
+                rk += (e + 2 < nl && q2 > km) ? 1 : 0;
+                rk += (e + 3 < nl && q3 > km) ? 1 : 0;
+            }
+            for (; e < nmax; ++e) rk += (e < nl && lkey[slot][e] > km) ? 1 : 0;
+            if (me < nl && rk < K) {
+                sel_i[slot][rk] = (int)~(unsigned)km;
+                sel_s[slot][rk] = lsc[slot][me];
+            }
+        }
+
+        if (over) {
+            overflow_select<NV>(row, bias_s, vmask, j, K, &sel_i[slot][0], &sel_s[slot][0]);
+        }
+        wave_sync();
+
+        if (valid && j < K) {
+            const int idx = sel_i[slot][j];
+            const float w = gate_weight(&sel_s[slot][0], K, j);
+            a.idx[t * K + j] = idx;
+            a.w[t * K + j] = w;
+            atomicAdd(&hist[idx], 1);
+        }
+        wave_sync();
+    }
+    __syncthreads();
+    flush_hist(hist, a.counts, E);
+}
+
+// Workgroup shape: waves per workgroup and resident workgroups per CU.  Every
+// workgroup flushes its histogram with one device atomic per non-zero bin, so
+// fewer, larger workgroups issue fewer atomics.
+constexpr int kRegWaves = 16;
+constexpr int kRegWgPerCu = 1;
+
+template <int NV>
+hipError_t launch_select_reg(const RouterArgs& a, const float* scores, hipStream_t stream) {
+    constexpr int TPB = 4 * kRegWaves;
+    const int64_t ntiles = (a.T + TPB - 1) / TPB;
+    int cus = 0;
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1)
+        cus = 256;
+    // one round of workgroups over the CUs; more tiles are walked grid-stride
+    const int64_t cap = (int64_t)cus * kRegWgPerCu;
+    const int grid = (int)(ntiles < cap ? ntiles : cap);
+    hipLaunchKernelGGL((select_reg_kernel<NV, kRegWaves>), dim3(grid), dim3(64 * kRegWaves), 0, stream, a, scores);
+    return hipGetLastError();
+}
+
 }  // namespace
 
 hipError_t launch_fill_i32(int32_t* p, int32_t value, int64_t n, hipStream_t stream) {
@@ -127,6 +398,12 @@ hipError_t launch_select_from_scores(const float* scores, const float* bias, int
     a.idx = idx;
     a.w = w;
     a.counts = counts;
+    if (K <= kRegMaxK && E % 4 == 0 && (reinterpret_cast<uintptr_t>(scores) & 15) == 0) {
+        if (E <= 256) return launch_select_reg<4>(a, scores, stream);
+        if (E <= 512) return launch_select_reg<8>(a, scores, stream);
+        if (E <= 768) return launch_select_reg<12>(a, scores, stream);
+        return launch_select_reg<16>(a, scores, stream);
+    }
     if (E <= 256) return launch_select_be<256>(a, scores, stream);
     if (E <= 512) return launch_select_be<512>(a, scores, stream);
     if (E <= 768) return launch_select_be<768>(a, scores, stream);

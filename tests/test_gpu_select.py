@@ -91,3 +91,39 @@ def test_gate_weights_sum_to_one_and_ignore_bias():
     i2, w2, _ = gpu_select(g, (b + np.float32(0.5)).astype(np.float32), 10)
     np.testing.assert_array_equal(i1, i2)
     np.testing.assert_array_equal(w1, w2)
+
+
+def test_more_tiles_than_workgroups():
+    # 70001 tokens in 16-token tiles: more tiles than the launch has
+    # workgroups, so each walks several (grid-stride), ragged last tile
+    s = synth.scores(70001, 64, "beta", seed=21)
+    b = synth.bias(64, "small", seed=22)
+    check(s, b, 4)
+
+
+@pytest.mark.parametrize("E", [30, 770])
+def test_expert_count_not_multiple_of_four(E):
+    for T, K in ((129, 10), (40, 3)):
+        s = synth.scores(T, E, "grid", seed=E + K)
+        b = synth.bias(E, "small", seed=K)
+        check(s, b, K)
+
+
+def test_misaligned_score_rows():
+    # a view starting one float into the allocation: rows are not 16-byte
+    # aligned, which the register-resident kernel needs
+    T, E, K = 300, 768, 10
+    s = synth.scores(T, E, "beta", seed=31)
+    b = synth.bias(E, "small", seed=32)
+    base = torch.empty(T * E + 1, dtype=torch.float32, device=DEV)
+    st = base[1:].view(T, E)
+    st.copy_(torch.from_numpy(s))
+    assert st.data_ptr() % 16 != 0
+    idx = torch.empty((T, K), dtype=torch.int32, device=DEV)
+    w = torch.empty((T, K), dtype=torch.float32, device=DEV)
+    c = torch.empty(E, dtype=torch.int32, device=DEV)
+    B.idb_select_from_scores(st, torch.from_numpy(b).to(DEV), K, idx, w, c, accumulate=False)
+    ridx, rw, rc = oracle.select(s, b, K)
+    np.testing.assert_array_equal(idx.cpu().numpy(), ridx)
+    np.testing.assert_array_equal(w.cpu().numpy().view(np.uint32), rw.view(np.uint32))
+    np.testing.assert_array_equal(c.cpu().numpy(), rc)
