@@ -229,6 +229,22 @@ idb_status idb_router_step(const void* x, const void* W_g, idb_dtype dtype, idb_
                            int32_t accumulate_counts, double* out_maxvio_minvio, void* workspace,
                            size_t workspace_bytes, int32_t variant, hipStream_t stream);
 
+/* The second launch of idb_router_step on its own: after
+ * idb_router_score_select on the same stream, with the same shape, variant,
+ * workspace and outputs, it merges the expert slices (gate weights, counts)
+ * and, once every token is counted, writes MaxVio/MinVio (when
+ * out_maxvio_minvio is not null) and applies the ID update of state; for
+ * one-slice tilings, whose router kernel already finished the outputs, it is
+ * the controller step's launch.  idb_router_score_select (bias =
+ * state->bias) followed by idb_router_merge_step enqueues exactly the kernels
+ * of idb_router_step, with the same results, so a caller can time or overlap
+ * the two launches separately.  The controller reads counts as the merge
+ * leaves them (accumulated when score_select accumulated). */
+idb_status idb_router_merge_step(int64_t T, int32_t d, int32_t K, idb_dtype dtype, const idb_controller_cfg* cfg,
+                                 const idb_controller_state* state, int32_t* expert_idx, float* gate_w,
+                                 int32_t* counts, double* out_maxvio_minvio, void* workspace, size_t workspace_bytes,
+                                 int32_t variant, hipStream_t stream);
+
 /* ---------------------------------------------------------------------------
  * All MoE layers' controller updates of one iteration in one launch (Alg. 1
  * runs per layer; one workgroup per layer), with the load statistics and the

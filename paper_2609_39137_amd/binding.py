@@ -35,7 +35,7 @@ EXPORTED = (
     "idb_status_string", "idb_last_error", "idb_router_packed_weight_bytes", "idb_router_pack_weight",
     "idb_controller_step", "idb_router_step", "idb_qb_router_workspace_bytes", "idb_qb_router_forward",
     "idb_qb_update", "idb_controller_update_layers", "idb_routing_entropy_workspace_bytes", "idb_routing_entropy",
-    "idb_aux_router_workspace_bytes", "idb_aux_router_forward",
+    "idb_aux_router_workspace_bytes", "idb_aux_router_forward", "idb_router_merge_step",
 )
 
 
@@ -93,6 +93,9 @@ def lib() -> ctypes.CDLL:
     L.idb_router_step.argtypes = [P, P, i32, i32, i64, i32, i32, ctypes.POINTER(idb_controller_cfg),
                                   ctypes.POINTER(idb_controller_state), P, P, P, i32, P, P, sz, i32, P]
     L.idb_router_step.restype = ctypes.c_int
+    L.idb_router_merge_step.argtypes = [i64, i32, i32, i32, ctypes.POINTER(idb_controller_cfg),
+                                        ctypes.POINTER(idb_controller_state), P, P, P, P, P, sz, i32, P]
+    L.idb_router_merge_step.restype = ctypes.c_int
     L.idb_qb_router_workspace_bytes.argtypes = [i64, i32, i32, i32, i32, i32]
     L.idb_qb_router_workspace_bytes.restype = sz
     L.idb_qb_router_forward.argtypes = [P, P, i32, i32, P, i64, i32, i32, i32, P, P, P, i32, P, P, P, sz, i32, P]
@@ -322,6 +325,23 @@ def idb_router_step(x, W_g, K, cfg: ControllerCfg, state: ControllerState, exper
                                int(bool(accumulate)), _ptr(out), _ptr(workspace), ws_bytes, int(variant),
                                _stream(stream))
     _check("idb_router_step", st)
+
+
+def idb_router_merge_step(T, d, K, dtype, cfg: ControllerCfg, state: ControllerState, expert_idx, gate_w, counts,
+                          out=None, workspace=None, variant=0, stream=None):
+    """The second launch of :func:`idb_router_step`, after :func:`idb_router_score_select` on the same stream:
+    the slice merge with MaxVio/MinVio and the ID update in its last workgroup (or the controller step)."""
+    E = cfg.E
+    if expert_idx.shape != (T, K) or gate_w.shape != (T, K) or counts.shape != (E,):
+        raise ValueError("router outputs have the wrong shape")
+    if out is not None and (out.dtype != torch.float64 or out.numel() != 2):
+        raise ValueError("out must be a float64 tensor of 2 elements")
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    c_cfg, c_state = cfg.c(), state.c()
+    st = lib().idb_router_merge_step(T, d, K, int(dtype), ctypes.byref(c_cfg), ctypes.byref(c_state),
+                                     _ptr(expert_idx), _ptr(gate_w), _ptr(counts), _ptr(out), _ptr(workspace),
+                                     ws_bytes, int(variant), _stream(stream))
+    _check("idb_router_merge_step", st)
 
 
 # ---------------------------------------------------------------------------- Quantile Balancing

@@ -168,7 +168,9 @@ idb_status prepare_router(const void* x, const void* W_g, idb_dtype dtype, idb_w
     a.cand_v = need ? reinterpret_cast<float*>(ws) : nullptr;
     a.cand_s = need ? reinterpret_cast<float*>(ws + part) : nullptr;
     a.cand_i = need ? reinterpret_cast<int32_t*>(ws + 2 * part) : nullptr;
-    a.ticket = nullptr;
+    // the merge's ticket slot; the router kernel's first workgroup zeroes it,
+    // so a merge that applies the controller update may follow any router call
+    a.ticket = need ? reinterpret_cast<unsigned*>(ws + 3 * part) : nullptr;
     a.alpha = nullptr;
     a.scores_t = nullptr;
     a.softmax = aux ? 1 : 0;
@@ -334,6 +336,27 @@ idb_status controller_call(const int32_t* counts, const idb_controller_cfg* cfg,
     if (!aligned(counts, 4)) return fail(IDB_ERR_INVALID_ARG, "misaligned buffer");
     return enqueue_controller(counts, cfg, state, stats, stream);
 }
+// The second launch of idb_router_step: the slice merge whose last workgroup
+// applies the update (multi-slice tilings), or the controller step launch
+// (one-slice tilings, whose router kernel finished the counts itself).
+idb_status enqueue_merge_step(const RouterCall& c, const idb_controller_cfg* cfg, const idb_controller_state* state,
+                              double* out_maxvio_minvio, hipStream_t stream) {
+    if (!c.ticket) return enqueue_controller(c.args.counts, cfg, state, out_maxvio_minvio, stream);
+    idb::CtrlArgs k;
+    k.Ki = cfg->Ki;
+    k.Kd = cfg->Kd;
+    k.sign_mode = cfg->integral_mode == IDB_INTEGRAL_SIGN;
+    k.center = cfg->center;
+    k.bias = state->bias;
+    k.e_prev = state->e_prev;
+    k.step = state->step;
+    k.status = state->status;
+    k.stats = out_maxvio_minvio;
+    k.ticket = c.ticket;
+    return hip_result(idb::launch_router_merge(c.tiling, c.args, &k, stream), "router merge launch");
+}
+
+
 }  // namespace
 
 idb_status idb_controller_update(const int32_t* counts, const idb_controller_cfg* cfg,
@@ -358,27 +381,22 @@ idb_status idb_router_step(const void* x, const void* W_g, idb_dtype dtype, idb_
     st = prepare_router(x, W_g, dtype, weight_layout, state->bias, T, d, cfg->E, K, expert_idx, gate_w, counts,
                         accumulate_counts, nullptr, workspace, workspace_bytes, variant, true, &c);
     if (st != IDB_OK) return st;
-    if (!c.ticket) {
-        // one-slice tiling: the router kernel finishes the counts itself
-        st = enqueue_score_select(c, accumulate_counts, stream);
-        if (st != IDB_OK) return st;
-        return enqueue_controller(counts, cfg, state, out_maxvio_minvio, stream);
-    }
-    c.args.ticket = c.ticket;
     st = enqueue_score_select(c, accumulate_counts, stream);
     if (st != IDB_OK) return st;
-    idb::CtrlArgs k;
-    k.Ki = cfg->Ki;
-    k.Kd = cfg->Kd;
-    k.sign_mode = cfg->integral_mode == IDB_INTEGRAL_SIGN;
-    k.center = cfg->center;
-    k.bias = state->bias;
-    k.e_prev = state->e_prev;
-    k.step = state->step;
-    k.status = state->status;
-    k.stats = out_maxvio_minvio;
-    k.ticket = c.ticket;
-    return hip_result(idb::launch_router_merge(c.tiling, c.args, &k, stream), "router merge launch");
+    return enqueue_merge_step(c, cfg, state, out_maxvio_minvio, stream);
+}
+
+idb_status idb_router_merge_step(int64_t T, int32_t d, int32_t K, idb_dtype dtype, const idb_controller_cfg* cfg,
+                                 const idb_controller_state* state, int32_t* expert_idx, float* gate_w,
+                                 int32_t* counts, double* out_maxvio_minvio, void* workspace, size_t workspace_bytes,
+                                 int32_t variant, hipStream_t stream) {
+    idb_status st = check_controller(cfg, state, out_maxvio_minvio);
+    if (st != IDB_OK) return st;
+    RouterCall c;
+    st = prepare_router(nullptr, nullptr, dtype, IDB_WEIGHT_ROW_MAJOR, nullptr, T, d, cfg->E, K, expert_idx, gate_w,
+                        counts, 1, nullptr, workspace, workspace_bytes, variant, false, &c);
+    if (st != IDB_OK) return st;
+    return enqueue_merge_step(c, cfg, state, out_maxvio_minvio, stream);
 }
 
 size_t idb_qb_router_workspace_bytes(int64_t T, int32_t d, int32_t E, int32_t K, idb_dtype dtype,

@@ -148,34 +148,33 @@ __device__ __forceinline__ float row_min(float x) {
     return fminf(x, row_rorf<1>(x));
 }
 
-// Row-wide best (v, i) under (v descending, i ascending); every lane of the
-// row gets it.
+// Row-wide maximum of a 64-bit rank key; every lane of the row gets it.
 template <int R>
-__device__ __forceinline__ void row_best_step(float& v, int& i) {
-    const float ov = row_rorf<R>(v);
-    const int oi = (int)row_ror<R>((unsigned)i);
-    if (ov > v || (ov == v && oi < i)) {
-        v = ov;
-        i = oi;
-    }
+__device__ __forceinline__ void row_max_key_step(unsigned long long& k) {
+    const unsigned lo = row_ror<R>((unsigned)k), hi = row_ror<R>((unsigned)(k >> 32));
+    const unsigned long long o = ((unsigned long long)hi << 32) | lo;
+    k = o > k ? o : k;
 }
-__device__ __forceinline__ void row_best(float& v, int& i) {
-    row_best_step<8>(v, i);
-    row_best_step<4>(v, i);
-    row_best_step<2>(v, i);
-    row_best_step<1>(v, i);
+__device__ __forceinline__ unsigned long long row_max_key(unsigned long long k) {
+    row_max_key_step<8>(k);
+    row_max_key_step<4>(k);
+    row_max_key_step<2>(k);
+    row_max_key_step<1>(k);
+    return k;
 }
 
 __device__ __forceinline__ float f4_at(const float4& v, int q) {
     return q == 0 ? v.x : q == 1 ? v.y : q == 2 ? v.z : v.w;
 }
 
-// Heavy ties (a candidate list that would overflow): K argmax rounds over the
-// row's biased scores in registers, by the token's 16 lanes (one DPP row, all
-// active).  Round r finds the element ranked next after the previous round's
-// (pv, pi); a lane visits its columns in ascending order, so among equal
-// values it keeps the first, i.e. the lowest index.  Not inlined: the main
-// path's register count (and occupancy) does not carry this rare path's.
+// Heavy ties (a candidate list that would overflow): K rounds over the row's
+// biased scores in registers, by the token's 16 lanes (one DPP row, all
+// active).  Round r takes the largest rank key strictly below the previous
+// round's pick.  Rank keys order (v descending, index ascending) with -0 ==
+// +0, and every real column's key is above the key 0 a round starts from --
+// -inf included, so a row with fewer than K finite biased scores still picks
+// its -inf columns by lowest index.  Not inlined: the main path's register
+// count (and occupancy) does not carry this rare path's.
 template <int NV>
 __device__ __attribute__((noinline)) void overflow_select(const float* row, const float* bias_s, unsigned vmask, int j,
                                                           int K, int* sel_i, float* sel_s) {
@@ -189,28 +188,21 @@ __device__ __attribute__((noinline)) void overflow_select(const float* row, cons
             vv[c] = make_float4(s4.x + b4.x, s4.y + b4.y, s4.z + b4.z, s4.w + b4.w);
         }
     }
-    float pv = INFINITY;
-    int pi = -1, mine = 0;
+    unsigned long long prev = ~0ull;
+    int mine = 0;
     for (int r = 0; r < K; ++r) {
-        float bv = -INFINITY;
-        int bi = 0x7fffffff;
+        unsigned long long best = 0ull;
 #pragma unroll
         for (int c = 0; c < NV; ++c) {
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
-                const float v = f4_at(vv[c], q);
-                const int i = 4 * (16 * c + j) + q;
-                const bool after = v < pv || (v == pv && i > pi);
-                if (((vmask >> c) & 1u) && after && v > bv) {
-                    bv = v;
-                    bi = i;
-                }
+                const unsigned long long kk = rank_key(f4_at(vv[c], q), 4 * (16 * c + j) + q);
+                if (((vmask >> c) & 1u) && kk < prev && kk > best) best = kk;
             }
         }
-        row_best(bv, bi);
-        pv = bv;
-        pi = bi;
-        if (j == r) mine = bi;
+        best = row_max_key(best);
+        prev = best;
+        if (j == r) mine = (int)~(unsigned)best;
     }
     if (j < K) {
         sel_i[j] = mine;

@@ -77,6 +77,12 @@ class RouterStep:
         B.idb_router_step(x, Wt, self.K, self.cfg, self.state, self.idx, self.w, self.counts, accumulate,
                           self.stats, self.workspace, self.variant, stream, layout)
 
+    def merge_step(self, stream=None):
+        """The second launch of :meth:`step` after :meth:`score_select` (same bias, same outputs): slice merge,
+        MaxVio/MinVio and the bias update."""
+        B.idb_router_merge_step(self.T, self.d, self.K, self.dtype_code, self.cfg, self.state, self.idx, self.w,
+                                self.counts, self.stats, self.workspace, self.variant, stream)
+
     # ------------------------------------------------------------ Quantile Balancing
 
     def qb_buffers(self):

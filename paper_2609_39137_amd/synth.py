@@ -243,3 +243,25 @@ def count_stream(E: int, total: int, steps: int, kind: str, seed: int) -> np.nda
     else:
         raise ValueError(kind)
     return out.astype(np.int32)
+
+
+def integer_drift_inputs(T: int, d: int, E: int, step: int, seed: int, dtype: str = "bf16", w_shift: int = 6):
+    """Integer-valued hidden states whose token groups drift from step to step, and a fixed integer router matrix.
+
+    x has entries in {-2..2} (fresh each step, stream ``step``); the tokens
+    fall into four groups, and group k's columns [16k, 16k + 16) are set to a
+    shared value c_k(t) = round(2 sin(2 pi (t + 3k) / 10)), so the load moves
+    between experts and back over the steps.  W has entries in {-2..2} *
+    2^-w_shift and does not depend on ``step``.  Every partial sum of W x is a
+    multiple of 2^-w_shift well inside fp32's exact range, so the logits are
+    exact on any summation order.
+    """
+    g = rng(9010, seed, step)
+    x = g.integers(-2, 3, size=(T, d)).astype(np.float32)
+    grp = g.integers(0, 4, size=T)
+    for k in range(4):
+        c = float(np.round(2.0 * np.sin(2.0 * np.pi * (step + 3 * k) / 10.0)))
+        x[grp == k, 16 * k:16 * k + 16] = c
+    gw = rng(9011, seed)
+    W = gw.integers(-2, 3, size=(E, d)).astype(np.float32) * np.float32(2.0 ** -w_shift)
+    return _store(x, dtype), _store(W, dtype)

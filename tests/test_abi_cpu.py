@@ -344,3 +344,25 @@ def test_controller_state_dict_round_trip():
     d["bias"] = d["bias"][:2]
     with pytest.raises(ValueError, match="bias"):
         b.load_state_dict(d)
+
+
+def test_merge_step_rejects_invalid_arguments():
+    L = B.lib()
+    cfg = B.idb_controller_cfg(768, 6e-3, 6e-3, 0, 1)
+    st = B.idb_controller_state(A16, A16, A16, A16)
+    args = dict(T=128, d=256, K=10, dtype=0, idx=A16, w=A16, counts=A16, out=A16, ws=A16, ws_bytes=1 << 30, variant=0)
+
+    def call(**kw):
+        a = dict(args, **kw)
+        return L.idb_router_merge_step(a["T"], a["d"], a["K"], a["dtype"], ctypes.byref(cfg), ctypes.byref(st),
+                                       a["idx"], a["w"], a["counts"], a["out"], a["ws"], a["ws_bytes"], a["variant"],
+                                       None)
+    assert call(T=0) == B.IDB_ERR_INVALID_ARG
+    assert call(idx=None) == B.IDB_ERR_INVALID_ARG
+    assert call(ws=None) == B.IDB_ERR_INVALID_ARG  # two slices: the candidates are in the workspace
+    assert call(ws_bytes=64) == B.IDB_ERR_INVALID_ARG
+    assert call(K=33) == B.IDB_ERR_UNSUPPORTED
+    assert call(out=A16 + 4) == B.IDB_ERR_INVALID_ARG
+    bad = B.idb_controller_state(None, A16, A16, A16)
+    assert L.idb_router_merge_step(128, 256, 10, 0, ctypes.byref(cfg), ctypes.byref(bad), A16, A16, A16, A16, A16,
+                                   1 << 30, 0, None) == B.IDB_ERR_INVALID_ARG

@@ -181,3 +181,21 @@ def test_router_step_graph_replays():
         s.update_and_stats()
         torch.cuda.synchronize()
         _assert_same_step(f, s, f"replay {t}")
+
+
+@pytest.mark.parametrize("T,d,E,K,variant", [(2048, 256, 768, 10, 6), (513, 256, 1024, 32, 0), (1000, 256, 768, 10, 7)])
+def test_score_select_then_merge_step_equals_router_step(T, d, E, K, variant):
+    """idb_router_score_select + idb_router_merge_step (the benchmark times the
+    router kernel between them) give exactly idb_router_step's results."""
+    _, W = synth.normal_router_inputs(T, d, E, seed=19)
+    Wt = _bf16(W)
+    cfg = B.ControllerCfg(E, 6e-3, 6e-3)
+    f = RouterStep(T, d, E, K, torch.bfloat16, cfg=cfg, variant=variant)
+    s = RouterStep(T, d, E, K, torch.bfloat16, cfg=cfg, variant=variant)
+    for t in range(4):
+        x = _bf16(synth.normal_router_inputs(T, d, E, seed=400 + t)[0])
+        x[:, :16] += 1.5
+        f.step(x, Wt)
+        s.score_select(x, Wt)
+        s.merge_step()
+        _assert_same_step(f, s, f"step {t}")

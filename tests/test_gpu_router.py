@@ -286,6 +286,24 @@ def test_workload_full_size_sampled_rows(name):
         np.testing.assert_array_equal(c, sc)
 
 
+def test_headline_full_batch_against_oracle():
+    """All 16384 rows of the Top-10-of-768 batch (d = 2048) against the oracle:
+    scores within rel 2e-3 everywhere, the oracle's selection on every token
+    outside near ties (at most 1%), counts = bincount of the indices."""
+    wl = synth.WORKLOADS["top10-of-768"]
+    x = synth.hidden_states(wl, step=0)
+    W = synth.router_weight(wl)
+    b = synth.bias(wl.E, "small", seed=wl.wid)
+    rs = RouterStep(wl.T, wl.d, wl.E, wl.K, torch.bfloat16)
+    rs.state.bias.copy_(torch.from_numpy(b))
+    dump = torch.empty((wl.T, wl.E), dtype=torch.float32, device=DEV)
+    rs.route(to_dev(x), to_dev(W), scores_dump=dump)
+    idx, w, c = rs.idx.cpu().numpy(), rs.w.cpu().numpy(), rs.counts.cpu().numpy()
+    check_invariants(idx, w, c, wl.T, wl.E, wl.K)
+    n = check_against_oracle(x, W, b, wl.K, idx, w, c, dump.cpu().numpy(), rows=None, max_uncertain=0.01)
+    print(f"headline full batch: {n} near-tie tokens of {wl.T}")
+
+
 @pytest.mark.parametrize("T,d,E,K,dtype,variant", [
     (517, 512, 768, 10, "bf16", 1), (517, 512, 768, 10, "bf16", 2), (300, 256, 768, 5, "bf16", 3),
     (129, 128, 800, 10, "bf16", 4), (1000, 256, 64, 4, "f32", 5), (64, 2048, 256, 8, "bf16", 0),

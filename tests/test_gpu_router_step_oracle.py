@@ -1,0 +1,80 @@
+"""The one-call iteration idb_router_step pinned to the oracle over gated trajectories (Alg. 1).
+
+idb_router_step runs the fused router kernel, then the slice merge, whose
+last workgroup applies the ID update (Eq. rapid-integral, rapid-delta,
+rapid-gate, rapid-update) and writes MaxVio/MinVio (Eq. vio).  Here it runs
+25 consecutive iterations from hidden states on the tilings the benchmark
+uses (two 384-expert slices merged per 128-token tile) and on the generic
+slice merge (three slices of 32 candidates), and every iteration is compared
+with the oracle's router + controller from the same host-generated inputs:
+
+* inputs: integer-valued hidden states with drifting token groups and an
+  integer router matrix (exact logits on both sides), T*K and E chosen so the
+  load errors are exact dyadic values, dyadic gains; the oracle's trajectory
+  satisfies the safety condition of tests/trajectory.py at every token of
+  every step (asserted here and in test_trajectory_design.py), so the
+  selection is decided identically;
+* bit-exact every step: expert indices (rank order), counts, bias, e_prev,
+  step, status and MaxVio/MinVio; gate weights within the score error;
+* the derivative gate opens (the update's active-gate fraction from the
+  oracle is above 10% after the first step), so the gated derivative term of
+  the timed code is pinned, not only the integral step.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2609_39137_amd import binding as B
+from paper_2609_39137_amd import synth
+from paper_2609_39137_amd.pipeline import RouterStep
+from tests import trajectory
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+
+
+def _bf16(a: np.ndarray) -> torch.Tensor:
+    return torch.from_numpy(a.view(np.int16)).to(DEV).view(torch.bfloat16)
+
+
+@pytest.mark.parametrize("T,d,E,K,a,variant,packed,slices", [
+    (2048, 256, 768, 8, 14, 6, True, 2),    # the benchmark's tiling: 16x16 MFMA tiles, two-slice tile merge
+    (2048, 256, 768, 8, 14, 1, False, 2),   # 32x32 MFMA tiles, row-major router matrix, same merge
+    (2048, 256, 1024, 32, 14, 6, True, 3),  # 3 slices x 32 candidates: the generic merge kernel's tail
+])
+def test_router_step_trajectory_is_the_oracle_s(T, d, E, K, a, variant, packed, slices):
+    gain = 2.0 ** -a
+    steps = 25
+    cfg = B.ControllerCfg(E, gain, gain)
+    rs = RouterStep(T, d, E, K, torch.bfloat16, cfg=cfg, variant=variant)
+    assert rs.info["slices"] == slices
+    _, W = synth.integer_drift_inputs(T, d, E, 0, seed=E)
+    Wt = _bf16(W)
+    if packed:
+        rs.pack(Wt)
+    ref = oracle.ControllerState(E)
+    gates = []
+    for t in range(steps):
+        x, _ = synth.integer_drift_inputs(T, d, E, t, seed=E)
+        print(f"[traj] T={T} E={E} K={K} variant={variant} step {t}", flush=True)
+        rs.step(_bf16(x), None if packed else Wt)
+        r = trajectory.oracle_step(x, W, ref, K, gain, gain)
+        assert r["safe"].all(), f"step {t}: input design leaves selections undecided"
+        torch.cuda.synchronize()
+        msg = f"step {t}"
+        np.testing.assert_array_equal(rs.idx.cpu().numpy(), r["idx"], err_msg=msg)
+        np.testing.assert_array_equal(rs.counts.cpu().numpy(), r["counts"], err_msg=msg)
+        np.testing.assert_array_equal(rs.state.bias.cpu().numpy().view(np.uint32), ref.bias.view(np.uint32),
+                                      err_msg=msg)
+        np.testing.assert_array_equal(rs.state.e_prev.cpu().numpy().view(np.uint32), ref.e_prev.view(np.uint32),
+                                      err_msg=msg)
+        assert int(rs.state.step.item()) == int(ref.step[0]) == t + 1
+        assert int(rs.state.status.item()) == int(ref.status[0]) == 0
+        np.testing.assert_array_equal(rs.stats.cpu().numpy().view(np.uint64), r["stats"].view(np.uint64),
+                                      err_msg=msg)
+        # gate weights: ratios of scores that agree to a few ulps
+        np.testing.assert_allclose(rs.w.cpu().numpy(), r["w"], rtol=4e-6, err_msg=msg)
+        gates.append(r["diag"][0])
+    assert gates[0] == 0.0 and min(gates[1:]) > 0.1, gates
+    assert np.abs(ref.bias).max() > 0

@@ -127,3 +127,41 @@ def test_misaligned_score_rows():
     np.testing.assert_array_equal(idx.cpu().numpy(), ridx)
     np.testing.assert_array_equal(w.cpu().numpy().view(np.uint32), rw.view(np.uint32))
     np.testing.assert_array_equal(c.cpu().numpy(), rc)
+
+
+@pytest.mark.parametrize("E,K", [(768, 10), (768, 3), (64, 4), (256, 10), (768, 16), (770, 10)])
+def test_rows_with_fewer_than_k_finite_biased_scores(E, K):
+    # finite inputs whose sums overflow: s = b = -FLT_MAX gives s + b = -inf.
+    # Rows where only 2 experts have a finite biased score must still select
+    # K experts: the finite ones, then the -inf ones by lowest index (the
+    # register kernel's overflow rounds and the epilogue's infinite-threshold
+    # masks); ordinary rows share the waves.
+    big = np.float32(-np.finfo(np.float32).max)
+    s = synth.scores(130, E, "beta", seed=E + K)
+    b = synth.bias(E, "small", seed=K)
+    live = np.array([E // 3, E - 1])
+    b_ovf = np.full(E, big, np.float32)
+    b_ovf[live] = b[live]
+    s[1::3] = big
+    s[1::3, live] = np.float32(0.5)
+    s[2::3, : E // 2] = big
+    check(s, b_ovf, K)
+    idx, _, _ = gpu_select(s, b_ovf, K)
+    assert set(idx[1, :2].tolist()) == set(live.tolist())
+
+
+@pytest.mark.parametrize("E,K", [(768, 16), (768, 10), (100, 12), (1024, 32)])
+def test_signed_zero_scores_and_bias_tie(E, K):
+    # every biased value is -0 or +0 (equal): the K lowest indices win, in
+    # both the register kernel and the epilogue's threshold masks
+    g = synth.rng(77, E, K)
+    s = np.where(g.random((96, E)) < 0.5, np.float32(-0.0), np.float32(0.0)).astype(np.float32)
+    b = np.where(g.random(E) < 0.5, np.float32(-0.0), np.float32(0.0)).astype(np.float32)
+    # a third of the rows: -0 scores with -0 bias on the low experts, +0 on the rest
+    s[::3, : E // 2] = np.float32(-0.0)
+    b2 = b.copy()
+    b2[: E // 2] = np.float32(-0.0)
+    for bb in (b, b2):
+        check(s, bb, K)
+        idx, _, _ = gpu_select(s, bb, K)
+        assert np.all(idx == np.arange(K)[None, :])
