@@ -132,12 +132,27 @@ def main() -> int:
     ap.add_argument("--aux-variant", type=int, default=0, help="one-slice router tiling of --controller aux")
     ap.add_argument("--rho", type=float, default=0.0, help="Quantile Balancing EMA weight (0: the plain target)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="wall-clock target of the CPU oracle sample")
+    ap.add_argument("--loop", action="store_true",
+                    help="run the workload's closed loop instead (its number of controller steps, fresh batch each "
+                         "step) with the ID controller, integral-only and DeepSeek's rule side by side, and report "
+                         "the load-balance trajectory")
+    ap.add_argument("--loop-steps", type=int, default=0, help="steps of --loop (0: the workload's own)")
+    ap.add_argument("--loop-md", default=None, help="also write a markdown summary of --loop to this path")
+    ap.add_argument("--gen-workers", type=int, default=8, help="processes generating the --loop input batches")
     args = ap.parse_args()
 
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported (the count all-reduce across "
               f"data-parallel ranks is design-only in this build)", file=sys.stderr)
         return 2
+
+    pool = None
+    if args.loop:
+        # the input-generating workers start before anything initialises the
+        # GPU in this process
+        import multiprocessing as mp
+
+        pool = mp.get_context("spawn").Pool(max(1, args.gen_workers))
 
     import torch
 
@@ -150,6 +165,11 @@ def main() -> int:
         return 1
     dev = "cuda"
     wl = synth.WORKLOADS[args.workload or synth.HEADLINE]
+    if args.loop:
+        try:
+            return loop_report(args, wl, pool)
+        finally:
+            pool.terminate()
     tdtype = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
     x_bytes = wl.T * wl.d * (2 if wl.dtype == "bf16" else 4)
     nbuf = args.buffers or max(1, min(8, math.ceil(512 * 2**20 / x_bytes)))
@@ -425,8 +445,9 @@ def kernel_time_in_steps(args, rs, W, xs, nbuf, stream):
     kernels of idb_router_step), with HIP events recorded on the stream right
     before and after the router kernel.  The steps are launched eagerly: on
     ROCm, events recorded inside a captured graph carry no timestamps (only
-    external events would, and they are not available there).  One untimed
-    pass of the same steps first fills the launch queue."""
+    external events would, and they are not available there).  All steps are
+    enqueued while a spin kernel holds the stream; nbuf untimed steps run
+    first."""
     import torch
 
     n = max(args.steps, nbuf)
@@ -442,13 +463,166 @@ def kernel_time_in_steps(args, rs, W, xs, nbuf, stream):
         rs.merge_step(stream=stream)
 
     with torch.cuda.stream(stream):
+        # a spin kernel holds the stream while the host enqueues every step, so
+        # the steps then run back to back from the queue (the host launches
+        # more slowly than the GPU runs them; without it the launch gaps would
+        # fall inside the event pairs)
+        torch.cuda._sleep(40_000_000)
         for i in range(nbuf):
             split_step(i, False)
         for i in range(n):
             split_step(i, True)
     torch.cuda.synchronize()
     ms = sum(a.elapsed_time(b) for a, b in pairs) / n
-    return ms, f"HIP events around each router kernel launch in {n} eagerly launched steps"
+    return ms, (f"HIP events around each router kernel launch in {n} steps (pack, router, merge + update) enqueued "
+                f"behind a spin kernel and run back to back")
+
+
+def _gen_batch(name: str, step: int) -> np.ndarray:
+    """Hidden states of one loop step (run in a worker process)."""
+    from paper_2609_39137_amd import synth
+
+    return synth.hidden_states(synth.WORKLOADS[name], step=step)
+
+
+def loop_report(args, wl, pool) -> int:
+    """Closed loop of Alg. 1 on the GPU: ``steps`` iterations of idb_router_step, each on a fresh batch.
+
+    Three controllers route the same batches side by side: ID Balancing
+    (K_i = K_d = 6e-3, centred), its integral-only ablation (K_d = 0) and
+    DeepSeek's rule (SIGN mode, 1e-3, no centring).  Each step records
+    MaxVio/MinVio (from the step itself) and the update's diagnostics
+    (active-gate fraction, busiest-10% share, inactive-expert ratio, mean
+    |bias change|) from idb_controller_update_layers applied to a copy of the
+    pre-step state with the step's counts; that copy's new bias must equal the
+    step's bit for bit.  Batches are generated by worker processes in step
+    order while the GPU runs."""
+    import torch
+
+    from paper_2609_39137_amd import binding as B
+    from paper_2609_39137_amd import metrics
+    from paper_2609_39137_amd import synth
+    from paper_2609_39137_amd.pipeline import RouterStep
+
+    dev = "cuda"
+    steps = args.loop_steps or wl.steps
+    tdtype = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
+    W_np = synth.router_weight(wl)
+    W = torch.from_numpy(W_np.view(np.int16) if W_np.dtype == np.uint16 else W_np).to(dev)
+    if W_np.dtype == np.uint16:
+        W = W.view(torch.bfloat16)
+    ctrls = {
+        "id": B.ControllerCfg(wl.E, 6e-3, 6e-3, B.IDB_INTEGRAL_ERROR, True),
+        "integral-only": B.ControllerCfg(wl.E, 6e-3, 0.0, B.IDB_INTEGRAL_ERROR, True),
+        "deepseek-sign": B.ControllerCfg(wl.E, 1e-3, 0.0, B.IDB_INTEGRAL_SIGN, False),
+    }
+    runs = {}
+    for name, cfg in ctrls.items():
+        rs = RouterStep(wl.T, wl.d, wl.E, wl.K, tdtype, cfg, variant=args.variant)
+        rs.pack(W)
+        shadow = B.ControllerState(wl.E, dev, layers=1)
+        runs[name] = {"rs": rs, "shadow": shadow, "stats": torch.empty((1, 2), dtype=torch.float64, device=dev),
+                      "diag": torch.empty((1, 4), dtype=torch.float64, device=dev), "rec": metrics.LoadRecord(),
+                      "diag_rows": [], "us": []}
+    log(f"closed loop {wl.name}: {steps} steps, T={wl.T} d={wl.d} E={wl.E} K={wl.K}; controllers {list(ctrls)}")
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    workers = max(1, args.gen_workers)
+    t_start = time.time()
+    window = 2 * workers  # batches in flight (bounded host memory)
+    futs = {t: pool.apply_async(_gen_batch, (wl.name, t)) for t in range(min(window, steps))}
+    for t in range(steps):
+        x_np = futs.pop(t).get()
+        if t + window < steps:
+            futs[t + window] = pool.apply_async(_gen_batch, (wl.name, t + window))
+        x = torch.from_numpy(x_np.view(np.int16) if x_np.dtype == np.uint16 else x_np).to(dev)
+        if x_np.dtype == np.uint16:
+            x = x.view(torch.bfloat16)
+        for name, r in runs.items():
+            rs, sh = r["rs"], r["shadow"]
+            sh.bias.copy_(rs.state.bias.view(1, -1))
+            sh.e_prev.copy_(rs.state.e_prev.view(1, -1))
+            sh.step.copy_(rs.state.step)
+            sh.status.copy_(rs.state.status)
+            ev0.record()
+            rs.step(x, None)
+            ev1.record()
+            B.idb_controller_update_layers(rs.counts.view(1, -1), rs.cfg, sh, r["stats"], r["diag"])
+            torch.cuda.synchronize()
+            r["us"].append(ev0.elapsed_time(ev1) * 1000.0)
+            if not torch.equal(sh.bias.view(-1).view(torch.int32), rs.state.bias.view(torch.int32)):
+                raise RuntimeError(f"{name} step {t}: the one-call step and the layers kernel disagree")
+            st = rs.stats.cpu().numpy()
+            if not np.array_equal(st.view(np.int64), r["stats"].cpu().numpy().reshape(-1).view(np.int64)):
+                raise RuntimeError(f"{name} step {t}: MaxVio/MinVio differ between the two kernels")
+            r["rec"].add(st)
+            r["diag_rows"].append(r["diag"].cpu().numpy().reshape(-1).copy())
+        if t % 10 == 0 or t == steps - 1:
+            mv = {n: round(float(r["rec"].maxvio[-1, 0]), 4) for n, r in runs.items()}
+            log(f"step {t}: MaxVio {mv} ({time.time() - t_start:.1f} s)")
+    out = {"metric": f"closed-loop load balance, Top-{wl.K}-of-{wl.E} ({wl.name}), {steps} controller steps",
+           "workload": wl.name, "T": wl.T, "d": wl.d, "E": wl.E, "K": wl.K, "steps": steps, "data": "synthetic",
+           "controllers": {}}
+    for name, r in runs.items():
+        diag = np.stack(r["diag_rows"])
+        last = max(1, steps // 10)
+        summ = r["rec"].summary(last=last)
+        summ.update({
+            "cumulative_excess_above_1": r["rec"].cumulative_excess(1.0),
+            "gate_fraction_first10_mean": float(np.nanmean(diag[1:11, 0])) if steps > 1 else None,
+            "gate_fraction_last10pct_mean": float(np.nanmean(diag[-last:, 0])),
+            "busiest10_share_last10pct_mean": float(np.mean(diag[-last:, 1])),
+            "inactive_ratio_last10pct_mean": float(np.mean(diag[-last:, 2])),
+            "step_us_median": float(np.median(r["us"])),
+            "last_window_steps": last,
+            "cfg": {"Ki": r["rs"].cfg.Ki, "Kd": r["rs"].cfg.Kd, "mode": r["rs"].cfg.integral_mode,
+                    "center": bool(r["rs"].cfg.center)},
+            "maxvio": [round(float(v), 6) for v in r["rec"].maxvio[:, 0]],
+            "minvio": [round(float(v), 6) for v in r["rec"].minvio[:, 0]],
+            "gate_fraction": [round(float(v), 6) for v in diag[:, 0]],
+            "busiest10_share": [round(float(v), 6) for v in diag[:, 1]],
+        })
+        out["controllers"][name] = summ
+    if args.loop_md:
+        with open(args.loop_md, "w") as f:
+            f.write(loop_markdown(out, sys.argv))
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+def loop_markdown(out: dict, argv) -> str:
+    """Markdown summary of a --loop run: per-controller aggregates, then the per-step trajectory."""
+    c = out["controllers"]
+    names = list(c)
+    last = c[names[0]]["last_window_steps"]
+    lines = [f"# Closed loop, {out['workload']} (T={out['T']}, d={out['d']}, E={out['E']}, K={out['K']}), "
+             f"{out['steps']} steps", "", "Command:", "", "```", "python " + " ".join(argv), "```", "",
+             "Each step: a fresh synthetic batch routed by idb_router_step with the controller's current bias "
+             "(fused router kernel, slice merge, update and MaxVio/MinVio in the merge's last workgroup). "
+             "Diagnostics from idb_controller_update_layers on a copy of the pre-step state (its bias equals the "
+             "step's bit for bit, checked every step).", "",
+             f"| controller | K_i | K_d | mode | centre | MaxVio last {last} | MaxVio avg | MaxVio worst | "
+             f"MinVio last {last} | MinVio avg | excess above 1 | gate frac. steps 1-10 | gate frac. last {last} | "
+             f"busiest-10% share last {last} | step us (median) |",
+             "|---|---:|---:|---|---|---:|---:|---:|---:|---:|---:|---:|---:|---:|---:|"]
+    for n in names:
+        s = c[n]
+        mode = "sign" if s["cfg"]["mode"] == 1 else "error"
+        lines.append(f"| {n} | {s['cfg']['Ki']:g} | {s['cfg']['Kd']:g} | {mode} | {s['cfg']['center']} | "
+                     f"{s['maxvio_last']:.4f} | {s['maxvio_avg']:.4f} | {s['maxvio_worst']:.4f} | "
+                     f"{s['minvio_last']:.4f} | {s['minvio_avg']:.4f} | {s['cumulative_excess_above_1']:.2f} | "
+                     f"{s['gate_fraction_first10_mean']:.4f} | {s['gate_fraction_last10pct_mean']:.4f} | "
+                     f"{s['busiest10_share_last10pct_mean']:.4f} | {s['step_us_median']:.1f} |")
+    lines += ["", "Per step (MaxVio, MinVio, active-gate fraction, busiest-10% share):", "",
+              "| step | " + " | ".join(f"{n} MaxVio | {n} MinVio" for n in names) + " | id gate frac. | "
+              "id busiest-10% |", "|---:|" + "---:|" * (2 * len(names) + 2)]
+    for t in range(out["steps"]):
+        cells = []
+        for n in names:
+            cells += [f"{c[n]['maxvio'][t]:.4f}", f"{c[n]['minvio'][t]:.4f}"]
+        lines.append(f"| {t} | " + " | ".join(cells) + f" | {c['id']['gate_fraction'][t]:.4f} | "
+                     f"{c['id']['busiest10_share'][t]:.4f} |")
+    return "\n".join(lines) + "\n"
 
 
 def graph_time_per_call(fn, per, reps, stream, capture):

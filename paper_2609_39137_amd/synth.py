@@ -32,7 +32,9 @@ def rng(*key: int) -> np.random.Generator:
 
 def to_bf16_bits(a: np.ndarray) -> np.ndarray:
     """Round fp32 values to bfloat16 (round to nearest, ties to even); returns the raw bits as uint16."""
-    u = np.ascontiguousarray(a, dtype=np.float32).view(np.uint32).astype(np.uint64)
+    u = np.ascontiguousarray(a, dtype=np.float32).view(np.uint32)
+    if u.size and int(u.max()) >= 0xFFFF8000:  # NaN payloads the 32-bit sum would wrap: widen
+        u = u.astype(np.uint64)
     lsb = (u >> 16) & 1
     return ((u + 0x7FFF + lsb) >> 16).astype(np.uint16)
 
@@ -245,23 +247,31 @@ def count_stream(E: int, total: int, steps: int, kind: str, seed: int) -> np.nda
     return out.astype(np.int32)
 
 
-def integer_drift_inputs(T: int, d: int, E: int, step: int, seed: int, dtype: str = "bf16", w_shift: int = 6):
+def integer_drift_inputs(T: int, d: int, E: int, step: int, seed: int, dtype: str = "bf16", w_shift: int = 6,
+                         balanced: bool = False, drift_cols: int = 16, drift_amp: float = 2.0):
     """Integer-valued hidden states whose token groups drift from step to step, and a fixed integer router matrix.
 
     x has entries in {-2..2} (fresh each step, stream ``step``); the tokens
-    fall into four groups, and group k's columns [16k, 16k + 16) are set to a
-    shared value c_k(t) = round(2 sin(2 pi (t + 3k) / 10)), so the load moves
-    between experts and back over the steps.  W has entries in {-2..2} *
-    2^-w_shift and does not depend on ``step``.  Every partial sum of W x is a
-    multiple of 2^-w_shift well inside fp32's exact range, so the logits are
-    exact on any summation order.
+    fall into four groups, and group k's columns [k c, k c + c), c =
+    ``drift_cols``, are set to a shared value round(A sin(2 pi (t + 3k) / 10)),
+    A = ``drift_amp``, so the load moves between experts and back over the
+    steps.  W has entries in {-2..2} * 2^-w_shift and does not depend on
+    ``step``; with ``balanced`` every row is a permutation of the same
+    multiset of values (equal norms, so no expert is favoured on average).
+    Every partial sum of W x is a multiple of 2^-w_shift well inside fp32's
+    exact range, so the logits are exact on any summation order.
     """
-    g = rng(9010, seed, step)
+    g = rng(9010 if not balanced else 9020, seed, step)
     x = g.integers(-2, 3, size=(T, d)).astype(np.float32)
     grp = g.integers(0, 4, size=T)
     for k in range(4):
-        c = float(np.round(2.0 * np.sin(2.0 * np.pi * (step + 3 * k) / 10.0)))
-        x[grp == k, 16 * k:16 * k + 16] = c
-    gw = rng(9011, seed)
-    W = gw.integers(-2, 3, size=(E, d)).astype(np.float32) * np.float32(2.0 ** -w_shift)
+        c = float(np.round(drift_amp * np.sin(2.0 * np.pi * (step + 3 * k) / 10.0)))
+        x[grp == k, drift_cols * k:drift_cols * k + drift_cols] = c
+    if balanced:
+        gw = rng(9021, seed)
+        base = np.resize(np.array([-2, -1, 0, 1, 2], np.float32), d)
+        W = np.stack([gw.permutation(base) for _ in range(E)]) * np.float32(2.0 ** -w_shift)
+    else:
+        gw = rng(9011, seed)
+        W = gw.integers(-2, 3, size=(E, d)).astype(np.float32) * np.float32(2.0 ** -w_shift)
     return _store(x, dtype), _store(W, dtype)

@@ -5,8 +5,10 @@ last workgroup applies the ID update (Eq. rapid-integral, rapid-delta,
 rapid-gate, rapid-update) and writes MaxVio/MinVio (Eq. vio).  Here it runs
 25 consecutive iterations from hidden states on the tilings the benchmark
 uses (two 384-expert slices merged per 128-token tile) and on the generic
-slice merge (three slices of 32 candidates), and every iteration is compared
-with the oracle's router + controller from the same host-generated inputs:
+slice merge (three slices of 32 candidates), and 200 iterations at Top-3 of
+768 (the drifting workload's K, E and length), and every iteration is
+compared with the oracle's router + controller from the same host-generated
+inputs:
 
 * inputs: integer-valued hidden states with drifting token groups and an
   integer router matrix (exact logits on both sides), T*K and E chosen so the
@@ -38,28 +40,36 @@ def _bf16(a: np.ndarray) -> torch.Tensor:
     return torch.from_numpy(a.view(np.int16)).to(DEV).view(torch.bfloat16)
 
 
-@pytest.mark.parametrize("T,d,E,K,a,variant,packed,slices", [
-    (2048, 256, 768, 8, 14, 6, True, 2),    # the benchmark's tiling: 16x16 MFMA tiles, two-slice tile merge
-    (2048, 256, 768, 8, 14, 1, False, 2),   # 32x32 MFMA tiles, row-major router matrix, same merge
-    (2048, 256, 1024, 32, 14, 6, True, 3),  # 3 slices x 32 candidates: the generic merge kernel's tail
-])
-def test_router_step_trajectory_is_the_oracle_s(T, d, E, K, a, variant, packed, slices):
+# (T, d, E, K, log2 of 1/gain, variant, packed router matrix, slices, steps, centring, input design)
+CASES = [
+    (2048, 256, 768, 8, 14, 6, True, 2, 25, True, {}),   # the benchmark's tiling: 16x16 tiles, two-slice tile merge
+    (2048, 256, 768, 8, 14, 1, False, 2, 25, True, {}),  # 32x32 MFMA tiles, row-major router matrix, same merge
+    (2048, 256, 1024, 32, 14, 6, True, 3, 25, True, {}),  # 3 slices x 32 candidates: the generic merge kernel's tail
+    # the Top-3-of-768 loop's length: 200 steps (no centring, which keeps every bias on the exact dyadic grid
+    # over a long run; centring is pinned by the cases above), balanced router rows so the bias stays small
+    (4096, 64, 768, 3, 16, 6, True, 2, 200, False, dict(balanced=True, drift_cols=4, drift_amp=1.0)),
+]
+
+
+@pytest.mark.parametrize("T,d,E,K,a,variant,packed,slices,steps,center,design", CASES)
+def test_router_step_trajectory_is_the_oracle_s(T, d, E, K, a, variant, packed, slices, steps, center, design):
     gain = 2.0 ** -a
-    steps = 25
-    cfg = B.ControllerCfg(E, gain, gain)
+    cfg = B.ControllerCfg(E, gain, gain, B.IDB_INTEGRAL_ERROR, center)
     rs = RouterStep(T, d, E, K, torch.bfloat16, cfg=cfg, variant=variant)
     assert rs.info["slices"] == slices
-    _, W = synth.integer_drift_inputs(T, d, E, 0, seed=E)
+    seed = E if not design else E + K
+    _, W = synth.integer_drift_inputs(T, d, E, 0, seed=seed, **design)
     Wt = _bf16(W)
     if packed:
         rs.pack(Wt)
     ref = oracle.ControllerState(E)
     gates = []
     for t in range(steps):
-        x, _ = synth.integer_drift_inputs(T, d, E, t, seed=E)
-        print(f"[traj] T={T} E={E} K={K} variant={variant} step {t}", flush=True)
+        x, _ = synth.integer_drift_inputs(T, d, E, t, seed=seed, **design)
+        if t % 25 == 0:
+            print(f"[traj] T={T} E={E} K={K} variant={variant} step {t}", flush=True)
         rs.step(_bf16(x), None if packed else Wt)
-        r = trajectory.oracle_step(x, W, ref, K, gain, gain)
+        r = trajectory.oracle_step(x, W, ref, K, gain, gain, center=center)
         assert r["safe"].all(), f"step {t}: input design leaves selections undecided"
         torch.cuda.synchronize()
         msg = f"step {t}"
@@ -69,7 +79,7 @@ def test_router_step_trajectory_is_the_oracle_s(T, d, E, K, a, variant, packed, 
                                       err_msg=msg)
         np.testing.assert_array_equal(rs.state.e_prev.cpu().numpy().view(np.uint32), ref.e_prev.view(np.uint32),
                                       err_msg=msg)
-        assert int(rs.state.step.item()) == int(ref.step[0]) == t + 1
+        assert int(rs.state.step.item()) == int(ref.step[0]) == t + 1, msg
         assert int(rs.state.status.item()) == int(ref.status[0]) == 0
         np.testing.assert_array_equal(rs.stats.cpu().numpy().view(np.uint64), r["stats"].view(np.uint64),
                                       err_msg=msg)
