@@ -246,6 +246,33 @@ idb_status idb_router_merge_step(int64_t T, int32_t d, int32_t K, idb_dtype dtyp
                                  int32_t variant, hipStream_t stream);
 
 /* ---------------------------------------------------------------------------
+ * idb_router_step without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation).  The call allocates nothing (no
+ * hipMalloc, hipFree or allocating library routine): the workspace is a fixed
+ * device array of IDB_NOALLOC_SCRATCH_BYTES inside the library, one copy per
+ * device, held until the process ends.  Arguments and results are exactly
+ * those of idb_router_step with workspace = that array.
+ * - Size limit: the tiling's workspace (idb_router_workspace_bytes) must fit
+ *   in IDB_NOALLOC_SCRATCH_BYTES, e.g. T <= 65536 at E = 768, K <= 10 on the
+ *   default tiling; larger shapes return IDB_ERR_UNSUPPORTED and enqueue
+ *   nothing.  One-slice tilings need no scratch.
+ * - The stream must belong to the calling thread's current device (else
+ *   IDB_ERR_INVALID_ARG).  The first call on a device looks up the array's
+ *   address there (hipGetSymbolAddress) and keeps it.
+ * - Every call on a device shares that device's array, which keeps the last
+ *   call's contents; the router kernel clears what must start at zero (the
+ *   merge's ticket) itself.  Calls that overlap on one device (other streams,
+ *   other threads) race on the array and must be serialised by the caller.
+ * ------------------------------------------------------------------------- */
+#define IDB_NOALLOC_SCRATCH_BYTES ((size_t)16 * 1024 * 1024 + 256)
+idb_status idb_router_step_noalloc(const void* x, const void* W_g, idb_dtype dtype, idb_weight_layout weight_layout,
+                                   int64_t T, int32_t d, int32_t K, const idb_controller_cfg* cfg,
+                                   const idb_controller_state* state, int32_t* expert_idx, float* gate_w,
+                                   int32_t* counts, int32_t accumulate_counts, double* out_maxvio_minvio,
+                                   int32_t variant, hipStream_t stream);
+
+/* ---------------------------------------------------------------------------
  * All MoE layers' controller updates of one iteration in one launch (Alg. 1
  * runs per layer; one workgroup per layer), with the load statistics and the
  * update's diagnostics.

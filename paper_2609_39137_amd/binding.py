@@ -36,6 +36,7 @@ EXPORTED = (
     "idb_controller_step", "idb_router_step", "idb_qb_router_workspace_bytes", "idb_qb_router_forward",
     "idb_qb_update", "idb_controller_update_layers", "idb_routing_entropy_workspace_bytes", "idb_routing_entropy",
     "idb_aux_router_workspace_bytes", "idb_aux_router_forward", "idb_router_merge_step",
+    "idb_router_step_noalloc",
 )
 
 
@@ -96,6 +97,9 @@ def lib() -> ctypes.CDLL:
     L.idb_router_merge_step.argtypes = [i64, i32, i32, i32, ctypes.POINTER(idb_controller_cfg),
                                         ctypes.POINTER(idb_controller_state), P, P, P, P, P, sz, i32, P]
     L.idb_router_merge_step.restype = ctypes.c_int
+    L.idb_router_step_noalloc.argtypes = [P, P, i32, i32, i64, i32, i32, ctypes.POINTER(idb_controller_cfg),
+                                          ctypes.POINTER(idb_controller_state), P, P, P, i32, P, i32, P]
+    L.idb_router_step_noalloc.restype = ctypes.c_int
     L.idb_qb_router_workspace_bytes.argtypes = [i64, i32, i32, i32, i32, i32]
     L.idb_qb_router_workspace_bytes.restype = sz
     L.idb_qb_router_forward.argtypes = [P, P, i32, i32, P, i64, i32, i32, i32, P, P, P, i32, P, P, P, sz, i32, P]
@@ -325,6 +329,24 @@ def idb_router_step(x, W_g, K, cfg: ControllerCfg, state: ControllerState, exper
                                int(bool(accumulate)), _ptr(out), _ptr(workspace), ws_bytes, int(variant),
                                _stream(stream))
     _check("idb_router_step", st)
+
+
+def idb_router_step_noalloc(x, W_g, K, cfg: ControllerCfg, state: ControllerState, expert_idx, gate_w, counts,
+                            accumulate=False, out=None, variant=0, stream=None, weight_layout=IDB_WEIGHT_ROW_MAJOR):
+    """:func:`idb_router_step` with the library's fixed device scratch as the workspace (allocates nothing)."""
+    T, d = x.shape
+    E = cfg.E
+    if W_g.shape != (E, d) or W_g.dtype != x.dtype or state.bias.shape != (E,):
+        raise ValueError("router operands disagree in shape or dtype")
+    if expert_idx.shape != (T, K) or gate_w.shape != (T, K) or counts.shape != (E,):
+        raise ValueError("router outputs have the wrong shape")
+    if out is not None and (out.dtype != torch.float64 or out.numel() != 2):
+        raise ValueError("out must be a float64 tensor of 2 elements")
+    c_cfg, c_state = cfg.c(), state.c()
+    st = lib().idb_router_step_noalloc(_ptr(x), _ptr(W_g), _dtype_code(x), int(weight_layout), T, d, K,
+                                       ctypes.byref(c_cfg), ctypes.byref(c_state), _ptr(expert_idx), _ptr(gate_w),
+                                       _ptr(counts), int(bool(accumulate)), _ptr(out), int(variant), _stream(stream))
+    _check("idb_router_step_noalloc", st)
 
 
 def idb_router_merge_step(T, d, K, dtype, cfg: ControllerCfg, state: ControllerState, expert_idx, gate_w, counts,

@@ -16,7 +16,8 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 OBJ = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libidb.so")
-SOURCES = ["abi.cpp", "controller.hip", "select.hip", "router.hip", "qb.hip", "entropy.hip", "aux.hip"]
+SOURCES = ["abi.cpp", "controller.hip", "select.hip", "router.hip", "qb.hip", "entropy.hip", "aux.hip",
+           "noalloc.hip"]
 ARCH = os.environ.get("IDB_OFFLOAD_ARCH", "gfx950")
 
 HIPCC = os.path.join(os.environ.get("ROCM_PATH", "/opt/rocm"), "bin", "hipcc")

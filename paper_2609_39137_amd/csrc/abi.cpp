@@ -399,6 +399,55 @@ idb_status idb_router_merge_step(int64_t T, int32_t d, int32_t K, idb_dtype dtyp
     return enqueue_merge_step(c, cfg, state, out_maxvio_minvio, stream);
 }
 
+idb_status idb_router_step_noalloc(const void* x, const void* W_g, idb_dtype dtype, idb_weight_layout weight_layout,
+                                   int64_t T, int32_t d, int32_t K, const idb_controller_cfg* cfg,
+                                   const idb_controller_state* state, int32_t* expert_idx, float* gate_w,
+                                   int32_t* counts, int32_t accumulate_counts, double* out_maxvio_minvio,
+                                   int32_t variant, hipStream_t stream) {
+    // every argument check of idb_router_step first, without any HIP call
+    idb_status st = check_controller(cfg, state, out_maxvio_minvio);
+    if (st != IDB_OK) return st;
+    st = check_router_shape(T, d, cfg->E, K, dtype);
+    if (st != IDB_OK) return st;
+    idb::RouterTiling t;
+    st = resolve_tiling(cfg->E, dtype, variant, &t);
+    if (st != IDB_OK) return st;
+    const size_t need = router_ws_bytes(T, cfg->E, K, t);
+    const size_t have = idb::noalloc_scratch_bytes();
+    if (need > have)
+        return fail(IDB_ERR_UNSUPPORTED,
+                    "idb_router_step_noalloc: this shape needs %zu bytes of scratch, the fixed scratch holds %zu "
+                    "(T=%lld, E=%d, K=%d; use idb_router_step with a workspace)",
+                    need, have, (long long)T, cfg->E, K);
+    {
+        // pointers, alignment and layout as idb_router_step checks them; the
+        // workspace stands in as an aligned placeholder (only its size and
+        // alignment are checked, nothing is dereferenced)
+        RouterCall probe;
+        st = prepare_router(x, W_g, dtype, weight_layout, state->bias, T, d, cfg->E, K, expert_idx, gate_w, counts,
+                            accumulate_counts, nullptr, reinterpret_cast<void*>(uintptr_t(256)), have, variant, true,
+                            &probe);
+        if (st != IDB_OK) return st;
+    }
+    void* ws = nullptr;
+    if (need > 0) {
+        int dev = -1;
+        st = hip_result(hipGetDevice(&dev), "current device");
+        if (st != IDB_OK) return st;
+        if (stream) {
+            hipDevice_t sdev = -1;
+            st = hip_result(hipStreamGetDevice(stream, &sdev), "stream device");
+            if (st != IDB_OK) return st;
+            if ((int)sdev != dev)
+                return fail(IDB_ERR_INVALID_ARG, "stream belongs to device %d, current device is %d", (int)sdev, dev);
+        }
+        st = hip_result(idb::noalloc_scratch(dev, &ws), "scratch address");
+        if (st != IDB_OK) return st;
+    }
+    return idb_router_step(x, W_g, dtype, weight_layout, T, d, K, cfg, state, expert_idx, gate_w, counts,
+                           accumulate_counts, out_maxvio_minvio, ws, need > 0 ? have : 0, variant, stream);
+}
+
 size_t idb_qb_router_workspace_bytes(int64_t T, int32_t d, int32_t E, int32_t K, idb_dtype dtype,
                                      int32_t variant) {
     if (K < 1 || check_router_shape(T, d, E, K + 1, dtype) != IDB_OK) return 0;

@@ -37,6 +37,12 @@ hipError_t launch_aux_stats(const float* prob_part, const int32_t* cnt_part, int
                             double alpha, int32_t* counts, double* f, double* P, double* loss, double* stats,
                             AuxPartial* partial, unsigned* ticket, hipStream_t stream);
 
+// Fixed scratch of idb_router_step_noalloc (noalloc.hip): its size, and its
+// device address on `device` (which must be the current device; the address
+// is looked up once per device and kept).
+size_t noalloc_scratch_bytes();
+hipError_t noalloc_scratch(int device, void** out);
+
 hipError_t launch_fill_i32(int32_t* p, int32_t value, int64_t n, hipStream_t stream);
 // Quantile Balancing's bias update from expert-major scores and cutoffs.
 hipError_t launch_qb_update(const float* scores_t, const float* alpha, int64_t T, int E, int K, float rho,

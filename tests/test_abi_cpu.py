@@ -366,3 +366,20 @@ def test_merge_step_rejects_invalid_arguments():
     bad = B.idb_controller_state(None, A16, A16, A16)
     assert L.idb_router_merge_step(128, 256, 10, 0, ctypes.byref(cfg), ctypes.byref(bad), A16, A16, A16, A16, A16,
                                    1 << 30, 0, None) == B.IDB_ERR_INVALID_ARG
+
+
+def test_noalloc_step_rejects_before_any_hip_call():
+    L = B.lib()
+    cfg = B.idb_controller_cfg(768, 6e-3, 6e-3, 0, 1)
+    st = B.idb_controller_state(A16, A16, A16, A16)
+
+    def call(T=128, d=256, K=10, x=A16, variant=0, state=st):
+        return L.idb_router_step_noalloc(x, A16, 0, 0, T, d, K, ctypes.byref(cfg), ctypes.byref(state), A16, A16,
+                                         A16, 0, None, variant, None)
+    # 2 slices x 10 candidates x 12 bytes per token: 2^17 tokens need 31 MB, beyond the fixed scratch
+    assert call(T=1 << 17) == B.IDB_ERR_UNSUPPORTED
+    assert "scratch" in B.idb_last_error()
+    assert call(T=0) == B.IDB_ERR_INVALID_ARG
+    assert call(x=None) == B.IDB_ERR_INVALID_ARG
+    assert call(K=33) == B.IDB_ERR_UNSUPPORTED
+    assert call(state=B.idb_controller_state(A16, None, A16, A16)) == B.IDB_ERR_INVALID_ARG
