@@ -43,18 +43,35 @@ def log(msg: str) -> None:
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-def load_traffic(workload: str, variant_id: int):
-    """HBM bytes per launch of the dominant kernel from a committed counter summary, or None if stale/absent."""
+def load_traffic(workload: str, variant_id: int, family: str = "router"):
+    """HBM bytes per launch of a counted kernel (router, merge, select) from the committed counter summary, or
+    None if it is stale (kernel sources changed since) or absent."""
     from paper_2609_39137_amd.profsum import router_source_hash
 
-    path = os.path.join(PROFILES, f"router_fused_kernel_{workload}_pmc.json")
+    path = os.path.join(PROFILES, f"router_step_{workload}_hbm_traffic.json")
     if not os.path.exists(path):
         return None
     with open(path) as f:
         d = json.load(f)
     if d.get("source_sha256") != router_source_hash() or d.get("variant") != variant_id:
         return None
-    return d.get("hbm_bytes_per_launch")
+    return d.get("kernels", {}).get(family, {}).get("hbm_bytes_per_launch")
+
+
+def load_kernel_trace_us(workload: str, family: str = "router"):
+    """Average kernel duration (us) of a kernel family in the committed rocprofv3 kernel trace of this benchmark,
+    or None if the trace is stale (kernel sources changed since) or absent."""
+    from paper_2609_39137_amd.profsum import router_source_hash
+
+    path = os.path.join(PROFILES, f"router_step_{workload}_kernel_stats.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        d = json.load(f)
+    if d.get("source_sha256") != router_source_hash():
+        return None
+    k = d.get("kernels", {}).get(family)
+    return None if k is None else round(k["avg_us"], 2)
 
 
 def cpu_baseline(wl, W, target_s: float):
@@ -214,7 +231,18 @@ def main() -> int:
     torch.cuda.synchronize()
 
     if args.pmc_pass:
+        # counter passes: the router's own scores of one batch for the unfused
+        # select (dumped before the calibration copy, so its extra writes stay
+        # out of the counted launches), then the copy of known size, then three
+        # steps (router kernel + slice merge with the update) and three
+        # selections from the dumped scores
         n_copy = args.copy_mib * 2**20
+        scores = torch.empty((wl.T, wl.E), dtype=torch.float32, device=dev)
+        sidx = torch.empty((wl.T, wl.K), dtype=torch.int32, device=dev)
+        sw = torch.empty((wl.T, wl.K), dtype=torch.float32, device=dev)
+        sc = torch.zeros(wl.E, dtype=torch.int32, device=dev)
+        with torch.cuda.stream(stream):
+            rs.route(xs[0], None, scores_dump=scores, stream=stream)
         src = torch.empty(n_copy, dtype=torch.uint8, device=dev).fill_(1)
         dst = torch.empty_like(src)
         torch.cuda.synchronize()
@@ -222,9 +250,13 @@ def main() -> int:
             dst.copy_(src)
             for i in range(3):
                 rs.score_select(xs[i % nbuf], None, stream=stream)
+                rs.merge_step(stream=stream)
+            for i in range(3):
+                B.idb_select_from_scores(scores, rs.state.bias, wl.K, sidx, sw, sc, accumulate=True, stream=stream)
         torch.cuda.synchronize()
         print(json.dumps({"pmc_pass": True, "copy_bytes": n_copy, "workload": wl.name,
-                          "variant": rs.info["variant"], "router_launches": 3}), flush=True)
+                          "variant": rs.info["variant"], "router_launches": 3, "merge_launches": 3,
+                          "select_launches": 3}), flush=True)
         return 0
 
     def capture(fn, n):
@@ -332,6 +364,12 @@ def main() -> int:
         "kernel_timing": k1_how,
         "flops_per_launch": flops,
     }
+    # the committed kernel trace of this command: the kernel's own execution
+    # time (the event pairs above also hold the dispatch and the events' own
+    # cost, a few us); reported beside, frac above is from the live events
+    trace_us = load_kernel_trace_us(wl.name)
+    roofline["kernel_trace_us"] = trace_us
+    roofline["frac_kernel_trace"] = None if trace_us is None else round(flops / (trace_us * 1e-6) / 1e12 / peak, 4)
     # the unfused selection (scores given) over materialised fp32 scores, an
     # HBM-bound pass: the router's own scores of each input batch, dumped
     # once; timed in accumulate mode, so each call is exactly one launch of
@@ -374,6 +412,7 @@ def main() -> int:
                   + " (idb_select_from_scores, fp32 scores [T][E] read from HBM)",
         "kernel_us": round(sel_ms * 1000, 2),
         "bytes_per_launch": sel_bytes,
+        "traffic": load_traffic(wl.name, rs.info["variant"], "select"),
     }
     # the paper's diagnostics on the same step: the full-pool and top-K
     # routing entropies over this batch (scores [T][E] read from HBM), and
