@@ -18,7 +18,9 @@ readings of points the paper leaves open):
 * :func:`load_stats` -- MaxVio / MinVio (Eq. vio)
 * :func:`controller_diag` -- one update plus its diagnostics (active-gate
   fraction, busiest-10% share, inactive-expert ratio, mean |bias change|)
-* :func:`topk_entropy`, :func:`full_entropy` -- routing entropies (Sec. 4.3)
+* :func:`topk_entropy`, :func:`full_entropy`, :func:`softmax_entropy` -- routing
+  entropies (Sec. 4.3): top-K gate weights, clamped biased sigmoid scores, and
+  the auxiliary-loss router's softmax probabilities
 * :func:`qb_alpha`, :func:`qb_update` -- Quantile Balancing's cutoffs and
   target bias, with the EMA variant (Eq. pid-quantile, Eq. pid-quantile-def)
 * :func:`aux_stats`, :func:`aux_router` -- the auxiliary-loss router's
@@ -91,6 +93,8 @@ def _declare(lib):
     lib.oracle_topk_entropy.restype = ctypes.c_double
     lib.oracle_full_entropy.argtypes = [P, P, i64, i32]
     lib.oracle_full_entropy.restype = ctypes.c_double
+    lib.oracle_softmax_entropy.argtypes = [P, i64, i32]
+    lib.oracle_softmax_entropy.restype = ctypes.c_double
     lib.oracle_qb_alpha.argtypes = [P, P, i64, i32, i32, P]
     lib.oracle_qb_update.argtypes = [P, P, i64, i32, i32, f32, P]
     lib.oracle_aux_stats.argtypes = [P, i64, i32, i32, ctypes.c_double, P, P, P, P, P, P]
@@ -280,6 +284,13 @@ def full_entropy(scores: np.ndarray, bias: np.ndarray) -> float:
     s = np.ascontiguousarray(scores, dtype=np.float32)
     b = np.ascontiguousarray(bias, dtype=np.float32)
     return float(_load().oracle_full_entropy(_ptr(s), _ptr(b), s.shape[0], s.shape[1]))
+
+
+def softmax_entropy(z: np.ndarray) -> float:
+    """Mean over tokens of H_full over the softmax probabilities of fp32 logits ``z`` [T][E] (nats; the
+    auxiliary-loss router's full-pool entropy, Sec. 4.3)."""
+    a = np.ascontiguousarray(z, dtype=np.float32)
+    return float(_load().oracle_softmax_entropy(_ptr(a), a.shape[0], a.shape[1]))
 
 
 def aux_stats(z: np.ndarray, K: int, alpha: float):

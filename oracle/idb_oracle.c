@@ -27,6 +27,7 @@
  *          busiest-10% share, inactive-expert ratio, mean    rapid-gate and its figure;
  *          absolute bias change                              Sec. 4.3; Sec. 3 bias drift)
  *   H1, H2 top-K and full-pool score entropy               (Sec. 4.3)
+ *   H3  full-pool entropy of the softmax router scores     (Sec. 4.3)
  *   Q1..Q4 Quantile Balancing's target bias, with the EMA   (Eq. pid-quantile,
  *          variant used as a diagnostic                      Eq. pid-quantile-def; Sec. 3,
  *                                                            EMA smoothing of the target)
@@ -399,6 +400,30 @@ double oracle_full_entropy(const float* s, const float* bias, int64_t T, int32_t
                     h -= p * log(p);
                 }
             }
+        acc += h;
+    }
+    return acc / (double)T;
+}
+
+/* H3: mean over T tokens of H_full for the auxiliary-loss router, whose
+ * selection scores are the softmax probabilities over the router logits
+ * (Sec. 4.3): p_e = exp(z_e - M) / sum_e' exp(z_e' - M) with M the token's
+ * largest logit, H_full = -sum_e p_e log p_e (0 log 0 = 0), all in fp64 from
+ * the fp32 logits z [T][E]. */
+double oracle_softmax_entropy(const float* z, int64_t T, int32_t E) {
+    double acc = 0.0;
+    for (int64_t t = 0; t < T; ++t) {
+        const float* zt = z + t * (int64_t)E;
+        double m = (double)zt[0];
+        for (int32_t e = 1; e < E; ++e)
+            if ((double)zt[e] > m) m = (double)zt[e];
+        double Z = 0.0;
+        for (int32_t e = 0; e < E; ++e) Z += exp((double)zt[e] - m);
+        double h = 0.0;
+        for (int32_t e = 0; e < E; ++e) {
+            const double p = exp((double)zt[e] - m) / Z;
+            if (p > 0.0) h -= p * log(p);
+        }
         acc += h;
     }
     return acc / (double)T;

@@ -47,6 +47,10 @@ MUTANTS = {
     "aux-f-over-tk": ("f[i] = (double)counts[i] / (double)T;", "f[i] = (double)counts[i] / (double)(T * K);"),
     "aux-loss-misaligned": ("L = L + f[i] * P[i];", "L = L + f[i] * P[E - 1 - i];"),
     "aux-rank-ascending": ("const float v = (float)zt[i];", "const float v = -(float)zt[i];"),
+    "softmax-entropy-no-max-shift": ("for (int32_t e = 0; e < E; ++e) Z += exp((double)zt[e] - m);",
+                                     "for (int32_t e = 0; e < E; ++e) Z += exp((double)zt[e]);"),
+    "softmax-entropy-log2": ("if (p > 0.0) h -= p * log(p);", "if (p > 0.0) h -= p * log2(p);"),
+    "softmax-entropy-sum-over-tokens": ("    return acc / (double)T;\n}\n\n/* S1", "    return acc;\n}\n\n/* S1"),
 }
 
 

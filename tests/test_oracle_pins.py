@@ -683,3 +683,39 @@ def test_aux_large_logits_do_not_overflow():
     np.testing.assert_array_equal(idx, [[1], [1]])
     np.testing.assert_allclose(P, [0.25, 0.75], rtol=1e-12)
     assert loss == pytest.approx(0.75, rel=1e-12)
+
+
+def test_softmax_entropy_closed_forms_and_scipy():
+    """H_full of the auxiliary-loss router (Sec. 4.3): p = softmax(z), H = -sum p log p."""
+    from scipy.special import softmax
+    from scipy.stats import entropy
+    E = 768
+    # equal logits: the uniform distribution, H = log E
+    assert abs(oracle.softmax_entropy(np.full((3, E), 0.75, F32)) - np.log(E)) < 1e-12
+    # one logit far above the rest: p is one-hot to fp64 precision, H = 0
+    z = np.full((2, E), -200.0, F32)
+    z[:, 5] = 200.0
+    assert oracle.softmax_entropy(z) < 1e-150
+    # two levels: n1 experts at logit a, the rest at 0 -> closed form
+    n1, a = 10, 3.0
+    z = np.zeros((1, E), F32)
+    z[0, :n1] = a
+    Z = n1 * np.exp(a) + (E - n1)
+    p1, p0 = np.exp(a) / Z, 1.0 / Z
+    want = -(n1 * p1 * np.log(p1) + (E - n1) * p0 * np.log(p0))
+    assert abs(oracle.softmax_entropy(z) - want) < 1e-12
+    # random logits against scipy's softmax and entropy (natural logarithm)
+    g = np.random.default_rng(5)
+    z = (g.standard_normal((40, E)) * 2.0).astype(F32)
+    want = np.mean([entropy(softmax(row.astype(np.float64))) for row in z])
+    np.testing.assert_allclose(oracle.softmax_entropy(z), want, rtol=1e-12)
+    # shift invariance (logits on a 2^-10 grid below 16 in size: adding 64 is
+    # exact in fp32) and no overflow for logits far beyond exp's range
+    z = (np.round(z.astype(np.float64) * 1024.0) / 1024.0).astype(F32)
+    assert np.abs(z).max() < 16
+    zs = (z + F32(64.0)).astype(F32)
+    assert np.array_equal((zs - F32(64.0)).astype(F32), z)
+    np.testing.assert_allclose(oracle.softmax_entropy(zs), oracle.softmax_entropy(z), rtol=1e-12)
+    zb = (z.astype(np.float64) * 1000.0).astype(F32)
+    hb = oracle.softmax_entropy(zb)
+    assert np.isfinite(hb) and 0.0 <= hb < np.log(E)
