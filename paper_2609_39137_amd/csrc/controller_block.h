@@ -501,11 +501,13 @@ __device__ inline void controller_wave(const int32_t* __restrict__ counts, int E
 
 // Run by every thread of each workgroup of a launch once it is done with
 // counts: the workgroup that finishes last (ticket) runs controller_block on
-// the complete counts.  Every wave first waits for its own memory operations
-// (the count atomics) to complete; after the barrier one thread's agent-scope
-// release fence publishes the workgroup's writes before its ticket increment
-// (one L2 write-back per workgroup, not per wave), and the last workgroup's
-// acquire fence orders the ticket before its count reads.
+// the complete counts.  The counts are written only by agent-scope atomics
+// (performed at the device's coherence point) and read only by agent-scope
+// loads (served there too), so no cache write-back or invalidation is needed:
+// every wave waits for its own memory operations (the count atomics) to
+// complete, the barrier collects the workgroup, and one thread takes the
+// ticket; the last workgroup reads the counts after its ticket returns.  The
+// controller state it reads is written by no other workgroup of the launch.
 template <int kPer>
 __device__ inline void controller_tail(const int32_t* counts, int E, float Ki, float Kd, int sign_mode, int center,
                                        float* bias, float* e_prev, int64_t* step, int32_t* status, double* stats,
@@ -513,13 +515,10 @@ __device__ inline void controller_tail(const int32_t* counts, int E, float Ki, f
     __shared__ int last;
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
-    if (threadIdx.x == 0) {
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+    if (threadIdx.x == 0)
         last = __hip_atomic_fetch_add(ticket, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == gridDim.x - 1;
-    }
     __syncthreads();
     if (!last) return;
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
     controller_block<kPer, true>(counts, E, ctrl_tree_size(E), Ki, Kd, sign_mode, center, bias, e_prev, step, status,
                            stats, sh);
 }
