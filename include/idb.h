@@ -314,6 +314,19 @@ size_t idb_routing_entropy_workspace_bytes(void);
 idb_status idb_routing_entropy(const float* gate_w, int64_t T, int32_t K, const float* scores, const float* bias,
                                int32_t E, void* workspace, size_t workspace_bytes, double* out, hipStream_t stream);
 
+/* The same entropies for the auxiliary-loss router, whose full-pool selection
+ * scores are the softmax probabilities over its logits (Sec. 4.3):
+ *   out[0] = mean H_topK over gate_w [T][K] (as idb_routing_entropy);
+ *   out[1] = mean H_full, H_full = -sum_e p_e log p_e, p = softmax(z) over the
+ *            fp32 logits [T][E] (idb_aux_router_forward's logits_dump), taken
+ *            as log Z - (sum_e t_e (z_e - M)) / Z with M the token's largest
+ *            logit, t_e = exp(z_e - M) from the hardware fp32 exponential and
+ *            Z = sum_e t_e, both sums in fp64.
+ * Workspace and determinism as idb_routing_entropy; 1 <= T <= 2^26,
+ * 1 <= K <= 32, 1 <= E <= 1024; finite logits. */
+idb_status idb_routing_entropy_softmax(const float* gate_w, int64_t T, int32_t K, const float* logits, int32_t E,
+                                       void* workspace, size_t workspace_bytes, double* out, hipStream_t stream);
+
 /* ---------------------------------------------------------------------------
  * Quantile Balancing (Eq. pid-quantile, Eq. pid-quantile-def): the paper's
  * strongest baseline controller, on the same fused router.

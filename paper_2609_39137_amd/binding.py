@@ -36,7 +36,7 @@ EXPORTED = (
     "idb_controller_step", "idb_router_step", "idb_qb_router_workspace_bytes", "idb_qb_router_forward",
     "idb_qb_update", "idb_controller_update_layers", "idb_routing_entropy_workspace_bytes", "idb_routing_entropy",
     "idb_aux_router_workspace_bytes", "idb_aux_router_forward", "idb_router_merge_step",
-    "idb_router_step_noalloc",
+    "idb_router_step_noalloc", "idb_routing_entropy_softmax",
 )
 
 
@@ -113,6 +113,8 @@ def lib() -> ctypes.CDLL:
     L.idb_routing_entropy_workspace_bytes.restype = sz
     L.idb_routing_entropy.argtypes = [P, i64, i32, P, P, i32, P, sz, P, P]
     L.idb_routing_entropy.restype = ctypes.c_int
+    L.idb_routing_entropy_softmax.argtypes = [P, i64, i32, P, i32, P, sz, P, P]
+    L.idb_routing_entropy_softmax.restype = ctypes.c_int
     L.idb_aux_router_workspace_bytes.argtypes = [i64, i32, i32, i32, i32, i32]
     L.idb_aux_router_workspace_bytes.restype = sz
     L.idb_aux_router_forward.argtypes = [P, P, i32, i32, i64, i32, i32, i32, ctypes.c_double, P, P, P, P, P, P, P,
@@ -466,3 +468,19 @@ def idb_routing_entropy(gate_w, out, scores=None, bias=None, workspace=None, str
     st = lib().idb_routing_entropy(_ptr(gate_w), T, K, _ptr(scores), _ptr(bias), E, _ptr(workspace),
                                    workspace.numel(), _ptr(out), _stream(stream))
     _check("idb_routing_entropy", st)
+
+
+def idb_routing_entropy_softmax(gate_w, logits, out, workspace=None, stream=None):
+    """Mean top-K entropy of ``gate_w`` and mean full-pool entropy of softmax(``logits``) (nats; the
+    auxiliary-loss router's score family) into the device double[2] ``out``."""
+    T, K = gate_w.shape
+    if logits.dim() != 2 or logits.shape[0] != T or logits.dtype != torch.float32:
+        raise ValueError("logits must be float32 [T][E]")
+    if out.dtype != torch.float64 or out.numel() != 2:
+        raise ValueError("out must be a float64 tensor of 2 elements")
+    if workspace is None:
+        workspace = torch.empty(int(lib().idb_routing_entropy_workspace_bytes()), dtype=torch.uint8,
+                                device=gate_w.device)
+    st = lib().idb_routing_entropy_softmax(_ptr(gate_w), T, K, _ptr(logits), logits.shape[1], _ptr(workspace),
+                                           workspace.numel(), _ptr(out), _stream(stream))
+    _check("idb_routing_entropy_softmax", st)

@@ -547,8 +547,23 @@ idb_status idb_routing_entropy(const float* gate_w, int64_t T, int32_t K, const 
     if (!aligned(gate_w, 4) || !aligned(out, 8) || !aligned(workspace, 8) || (scores && !aligned(scores, 4)) ||
         (bias && !aligned(bias, 4)))
         return fail(IDB_ERR_INVALID_ARG, "misaligned buffer");
-    return hip_result(idb::launch_routing_entropy(gate_w, T, K, scores, bias, E, static_cast<double*>(workspace), out,
-                                                  stream),
+    return hip_result(idb::launch_routing_entropy(gate_w, T, K, scores, bias, E, 0, static_cast<double*>(workspace),
+                                                  out, stream),
+                      "routing entropy launch");
+}
+
+idb_status idb_routing_entropy_softmax(const float* gate_w, int64_t T, int32_t K, const float* logits, int32_t E,
+                                       void* workspace, size_t workspace_bytes, double* out, hipStream_t stream) {
+    if (!gate_w || !logits || !out || !workspace) return fail(IDB_ERR_INVALID_ARG, "null pointer");
+    if (T < 1 || T > kMaxTokens) return fail(IDB_ERR_INVALID_ARG, "T=%lld out of [1, 2^26]", (long long)T);
+    if (K < 1 || K > kMaxKGpu) return fail(IDB_ERR_INVALID_ARG, "K=%d out of [1, %d]", K, kMaxKGpu);
+    if (E < 1 || E > kMaxExperts) return fail(IDB_ERR_INVALID_ARG, "E=%d out of [1, %d]", E, kMaxExperts);
+    if (workspace_bytes < idb_routing_entropy_workspace_bytes())
+        return fail(IDB_ERR_INVALID_ARG, "workspace of %zu bytes needed", idb_routing_entropy_workspace_bytes());
+    if (!aligned(gate_w, 4) || !aligned(out, 8) || !aligned(workspace, 8) || !aligned(logits, 4))
+        return fail(IDB_ERR_INVALID_ARG, "misaligned buffer");
+    return hip_result(idb::launch_routing_entropy(gate_w, T, K, logits, nullptr, E, 1,
+                                                  static_cast<double*>(workspace), out, stream),
                       "routing entropy launch");
 }
 

@@ -6,6 +6,10 @@
 //            (H_full = 0 when C = 0), each c_e log2 c_e with the hardware
 //            fp32 log2 and summed in fp64 (terms with c_e below the smallest
 //            normal fp32 count as 0).
+// The softmax form (the auxiliary-loss router, whose selection scores are the
+// softmax probabilities of its logits): H_full = log Z - (sum_e t_e (z_e - M))
+// / Z with M the token's largest logit, t_e = exp(z_e - M) from the hardware
+// exp2 in fp32 and Z = sum_e t_e, both sums in fp64.
 // Deterministic: a fixed grid of kEntropyBlocks workgroups with fixed token
 // assignments and fixed reduction trees writes per-workgroup partial sums,
 // which one wave adds in a fixed order.
@@ -41,6 +45,33 @@ __device__ inline double clog2c(float c) {
     return c >= 1.17549435e-38f ? (double)c * (double)__builtin_amdgcn_logf(c) : 0.0;
 }
 
+// One token's H_full over the softmax of its logits z (one wave, lane l
+// holding z_{l + 64 j}; padding lanes -inf).
+__device__ inline double softmax_entropy_wave(const float (&z)[kEntPerLane]) {
+    float m = -INFINITY;
+#pragma unroll
+    for (int j = 0; j < kEntPerLane; ++j) m = fmaxf(m, z[j]);
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) m = fmaxf(m, __shfl_xor(m, o));
+    double Z = 0.0, D = 0.0;
+#pragma unroll
+    for (int j = 0; j < kEntPerLane; ++j) {
+        if (z[j] != -INFINITY) {
+            const float x = z[j] - m;
+            const float t = __builtin_amdgcn_exp2f(x * 1.4426950408889634f);
+            Z += (double)t;
+            D += (double)t * (double)x;
+        }
+    }
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) {
+        Z += __shfl_xor(Z, o);
+        D += __shfl_xor(D, o);
+    }
+    return log(Z) - D / Z;
+}
+
+template <bool SOFTMAX>
 __global__ __launch_bounds__(kEntThreads) void entropy_partial_kernel(const float* __restrict__ w, int64_t T, int K,
                                                                       const float* __restrict__ scores,
                                                                       const float* __restrict__ bias, int E,
@@ -61,7 +92,19 @@ __global__ __launch_bounds__(kEntThreads) void entropy_partial_kernel(const floa
     // H_full: one wave per token, a lane's experts lane, lane + 64, ...; the
     // bias stays in registers, and two tokens' scores are loaded at once
     double hfull = 0.0;
-    if (scores) {
+    if (SOFTMAX) {
+        // one wave per token, a lane's logits lane, lane + 64, ...
+        for (int64_t t = (int64_t)blockIdx.x * kEntWaves + wv; t < T; t += (int64_t)gridDim.x * kEntWaves) {
+            float z[kEntPerLane];
+#pragma unroll
+            for (int j = 0; j < kEntPerLane; ++j) {
+                const int e = lane + 64 * j;
+                z[j] = e < E ? scores[t * E + e] : -INFINITY;
+            }
+            const double h = softmax_entropy_wave(z);
+            if (lane == 0) hfull += h;
+        }
+    } else if (scores) {
         float b[kEntPerLane];
 #pragma unroll
         for (int j = 0; j < kEntPerLane; ++j) b[j] = lane + 64 * j < E ? bias[lane + 64 * j] : 0.0f;
@@ -132,9 +175,13 @@ __global__ __launch_bounds__(64) void entropy_final_kernel(const double* __restr
 }  // namespace
 
 hipError_t launch_routing_entropy(const float* gate_w, int64_t T, int K, const float* scores, const float* bias,
-                                  int E, double* partial, double* out, hipStream_t stream) {
-    hipLaunchKernelGGL(entropy_partial_kernel, dim3(kEntropyBlocks), dim3(kEntThreads), 0, stream, gate_w, T, K,
-                       scores, bias, E, partial);
+                                  int E, int softmax, double* partial, double* out, hipStream_t stream) {
+    if (softmax)
+        hipLaunchKernelGGL(entropy_partial_kernel<true>, dim3(kEntropyBlocks), dim3(kEntThreads), 0, stream, gate_w,
+                           T, K, scores, bias, E, partial);
+    else
+        hipLaunchKernelGGL(entropy_partial_kernel<false>, dim3(kEntropyBlocks), dim3(kEntThreads), 0, stream, gate_w,
+                           T, K, scores, bias, E, partial);
     hipLaunchKernelGGL(entropy_final_kernel, dim3(1), dim3(64), 0, stream, partial, kEntropyBlocks, T,
                        scores ? 1 : 0, out);
     return hipGetLastError();

@@ -17,10 +17,11 @@ hipError_t launch_load_stats(const int32_t* counts, int E, double* out, hipStrea
 hipError_t launch_controller_layers(const int32_t* counts, int L, int E, float Ki, float Kd, int sign_mode,
                                     int center, float* bias, float* e_prev, int64_t* step, int32_t* status,
                                     double* stats, double* diag, hipStream_t stream);
-// Routing entropies: partial sums into workspace [kEntropyBlocks][2], then the means into out[2].
+// Routing entropies: partial sums into workspace [kEntropyBlocks][2], then the means into out[2]; softmax:
+// H_full over the softmax of the logits in scores (bias unused).
 constexpr int kEntropyBlocks = 512;
 hipError_t launch_routing_entropy(const float* gate_w, int64_t T, int K, const float* scores, const float* bias,
-                                  int E, double* partial, double* out, hipStream_t stream);
+                                  int E, int softmax, double* partial, double* out, hipStream_t stream);
 
 // Auxiliary-loss statistics from the router's per-tile softmax column sums
 // prob_part [tiles][E] and counts cnt_part [tiles][E]: counts [E], f [E],

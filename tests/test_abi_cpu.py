@@ -383,3 +383,16 @@ def test_noalloc_step_rejects_before_any_hip_call():
     assert call(x=None) == B.IDB_ERR_INVALID_ARG
     assert call(K=33) == B.IDB_ERR_UNSUPPORTED
     assert call(state=B.idb_controller_state(A16, None, A16, A16)) == B.IDB_ERR_INVALID_ARG
+
+
+def test_softmax_entropy_rejects_invalid_arguments():
+    L = B.lib()
+    ws = B.idb_routing_entropy_workspace_bytes() if hasattr(B, "idb_routing_entropy_workspace_bytes") else 1 << 20
+    call = L.idb_routing_entropy_softmax
+    assert call(A16, 128, 10, None, 768, A16, 1 << 20, A16, None) == B.IDB_ERR_INVALID_ARG   # no logits
+    assert call(A16, 0, 10, A16, 768, A16, 1 << 20, A16, None) == B.IDB_ERR_INVALID_ARG     # T = 0
+    assert call(A16, 128, 33, A16, 768, A16, 1 << 20, A16, None) == B.IDB_ERR_INVALID_ARG   # K > 32
+    assert call(A16, 128, 10, A16, 2048, A16, 1 << 20, A16, None) == B.IDB_ERR_INVALID_ARG  # E > 1024
+    assert call(A16, 128, 10, A16, 768, A16, 8, A16, None) == B.IDB_ERR_INVALID_ARG         # workspace too small
+    assert call(A16, 128, 10, A16 + 2, 768, A16, 1 << 20, A16, None) == B.IDB_ERR_INVALID_ARG  # misaligned
+    assert ws > 0

@@ -95,3 +95,34 @@ def test_routing_entropy_matches_oracle(T, E, K):
     B.idb_routing_entropy(wt, out)  # without scores: H_full is NaN
     got2 = out.cpu().numpy()
     assert got2[0] == got[0] and np.isnan(got2[1])
+
+
+@pytest.mark.parametrize("T,E,K,scale", [(2048, 768, 10, 1.0), (1000, 64, 4, 3.0), (333, 1024, 32, 0.3),
+                                         (129, 768, 10, 40.0)])
+def test_softmax_routing_entropy_matches_oracle(T, E, K, scale):
+    """H_full of the auxiliary-loss router over softmax(z) (Sec. 4.3).  Bound of
+    the kernel's error per token: t_e = exp(x_e) (1 + d_e) with x_e = z_e - M,
+    |d_e| <= (1.5 |x_e| + 1) 2^-23 (the rounded difference, the product with
+    log2 e and the hardware exp2), and H = log Z - sum t x / Z moves by
+    sum_e p_e d_e (1 - log p_e - H), plus sum_e p_e |x_e| 2^-24 from the
+    rounded x in the second sum; the fp64 sums add far less."""
+    r = synth.rng(T, E, K, 5)
+    z = (r.standard_normal((T, E)) * scale).astype(np.float32)
+    z[3] = np.float32(0.5)  # equal logits: H = log E
+    w = r.random((T, K)).astype(np.float32) + np.float32(1e-3)
+    w = (w / w.sum(axis=1, keepdims=True)).astype(np.float32)
+    out = torch.empty(2, dtype=torch.float64, device=DEV)
+    B.idb_routing_entropy_softmax(torch.from_numpy(w).to(DEV), torch.from_numpy(z).to(DEV), out)
+    got = out.cpu().numpy()
+    np.testing.assert_allclose(got[0], oracle.topk_entropy(w), rtol=1e-9)
+    x = z.astype(np.float64) - z.max(axis=1, keepdims=True).astype(np.float64)
+    p = np.exp(x)
+    p /= p.sum(axis=1, keepdims=True)
+    with np.errstate(divide="ignore", invalid="ignore"):
+        lp = np.where(p > 0, np.log(np.where(p > 0, p, 1.0)), 0.0)
+    H = -(p * lp).sum(axis=1, keepdims=True)
+    d = (1.5 * np.abs(x) + 1.0) * 2.0 ** -23
+    per_token = (p * d * np.abs(1.0 - lp - H)).sum(axis=1) + (p * np.abs(x)).sum(axis=1) * 2.0 ** -24
+    tol = per_token.mean() + 1e-12
+    want = oracle.softmax_entropy(z)
+    assert abs(got[1] - want) <= tol, (got[1], want, tol)
