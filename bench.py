@@ -506,7 +506,7 @@ def kernel_time_in_steps(args, rs, W, xs, nbuf, stream):
         # the steps then run back to back from the queue (the host launches
         # more slowly than the GPU runs them; without it the launch gaps would
         # fall inside the event pairs)
-        torch.cuda._sleep(40_000_000)
+        torch.cuda._sleep(12_000_000)
         for i in range(nbuf):
             split_step(i, False)
         for i in range(n):
