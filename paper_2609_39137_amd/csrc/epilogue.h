@@ -269,24 +269,13 @@ __device__ __forceinline__ void epi_tile(const RouterArgs& a, int NS, int slice,
                 for (int o = 1; o < C::TPT; o <<= 1) zsum = zsum + __shfl_xor(zsum, o);
             }
         }
-        // Bit j: v_j >= tau.  For a finite tau it is read off the sign of
-        // v_j - tau: x - y is +0 exactly when x == y (round to nearest) and
-        // -inf - tau < 0; tau = +-0 is taken as -0, so that v_j = -0 and
-        // v_j = +0 (both equal to tau) give +0.  An infinite tau (a sum that
-        // overflowed, or fewer than K finite values) compares directly, as
-        // inf - inf would be NaN.  Padding columns are masked out.
+        // Bit j: v_j >= tau, an IEEE comparison (-0 == +0; every real value
+        // reaches tau = -inf).  Padding columns are masked out.
         unsigned msk[C::MW];
 #pragma unroll
         for (int w = 0; w < C::MW; ++w) msk[w] = 0u;
-        if (__builtin_isfinite(tau)) {  // uniform over the token's threads
-            const float taum = (tau == 0.0f) ? -0.0f : tau;
 #pragma unroll
-            for (int j = 0; j < C::VPT; ++j)
-                msk[j / 32] |= ((__float_as_uint(v[j] - taum) >> 31) ^ 1u) << (j % 32);
-        } else {
-#pragma unroll
-            for (int j = 0; j < C::VPT; ++j) msk[j / 32] |= (v[j] >= tau ? 1u : 0u) << (j % 32);
-        }
+        for (int j = 0; j < C::VPT; ++j) msk[j / 32] |= (v[j] >= tau ? 1u : 0u) << (j % 32);
         int mine_n = 0;
 #pragma unroll
         for (int w = 0; w < C::MW; ++w) {
