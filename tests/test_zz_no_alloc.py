@@ -72,3 +72,39 @@ def test_noalloc_rejects_shapes_beyond_the_scratch():
     assert ei.value.status == B.IDB_ERR_UNSUPPORTED
     torch.cuda.synchronize()
     assert torch.all(counts == 5)  # nothing was enqueued
+
+
+def test_noalloc_step_captured_in_a_graph_replays_like_eager():
+    """The callers this entry point serves capture it: a graph of one step
+    replayed four times (fresh inputs copied in between, eager work and
+    synchronisation between the replays) equals the eager workspace calls."""
+    T, d, E, K = 2048, 256, 768, 10
+    cfg = B.ControllerCfg(E, 6e-3, 6e-3)
+    _, W = synth.normal_router_inputs(8, d, E, seed=43)
+    Wt = _bf16(W)
+    xs = [_bf16(synth.normal_router_inputs(T, d, E, seed=60 + t)[0]) for t in range(4)]
+    x = torch.empty_like(xs[0])
+    st = B.ControllerState(E, DEV)
+    idx = torch.empty((T, K), dtype=torch.int32, device=DEV)
+    w = torch.empty((T, K), dtype=torch.float32, device=DEV)
+    counts = torch.empty(E, dtype=torch.int32, device=DEV)
+    stats = torch.empty(2, dtype=torch.float64, device=DEV)
+    ref = RouterStep(T, d, E, K, torch.bfloat16, cfg=cfg)
+    side = torch.cuda.Stream()
+    x.copy_(xs[0])
+    # one eager call (on a throwaway state) before capture: the scratch
+    # address is looked up on a device's first call
+    B.idb_router_step_noalloc(x, Wt, K, cfg, B.ControllerState(E, DEV), idx, w, counts, out=stats)
+    torch.cuda.synchronize()
+    print(f"[noalloc] graph capture T={T} E={E} K={K}", flush=True)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=side):
+        B.idb_router_step_noalloc(x, Wt, K, cfg, st, idx, w, counts, out=stats)
+    for t, xt in enumerate(xs):
+        x.copy_(xt)
+        g.replay()
+        ref.step(xt, Wt)
+        torch.cuda.synchronize()
+        for a, b in ((idx, ref.idx), (w, ref.w), (counts, ref.counts), (stats, ref.stats), (st.bias, ref.state.bias),
+                     (st.e_prev, ref.state.e_prev), (st.step, ref.state.step)):
+            np.testing.assert_array_equal(_bits(a), _bits(b), err_msg=f"replay {t}")
