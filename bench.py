@@ -341,10 +341,10 @@ def main() -> int:
 
     # live timing of the dominant kernel inside steps like the timed ones: the
     # same calls split at the kernel boundary (pack, the fused router kernel,
-    # the slice merge with the update; idb_router_score_select +
+    # the slice merge with the update; idb_router_score_select_timed +
     # idb_router_merge_step enqueue exactly the kernels of idb_router_step),
-    # with a pair of HIP events on the benchmark's stream around every router
-    # kernel launch
+    # each router launch writing its own start and end into a pair of HIP
+    # events on the benchmark's stream
     k1_ms, k1_how = kernel_time_in_steps(args, rs, W, xs, nbuf, stream)
     log(f"fused router kernel: {k1_ms * 1000:.2f} us/launch ({k1_how})")
 
@@ -364,9 +364,9 @@ def main() -> int:
         "kernel_timing": k1_how,
         "flops_per_launch": flops,
     }
-    # the committed kernel trace of this command: the kernel's own execution
-    # time (the event pairs above also hold the dispatch and the events' own
-    # cost, a few us); reported beside, frac above is from the live events
+    # the committed kernel trace of this command (the kernel's average over
+    # every launch of that run), reported beside; frac above is from the live
+    # events
     trace_us = load_kernel_trace_us(wl.name)
     roofline["kernel_trace_us"] = trace_us
     roofline["frac_kernel_trace"] = None if trace_us is None else round(flops / (trace_us * 1e-6) / 1e12 / peak, 4)
@@ -480,25 +480,28 @@ def main() -> int:
 def kernel_time_in_steps(args, rs, W, xs, nbuf, stream):
     """Average duration of the fused router kernel over ``args.steps`` steps like the timed ones.
 
-    Each step is pack + idb_router_score_select + idb_router_merge_step (the
-    kernels of idb_router_step), with HIP events recorded on the stream right
-    before and after the router kernel.  The steps are launched eagerly: on
-    ROCm, events recorded inside a captured graph carry no timestamps (only
-    external events would, and they are not available there).  All steps are
-    enqueued while a spin kernel holds the stream; nbuf untimed steps run
-    first."""
+    Each step is pack + idb_router_score_select_timed + idb_router_merge_step
+    (the kernels of idb_router_step): the router kernel is started by an
+    extended launch that writes its own start and end timestamps into a pair
+    of HIP events on the benchmark's stream, so each interval is that
+    kernel's execution (no dispatch, no separately recorded events).  The
+    steps are launched eagerly: on ROCm, events recorded inside a captured
+    graph carry no timestamps (only external events would, and they are not
+    available there).  All steps are enqueued while a spin kernel holds the
+    stream, so they run back to back like the timed ones; nbuf untimed steps
+    run first."""
     import torch
 
     n = max(args.steps, nbuf)
     pairs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n)]
+    for a, b in pairs:  # torch creates an event on its first record
+        a.record(stream)
+        b.record(stream)
+    torch.cuda.synchronize()
 
     def split_step(i, timed):
         rs.pack(W, stream=stream)
-        if timed:
-            pairs[i][0].record(stream)
-        rs.score_select(xs[i % nbuf], None, stream=stream)
-        if timed:
-            pairs[i][1].record(stream)
+        rs.score_select(xs[i % nbuf], None, stream=stream, events=pairs[i] if timed else None)
         rs.merge_step(stream=stream)
 
     with torch.cuda.stream(stream):
@@ -513,8 +516,8 @@ def kernel_time_in_steps(args, rs, W, xs, nbuf, stream):
             split_step(i, True)
     torch.cuda.synchronize()
     ms = sum(a.elapsed_time(b) for a, b in pairs) / n
-    return ms, (f"HIP events around each router kernel launch in {n} steps (pack, router, merge + update) enqueued "
-                f"behind a spin kernel and run back to back")
+    return ms, (f"HIP events taking each router kernel's own start and end (extended launch) in {n} steps "
+                f"(pack, router, merge + update) enqueued behind a spin kernel and run back to back")
 
 
 def _gen_batch(name: str, step: int) -> np.ndarray:

@@ -146,6 +146,23 @@ idb_status idb_router_merge(int64_t T, int32_t d, int32_t E, int32_t K, idb_dtyp
                             float* gate_w, int32_t* counts, void* workspace, size_t workspace_bytes,
                             int32_t variant, hipStream_t stream);
 
+/* idb_router_score_select for measurement: the same arguments, checks and
+ * outputs, with the fused router kernel started by an extended launch that
+ * writes that kernel's own start and end timestamps into start_event and
+ * stop_event (HIP events the caller created, e.g. with hipEventCreate; either
+ * may be null, and with both null this is idb_router_score_select).  The
+ * elapsed time between the two events is the kernel's execution time alone,
+ * without the dispatch of the launch or the cost of separately recorded
+ * events; a counts-zeroing launch that precedes the kernel (single-slice
+ * tilings) is outside the interval.  The events must belong to the device
+ * of `stream` and must not be recorded elsewhere until the kernel is done. */
+idb_status idb_router_score_select_timed(const void* x, const void* W_g, idb_dtype dtype,
+                                         idb_weight_layout weight_layout, const float* bias, int64_t T, int32_t d,
+                                         int32_t E, int32_t K, int32_t* expert_idx, float* gate_w, int32_t* counts,
+                                         int32_t accumulate_counts, float* scores_dump, void* workspace,
+                                         size_t workspace_bytes, int32_t variant, hipStream_t stream,
+                                         hipEvent_t start_event, hipEvent_t stop_event);
+
 /* The router matrix in the layout the MFMA A operands are read in: for every
  * 16-expert block b, 128-byte chunk c of the rows and 64-byte half s < 2 of
  * the chunk, one contiguous 1 KB piece, at byte ((b*NCH + c)*2 + s)*1024 with

@@ -36,7 +36,7 @@ EXPORTED = (
     "idb_controller_step", "idb_router_step", "idb_qb_router_workspace_bytes", "idb_qb_router_forward",
     "idb_qb_update", "idb_controller_update_layers", "idb_routing_entropy_workspace_bytes", "idb_routing_entropy",
     "idb_aux_router_workspace_bytes", "idb_aux_router_forward", "idb_router_merge_step",
-    "idb_router_step_noalloc", "idb_routing_entropy_softmax",
+    "idb_router_step_noalloc", "idb_routing_entropy_softmax", "idb_router_score_select_timed",
 )
 
 
@@ -74,6 +74,8 @@ def lib() -> ctypes.CDLL:
     for name in ("idb_router_forward", "idb_router_score_select"):
         getattr(L, name).argtypes = router_args
         getattr(L, name).restype = ctypes.c_int
+    L.idb_router_score_select_timed.argtypes = router_args + [P, P]
+    L.idb_router_score_select_timed.restype = ctypes.c_int
     L.idb_router_merge.argtypes = [i64, i32, i32, i32, i32, P, P, P, P, sz, i32, P]
     L.idb_router_merge.restype = ctypes.c_int
     L.idb_router_packed_weight_bytes.argtypes = [i32, i32, i32]
@@ -190,7 +192,7 @@ def idb_router_pack_weight(W_g, W_packed, stream=None):
 
 
 def _router_call(fn: str, x, W_g, bias, K, expert_idx, gate_w, counts, accumulate, scores_dump, workspace,
-                 variant, stream, weight_layout=IDB_WEIGHT_ROW_MAJOR):
+                 variant, stream, weight_layout=IDB_WEIGHT_ROW_MAJOR, extra=()):
     T, d = x.shape
     E = W_g.shape[0]
     if W_g.shape[1] != d or W_g.dtype != x.dtype or bias.shape != (E,) or bias.dtype != torch.float32:
@@ -203,7 +205,7 @@ def _router_call(fn: str, x, W_g, bias, K, expert_idx, gate_w, counts, accumulat
     st = getattr(lib(), fn)(_ptr(x), _ptr(W_g), _dtype_code(x), int(weight_layout), _ptr(bias), T, d, E, K,
                             _ptr(expert_idx),
                             _ptr(gate_w), _ptr(counts), int(bool(accumulate)), _ptr(scores_dump),
-                            _ptr(workspace), ws_bytes, int(variant), _stream(stream))
+                            _ptr(workspace), ws_bytes, int(variant), _stream(stream), *extra)
     _check(fn, st)
 
 
@@ -218,6 +220,25 @@ def idb_router_score_select(x, W_g, bias, K, expert_idx, gate_w, counts, accumul
                             workspace=None, variant=0, stream=None, weight_layout=IDB_WEIGHT_ROW_MAJOR):
     _router_call("idb_router_score_select", x, W_g, bias, K, expert_idx, gate_w, counts, accumulate, scores_dump,
                  workspace, variant, stream, weight_layout)
+
+
+def _event_handle(ev) -> int | None:
+    """Raw HIP event of a ``torch.cuda.Event`` (recorded once, so it exists), or None."""
+    if ev is None:
+        return None
+    if not getattr(ev, "cuda_event", 0):
+        raise ValueError("record the event once before passing it (torch creates events on first record)")
+    return int(ev.cuda_event)
+
+
+def idb_router_score_select_timed(x, W_g, bias, K, expert_idx, gate_w, counts, start_event, stop_event,
+                                  accumulate=False, scores_dump=None, workspace=None, variant=0, stream=None,
+                                  weight_layout=IDB_WEIGHT_ROW_MAJOR):
+    """:func:`idb_router_score_select` with the fused kernel's own start and end timestamps written into the
+    two ``torch.cuda.Event`` objects (``enable_timing=True``, each recorded once beforehand)."""
+    _router_call("idb_router_score_select_timed", x, W_g, bias, K, expert_idx, gate_w, counts, accumulate,
+                 scores_dump, workspace, variant, stream, weight_layout,
+                 extra=(_event_handle(start_event), _event_handle(stop_event)))
 
 
 def idb_router_merge(T, d, E, K, dtype, expert_idx, gate_w, counts, workspace=None, variant=0, stream=None):

@@ -194,13 +194,15 @@ idb_status prepare_router(const void* x, const void* W_g, idb_dtype dtype, idb_w
     return IDB_OK;
 }
 
-idb_status enqueue_score_select(const RouterCall& c, int32_t accumulate_counts, hipStream_t stream) {
+idb_status enqueue_score_select(const RouterCall& c, int32_t accumulate_counts, hipStream_t stream,
+                                hipEvent_t start = nullptr, hipEvent_t stop = nullptr) {
     const int ns = idb::router_slices(c.tiling, c.args.E);
     if (ns <= 1 && !accumulate_counts && !c.args.cnt_part) {
         idb_status st = hip_result(idb::launch_fill_i32(c.args.counts, 0, c.args.E, stream), "zero counts");
         if (st != IDB_OK) return st;
     }
-    return hip_result(idb::launch_router_score_select(c.tiling, c.args, stream), "router score/select launch");
+    return hip_result(idb::launch_router_score_select(c.tiling, c.args, stream, start, stop),
+                      "router score/select launch");
 }
 
 }  // namespace
@@ -239,6 +241,19 @@ idb_status idb_router_score_select(const void* x, const void* W_g, idb_dtype dty
                                    scores_dump, workspace, workspace_bytes, variant, true, &c);
     if (st != IDB_OK) return st;
     return enqueue_score_select(c, accumulate_counts, stream);
+}
+
+idb_status idb_router_score_select_timed(const void* x, const void* W_g, idb_dtype dtype,
+                                         idb_weight_layout weight_layout, const float* bias, int64_t T, int32_t d,
+                                         int32_t E, int32_t K, int32_t* expert_idx, float* gate_w, int32_t* counts,
+                                         int32_t accumulate_counts, float* scores_dump, void* workspace,
+                                         size_t workspace_bytes, int32_t variant, hipStream_t stream,
+                                         hipEvent_t start_event, hipEvent_t stop_event) {
+    RouterCall c;
+    idb_status st = prepare_router(x, W_g, dtype, weight_layout, bias, T, d, E, K, expert_idx, gate_w, counts, accumulate_counts,
+                                   scores_dump, workspace, workspace_bytes, variant, true, &c);
+    if (st != IDB_OK) return st;
+    return enqueue_score_select(c, accumulate_counts, stream, start_event, stop_event);
 }
 
 idb_status idb_router_merge(int64_t T, int32_t d, int32_t E, int32_t K, idb_dtype dtype, int32_t* expert_idx,

@@ -122,7 +122,10 @@ struct CtrlArgs {
     unsigned* ticket;
 };
 
-hipError_t launch_router_score_select(const RouterTiling& t, const RouterArgs& a, hipStream_t stream);
+// start/stop: nullable events that take the kernel's own start and end
+// timestamps (an extended launch; measurement only).
+hipError_t launch_router_score_select(const RouterTiling& t, const RouterArgs& a, hipStream_t stream,
+                                      hipEvent_t start = nullptr, hipEvent_t stop = nullptr);
 // ctrl: nullable; with it, the merge also runs the controller update on the
 // finished counts (multi-slice tilings only).
 hipError_t launch_router_merge(const RouterTiling& t, const RouterArgs& a, const CtrlArgs* ctrl,

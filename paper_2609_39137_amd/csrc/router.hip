@@ -41,6 +41,8 @@
 #include "epilogue.h"
 #include "internal.h"
 
+#include <hip/hip_ext.h>
+
 #pragma clang fp contract(off)
 
 namespace idb {
@@ -690,44 +692,54 @@ __global__ void pack_weight_kernel(const char* __restrict__ W, char* __restrict_
     }
 }
 
+// One launch of kernel k; with an event set, an extended launch that records
+// the kernel's own start and end timestamps in them.
+template <class Kern>
+hipError_t launch_kernel(Kern k, int64_t blocks, int threads, const RouterArgs& a, int NS, hipStream_t stream,
+                         hipEvent_t start, hipEvent_t stop) {
+    if (start || stop)
+        hipExtLaunchKernelGGL(k, dim3((unsigned)blocks), dim3(threads), 0, stream, start, stop, 0, a, NS);
+    else
+        hipLaunchKernelGGL(k, dim3((unsigned)blocks), dim3(threads), 0, stream, a, NS);
+    return hipGetLastError();
+}
+
 template <bool F32, bool PACKED, int WAVES, int TBW, int NBLK, bool SM = false>
-hipError_t launch32(const RouterArgs& a, int NS, hipStream_t stream) {
+hipError_t launch32(const RouterArgs& a, int NS, hipStream_t stream, hipEvent_t start, hipEvent_t stop) {
     using C = Cfg32<F32, WAVES, TBW, NBLK>;
     const int64_t blocks = (a.T + C::BT - 1) / C::BT * NS;
-    hipLaunchKernelGGL((router32_kernel<F32, PACKED, WAVES, TBW, NBLK, SM>), dim3((unsigned)blocks), dim3(C::NT), 0,
-                       stream, a, NS);
-    return hipGetLastError();
+    return launch_kernel(router32_kernel<F32, PACKED, WAVES, TBW, NBLK, SM>, blocks, C::NT, a, NS, stream, start,
+                         stop);
 }
 
 template <bool PACKED, int WAVES, int TT, int ET, bool SM = false>
-hipError_t launch16(const RouterArgs& a, int NS, hipStream_t stream) {
+hipError_t launch16(const RouterArgs& a, int NS, hipStream_t stream, hipEvent_t start, hipEvent_t stop) {
     using C = Cfg16<WAVES, TT, ET>;
     const int64_t blocks = (a.T + C::BT - 1) / C::BT * NS;
-    hipLaunchKernelGGL((router16_kernel<PACKED, WAVES, TT, ET, SM>), dim3((unsigned)blocks), dim3(C::NT), 0, stream,
-                       a, NS);
-    return hipGetLastError();
+    return launch_kernel(router16_kernel<PACKED, WAVES, TT, ET, SM>, blocks, C::NT, a, NS, stream, start, stop);
 }
 
 template <bool PACKED>
-hipError_t launch_layout(const RouterTiling& t, const RouterArgs& a, int NS, hipStream_t stream) {
+hipError_t launch_layout(const RouterTiling& t, const RouterArgs& a, int NS, hipStream_t stream, hipEvent_t e0,
+                         hipEvent_t e1) {
     if (a.softmax) {
         // softmax mode: compiled for the tilings marked in kTilings only
         switch (t.id) {
-            case 2: return launch32<false, PACKED, 8, 2, 3, true>(a, NS, stream);
-            case 4: return launch32<false, PACKED, 4, 4, 1, true>(a, NS, stream);
-            case 5: return launch32<true, PACKED, 4, 4, 1, true>(a, NS, stream);
-            case 7: return launch16<PACKED, 8, 4, 6, true>(a, NS, stream);
+            case 2: return launch32<false, PACKED, 8, 2, 3, true>(a, NS, stream, e0, e1);
+            case 4: return launch32<false, PACKED, 4, 4, 1, true>(a, NS, stream, e0, e1);
+            case 5: return launch32<true, PACKED, 4, 4, 1, true>(a, NS, stream, e0, e1);
+            case 7: return launch16<PACKED, 8, 4, 6, true>(a, NS, stream, e0, e1);
             default: return hipErrorInvalidValue;
         }
     }
     switch (t.id) {
-        case 1: return launch32<false, PACKED, 4, 4, 3>(a, NS, stream);
-        case 2: return launch32<false, PACKED, 8, 2, 3>(a, NS, stream);
-        case 3: return launch32<false, PACKED, 4, 4, 2>(a, NS, stream);
-        case 4: return launch32<false, PACKED, 4, 4, 1>(a, NS, stream);
-        case 5: return launch32<true, PACKED, 4, 4, 1>(a, NS, stream);
-        case 6: return launch16<PACKED, 8, 8, 3>(a, NS, stream);
-        case 7: return launch16<PACKED, 8, 4, 6>(a, NS, stream);
+        case 1: return launch32<false, PACKED, 4, 4, 3>(a, NS, stream, e0, e1);
+        case 2: return launch32<false, PACKED, 8, 2, 3>(a, NS, stream, e0, e1);
+        case 3: return launch32<false, PACKED, 4, 4, 2>(a, NS, stream, e0, e1);
+        case 4: return launch32<false, PACKED, 4, 4, 1>(a, NS, stream, e0, e1);
+        case 5: return launch32<true, PACKED, 4, 4, 1>(a, NS, stream, e0, e1);
+        case 6: return launch16<PACKED, 8, 8, 3>(a, NS, stream, e0, e1);
+        case 7: return launch16<PACKED, 8, 4, 6>(a, NS, stream, e0, e1);
         default: return hipErrorInvalidValue;
     }
 }
@@ -750,9 +762,11 @@ const RouterTiling kTilings[] = {
 int router_tiling_count() { return (int)(sizeof(kTilings) / sizeof(kTilings[0])); }
 RouterTiling router_tiling(int i) { return kTilings[i]; }
 
-hipError_t launch_router_score_select(const RouterTiling& t, const RouterArgs& a, hipStream_t stream) {
+hipError_t launch_router_score_select(const RouterTiling& t, const RouterArgs& a, hipStream_t stream,
+                                      hipEvent_t start, hipEvent_t stop) {
     const int NS = router_slices(t, a.E);
-    return a.w_packed ? launch_layout<true>(t, a, NS, stream) : launch_layout<false>(t, a, NS, stream);
+    return a.w_packed ? launch_layout<true>(t, a, NS, stream, start, stop)
+                      : launch_layout<false>(t, a, NS, stream, start, stop);
 }
 
 hipError_t launch_router_merge(const RouterTiling& t, const RouterArgs& a, const CtrlArgs* ctrl,

@@ -51,10 +51,17 @@ class RouterStep:
         B.idb_router_forward(x, Wt, self.state.bias, self.K, self.idx, self.w, self.counts, accumulate, scores_dump,
                              self.workspace, self.variant, stream, layout)
 
-    def score_select(self, x, W=None, accumulate: bool = False, scores_dump=None, stream=None):
+    def score_select(self, x, W=None, accumulate: bool = False, scores_dump=None, stream=None, events=None):
+        """The router's first launch; ``events`` = (start, stop) ``torch.cuda.Event`` pair that then takes the
+        fused kernel's own start and end timestamps."""
         Wt, layout = self._weights(W)
-        B.idb_router_score_select(x, Wt, self.state.bias, self.K, self.idx, self.w, self.counts, accumulate,
-                                  scores_dump, self.workspace, self.variant, stream, layout)
+        if events is None:
+            B.idb_router_score_select(x, Wt, self.state.bias, self.K, self.idx, self.w, self.counts, accumulate,
+                                      scores_dump, self.workspace, self.variant, stream, layout)
+        else:
+            B.idb_router_score_select_timed(x, Wt, self.state.bias, self.K, self.idx, self.w, self.counts,
+                                            events[0], events[1], accumulate, scores_dump, self.workspace,
+                                            self.variant, stream, layout)
 
     def merge(self, stream=None):
         B.idb_router_merge(self.T, self.d, self.E, self.K, self.dtype_code, self.idx, self.w, self.counts,

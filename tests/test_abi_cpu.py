@@ -30,11 +30,12 @@ def test_library_exports_every_header_function():
 
 def router(T=128, d=256, E=768, K=10, dtype=B.IDB_DTYPE_BF16, x=A16, W=A16, bias=A16, idx=A16, w=A16, counts=A16,
            dump=None, ws=A16, ws_bytes=1 << 30, variant=0, fn="idb_router_forward", layout=0):
+    extra = (None, None) if fn.endswith("_timed") else ()  # the timed call's two events
     return getattr(B.lib(), fn)(x, W, dtype, layout, bias, T, d, E, K, idx, w, counts, 0, dump, ws, ws_bytes, variant,
-                                None)
+                                None, *extra)
 
 
-@pytest.mark.parametrize("fn", ["idb_router_forward", "idb_router_score_select"])
+@pytest.mark.parametrize("fn", ["idb_router_forward", "idb_router_score_select", "idb_router_score_select_timed"])
 @pytest.mark.parametrize("kw,code", [
     (dict(T=0), B.IDB_ERR_INVALID_ARG),
     (dict(T=(1 << 26) + 1), B.IDB_ERR_INVALID_ARG),

@@ -199,3 +199,35 @@ def test_score_select_then_merge_step_equals_router_step(T, d, E, K, variant):
         s.score_select(x, Wt)
         s.merge_step()
         _assert_same_step(f, s, f"step {t}")
+
+
+@pytest.mark.parametrize("variant", [6, 7])
+def test_timed_score_select_equals_untimed(variant):
+    """idb_router_score_select_timed (the benchmark's live kernel timing) gives
+    the untimed call's results bit for bit, and its events bracket the fused
+    kernel: a positive interval, shorter than the whole call sequence around it."""
+    T, d, E, K = 4096, 1024, 768, 10
+    _, W = synth.normal_router_inputs(T, d, E, seed=23)
+    Wt = _bf16(W)
+    cfg = B.ControllerCfg(E, 6e-3, 6e-3)
+    f = RouterStep(T, d, E, K, torch.bfloat16, cfg=cfg, variant=variant)
+    s = RouterStep(T, d, E, K, torch.bfloat16, cfg=cfg, variant=variant)
+    ev = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+    outer = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+    for e in ev:
+        e.record()
+    for t in range(3):
+        x = _bf16(synth.normal_router_inputs(T, d, E, seed=500 + t)[0])
+        x[:, :16] += 1.5
+        f.score_select(x, Wt)
+        f.merge_step()
+        outer[0].record()
+        s.score_select(x, Wt, events=ev)
+        outer[1].record()
+        s.merge_step()
+        torch.cuda.synchronize()
+        print(f"[timed] variant {variant} step {t}: kernel {ev[0].elapsed_time(ev[1]) * 1000:.1f} us, "
+              f"call {outer[0].elapsed_time(outer[1]) * 1000:.1f} us", flush=True)
+        _assert_same_step(f, s, f"step {t}")
+        kernel_ms = ev[0].elapsed_time(ev[1])
+        assert 0.0 < kernel_ms <= outer[0].elapsed_time(outer[1])
