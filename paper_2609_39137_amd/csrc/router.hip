@@ -42,6 +42,7 @@
 #include "internal.h"
 
 #include <hip/hip_ext.h>
+#include <type_traits>
 
 #pragma clang fp contract(off)
 
@@ -438,7 +439,11 @@ __global__ __launch_bounds__(WAVES * 64) void router16_kernel(RouterArgs a, int 
         if constexpr (SM) return z;
         else return sigmoid_fast(z);
     };
-    auto store_pass = [&](int pass, float* sc) {
+    // The wave's expert tiles are all real unless the slice ends inside them;
+    // without a dump and with all tiles real the store loop needs no checks
+    // (both conditions are uniform over the workgroup).
+    const bool all_real = sbase + wave * C::WE + C::WE <= E;
+    auto store_tiles = [&](int pass, float* sc, auto checked) {
         constexpr int PT = EC::TPP / 16;  // token tiles per pass
 #pragma unroll
         for (int pt = 0; pt < PT; ++pt) {
@@ -447,17 +452,29 @@ __global__ __launch_bounds__(WAVES * 64) void router16_kernel(RouterArgs a, int 
             const int64_t tok = tok0 + tt * 16 + l16;
 #pragma unroll
             for (int et = 0; et < ET; ++et) {
-                const bool real = sbase + wave * C::WE + et * 16 < E;
-                float4 s4;
-                s4.x = real ? act(acc[tt][et][0]) : -INFINITY;
-                s4.y = real ? act(acc[tt][et][1]) : -INFINITY;
-                s4.z = real ? act(acc[tt][et][2]) : -INFINITY;
-                s4.w = real ? act(acc[tt][et][3]) : -INFINITY;
                 const int col = wave * C::WE + et * 16 + 4 * g4;
-                *reinterpret_cast<float4*>(sc + row * EC::RS + col) = s4;
-                if (a.dump && real && tok < T) *reinterpret_cast<float4*>(a.dump + tok * E + sbase + col) = s4;
+                float4 s4;
+                if constexpr (decltype(checked)::value) {
+                    const bool real = sbase + wave * C::WE + et * 16 < E;
+                    s4.x = real ? act(acc[tt][et][0]) : -INFINITY;
+                    s4.y = real ? act(acc[tt][et][1]) : -INFINITY;
+                    s4.z = real ? act(acc[tt][et][2]) : -INFINITY;
+                    s4.w = real ? act(acc[tt][et][3]) : -INFINITY;
+                    *reinterpret_cast<float4*>(sc + row * EC::RS + col) = s4;
+                    if (a.dump && real && tok < T) *reinterpret_cast<float4*>(a.dump + tok * E + sbase + col) = s4;
+                } else {
+                    s4.x = act(acc[tt][et][0]);
+                    s4.y = act(acc[tt][et][1]);
+                    s4.z = act(acc[tt][et][2]);
+                    s4.w = act(acc[tt][et][3]);
+                    *reinterpret_cast<float4*>(sc + row * EC::RS + col) = s4;
+                }
             }
         }
+    };
+    auto store_pass = [&](int pass, float* sc) {
+        if (!a.dump && all_real) store_tiles(pass, sc, std::false_type{});
+        else store_tiles(pass, sc, std::true_type{});
     };
     select_epilogue<EC, SM>(a, NS, slice, tok0, smem, breg, store_pass);
 }
