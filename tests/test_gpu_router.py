@@ -286,6 +286,52 @@ def test_workload_full_size_sampled_rows(name):
         np.testing.assert_array_equal(c, sc)
 
 
+@pytest.mark.parametrize("name", ["top10-of-768", "top5-of-768-mixture", "top3-of-768-drift", "large-d4096-top10"])
+def test_benchmarked_step_full_size(name):
+    """The call the benchmark times, in its launch configuration, at the
+    workload's full size: the packed router matrix and idb_router_step (the
+    fused kernel on the two-slice tiling, then the slice merge whose last
+    workgroup applies the ID update and writes MaxVio/MinVio), two steps in a
+    row (the second routes with the bias the first one produced).  Sampled rows
+    against the oracle's scores and selection (margin-aware, the fused kernel's
+    scores taken from a dumping call on the same inputs); counts equal the
+    bincount of the indices; the new bias, e_prev, step and MaxVio/MinVio are
+    bit-identical to the oracle's controller on the step's counts."""
+    wl = synth.WORKLOADS[name]
+    W = synth.router_weight(wl)
+    Wd = to_dev(W)
+    cfg = B.ControllerCfg(wl.E, 6e-3, 6e-3)
+    rs = RouterStep(wl.T, wl.d, wl.E, wl.K, torch.bfloat16, cfg=cfg)
+    assert rs.info["variant"] == 6 and rs.info["slices"] == 2
+    rs.pack(Wd)
+    probe = RouterStep(wl.T, wl.d, wl.E, wl.K, torch.bfloat16)  # same tiling, for the score dump
+    probe.pack(Wd)
+    dump = torch.empty((wl.T, wl.E), dtype=torch.float32, device=DEV)
+    ref = oracle.ControllerState(wl.E)
+    for t in range(2):
+        x = synth.hidden_states(wl, step=t)
+        xd = to_dev(x)
+        b = rs.state.bias.cpu().numpy().copy()
+        print(f"[bench-step] {name} step {t}", flush=True)
+        rs.step(xd, None)
+        probe.state.bias.copy_(torch.from_numpy(b).to(DEV))  # the bias this step routed with
+        probe.route(xd, None, scores_dump=dump)
+        torch.cuda.synchronize()
+        idx, w, c = rs.idx.cpu().numpy(), rs.w.cpu().numpy(), rs.counts.cpu().numpy()
+        check_invariants(idx, w, c, wl.T, wl.E, wl.K)
+        np.testing.assert_array_equal(probe.idx.cpu().numpy(), idx)  # same kernels, same bias
+        rows = synth.rng(78 + t, wl.wid).choice(wl.T, size=48, replace=False)
+        rows = np.sort(np.concatenate([rows, [0, wl.T - 1]]))
+        s_rows = dump[torch.from_numpy(rows).to(DEV)].cpu().numpy()
+        check_against_oracle(x[rows], W, b, wl.K, idx[rows], w[rows], c, s_rows, rows=None, max_uncertain=0.05)
+        assert oracle.controller(c, ref, 6e-3, 6e-3) == 0
+        np.testing.assert_array_equal(rs.state.bias.cpu().numpy().view(np.uint32), ref.bias.view(np.uint32))
+        np.testing.assert_array_equal(rs.state.e_prev.cpu().numpy().view(np.uint32), ref.e_prev.view(np.uint32))
+        assert int(rs.state.step.item()) == int(ref.step[0]) == t + 1
+        np.testing.assert_array_equal(rs.stats.cpu().numpy().view(np.uint64), oracle.load_stats(c).view(np.uint64))
+    assert np.abs(ref.bias).max() > 0
+
+
 def test_headline_full_batch_against_oracle():
     """All 16384 rows of the Top-10-of-768 batch (d = 2048) against the oracle:
     scores within rel 2e-3 everywhere, the oracle's selection on every token
