@@ -160,7 +160,7 @@ def main() -> int:
 
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported (the count all-reduce across "
-              f"data-parallel ranks is design-only in this build)", file=sys.stderr)
+              f"data-parallel ranks is not implemented: one GPU runs the whole path)", file=sys.stderr)
         return 2
 
     pool = None
