@@ -599,6 +599,9 @@ def loop_report(args, wl, pool) -> int:
                 raise RuntimeError(f"{name} step {t}: MaxVio/MinVio differ between the two kernels")
             r["rec"].add(st)
             r["diag_rows"].append(r["diag"].cpu().numpy().reshape(-1).copy())
+            if wl.E <= 64:  # small pools: the per-expert trajectory too
+                r.setdefault("counts", []).append(rs.counts.cpu().numpy().tolist())
+                r.setdefault("bias", []).append([float(v) for v in rs.state.bias.cpu().numpy()])
         if t % 10 == 0 or t == steps - 1:
             mv = {n: round(float(r["rec"].maxvio[-1, 0]), 4) for n, r in runs.items()}
             log(f"step {t}: MaxVio {mv} ({time.time() - t_start:.1f} s)")
@@ -624,6 +627,9 @@ def loop_report(args, wl, pool) -> int:
             "gate_fraction": [round(float(v), 6) for v in diag[:, 0]],
             "busiest10_share": [round(float(v), 6) for v in diag[:, 1]],
         })
+        if "counts" in r:
+            summ["counts"] = r["counts"]
+            summ["bias_after_step"] = r["bias"]
         out["controllers"][name] = summ
     if args.loop_md:
         with open(args.loop_md, "w") as f:
@@ -640,7 +646,8 @@ def loop_markdown(out: dict, argv) -> str:
     lines = [f"# Closed loop, {out['workload']} (T={out['T']}, d={out['d']}, E={out['E']}, K={out['K']}), "
              f"{out['steps']} steps", "", "Command:", "", "```", "python " + " ".join(argv), "```", "",
              "Each step: a fresh synthetic batch routed by idb_router_step with the controller's current bias "
-             "(fused router kernel, slice merge, update and MaxVio/MinVio in the merge's last workgroup). "
+             "(the fused router kernel, then the slice merge with the update and MaxVio/MinVio in its last "
+             "workgroup, or the controller step when one slice covers all experts). "
              "Diagnostics from idb_controller_update_layers on a copy of the pre-step state (its bias equals the "
              "step's bit for bit, checked every step).", "",
              f"| controller | K_i | K_d | mode | centre | MaxVio last {last} | MaxVio avg | MaxVio worst | "
@@ -664,6 +671,13 @@ def loop_markdown(out: dict, argv) -> str:
             cells += [f"{c[n]['maxvio'][t]:.4f}", f"{c[n]['minvio'][t]:.4f}"]
         lines.append(f"| {t} | " + " | ".join(cells) + f" | {c['id']['gate_fraction'][t]:.4f} | "
                      f"{c['id']['busiest10_share'][t]:.4f} |")
+    if "counts" in c["id"]:
+        E = out["E"]
+        lines += ["", "ID Balancing, per step: the counts n_i (experts 0..E-1), then the bias b_i after the step's "
+                  "update (fp32, 9 significant digits):", ""]
+        for t in range(out["steps"]):
+            lines.append(f"- step {t} counts: " + " ".join(str(v) for v in c["id"]["counts"][t]))
+            lines.append(f"- step {t} bias: " + " ".join(f"{v:.9g}" for v in c["id"]["bias_after_step"][t]))
     return "\n".join(lines) + "\n"
 
 
