@@ -124,6 +124,7 @@ hipError_t launch_select_be(const RouterArgs& a, const float* scores, hipStream_
 // Register-resident selection.
 constexpr int kRegMaxK = 10;   // largest K of this kernel
 constexpr int kRegCap = 64;    // candidate list entries per token
+constexpr int kRegStage = 4;   // marked chunks per lane staged in LDS
 
 // DPP rotation by R lanes inside each 16-lane row.
 template <int R>
@@ -223,6 +224,9 @@ __global__ __launch_bounds__(64 * WAVES) void select_reg_kernel(RouterArgs a, co
     __shared__ float lsc[TPB][kRegCap];
     __shared__ int sel_i[TPB][kRegMaxK];
     __shared__ float sel_s[TPB][kRegMaxK];
+    // each lane's first kRegStage marked chunks, copied from its registers
+    // (slot-major, so a wave's copies are consecutive 16-byte units)
+    __shared__ float4 staged[kRegStage][64 * WAVES];
 
     const int tid = threadIdx.x;
     const int E = a.E, K = a.K;
@@ -274,15 +278,31 @@ __global__ __launch_bounds__(64 * WAVES) void select_reg_kernel(RouterArgs a, co
         cmask &= valid ? vmask : 0u;
 
         if (j == 0) cnt[slot] = 0;
+        // the first kRegStage marked chunks go from registers to LDS, in
+        // ascending chunk order (the order the loop below takes them)
+        {
+            int k = 0;
+#pragma unroll
+            for (int c = 0; c < NV; ++c) {
+                if ((cmask >> c) & 1u) {
+                    if (k < kRegStage) staged[k][tid] = sv[c];
+                    ++k;
+                }
+            }
+        }
         wave_sync();
         // candidates: the values >= tau of the marked chunks, appended to the
-        // token's list (list order is irrelevant: ranks are counted below)
+        // token's list (list order is irrelevant: ranks are counted below);
+        // a lane's chunks past the staged ones are read again from memory
+        int taken = 0;
         while (__ballot(cmask != 0u) != 0) {
             if (cmask != 0u) {
                 const int c = __ffs(cmask) - 1;
                 cmask &= cmask - 1u;
                 const int col0 = 4 * (16 * c + j);
-                const float4 s4 = *reinterpret_cast<const float4*>(row + col0);
+                const float4 s4 = taken < kRegStage ? staged[taken][tid]
+                                                    : *reinterpret_cast<const float4*>(row + col0);
+                ++taken;
                 const float4 b4 = *reinterpret_cast<const float4*>(bias_s + col0);
                 const float4 v4 = make_float4(s4.x + b4.x, s4.y + b4.y, s4.z + b4.z, s4.w + b4.w);
                 const int n4 = (v4.x >= tau) + (v4.y >= tau) + (v4.z >= tau) + (v4.w >= tau);
