@@ -187,6 +187,14 @@ def counters(args) -> None:
                   f"{mean['SQ_WAIT_INST_ANY'] / mean['SQ_WAVE_CYCLES']:.3f}")
     if "SQ_WAIT_INST_LDS" in mean and "SQ_WAVE_CYCLES" in mean:
         md.append(f"Share of wave cycles waiting on LDS: {mean['SQ_WAIT_INST_LDS'] / mean['SQ_WAVE_CYCLES']:.3f}")
+    if "TCC_HIT_sum" in mean and "TCC_MISS_sum" in mean and mean["TCC_HIT_sum"] + mean["TCC_MISS_sum"] > 0:
+        md.append(f"L2 hit rate: {mean['TCC_HIT_sum'] / (mean['TCC_HIT_sum'] + mean['TCC_MISS_sum']):.3f}")
+    if args.units:
+        # instruction counters count wave instructions; a wave has 64 lanes
+        for c in sorted(mean):
+            if c.startswith("SQ_INSTS_"):
+                md.append(f"{c} per {args.unit_name}: {mean[c] / args.units:.4g} wave instructions, "
+                          f"{64 * mean[c] / args.units:.4g} lane operations")
     md.append("")
     with open(args.out, "w") as fh:
         fh.write("\n".join(md))
@@ -216,6 +224,8 @@ def main(argv=None) -> int:
     c.add_argument("--title", default="Hardware counters")
     c.add_argument("--simds", type=int, default=1024)
     c.add_argument("--family", default="router", choices=sorted(FAMILIES))
+    c.add_argument("--units", type=float, default=0.0, help="work units per dispatch (e.g. T*E scores)")
+    c.add_argument("--unit-name", default="unit")
     c.add_argument("--out", required=True)
     args = ap.parse_args(argv)
     if args.action == "stats":
