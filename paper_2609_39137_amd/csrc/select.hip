@@ -10,7 +10,7 @@
 //    the token's K-th largest biased score; only the float4 chunks whose
 //    maximum reaches tau are read again, and their values >= tau go to a short
 //    LDS list whose entries are ranked by counting.  A token whose list would
-//    overflow takes K exact argmax rounds over its registers instead.
+//    overflow takes K exact argmax rounds over its row instead.
 //  * select_kernel (every other case): a workgroup of 512 threads walks tiles
 //    of 32 tokens (grid-stride, one workgroup per CU: the score rows of a tile
 //    take most of the LDS).  A tile's scores go from registers into the LDS
@@ -169,36 +169,32 @@ __device__ __forceinline__ float f4_at(const float4& v, int q) {
 }
 
 // Heavy ties (a candidate list that would overflow): K rounds over the row's
-// biased scores in registers, by the token's 16 lanes (one DPP row, all
-// active).  Round r takes the largest rank key strictly below the previous
-// round's pick.  Rank keys order (v descending, index ascending) with -0 ==
-// +0, and every real column's key is above the key 0 a round starts from --
-// -inf included, so a row with fewer than K finite biased scores still picks
-// its -inf columns by lowest index.  Not inlined: the main path's register
-// count (and occupancy) does not carry this rare path's.
+// biased scores by the token's 16 lanes (one DPP row, all active).  Round r
+// takes the largest rank key strictly below the previous round's pick.  Rank
+// keys order (v descending, index ascending) with -0 == +0, and every real
+// column's key is above the key 0 a round starts from -- -inf included, so a
+// row with fewer than K finite biased scores still picks its -inf columns by
+// lowest index.  Each round reads the row again, one float4 at a time (from
+// L2), so that this rare path adds few registers to the main path's.
 template <int NV>
-__device__ __attribute__((noinline)) void overflow_select(const float* row, const float* bias_s, unsigned vmask, int j,
-                                                          int K, int* sel_i, float* sel_s) {
-    float4 vv[NV];
-#pragma unroll
-    for (int c = 0; c < NV; ++c) {
-        vv[c] = make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY);
-        if ((vmask >> c) & 1u) {
-            const float4 s4 = *reinterpret_cast<const float4*>(row + 4 * (16 * c + j));
-            const float4 b4 = *reinterpret_cast<const float4*>(bias_s + 4 * (16 * c + j));
-            vv[c] = make_float4(s4.x + b4.x, s4.y + b4.y, s4.z + b4.z, s4.w + b4.w);
-        }
-    }
+__device__ __forceinline__ void overflow_select(const float* row, const float* bias_s, unsigned vmask, int j, int K,
+                                                int* sel_i, float* sel_s) {
     unsigned long long prev = ~0ull;
     int mine = 0;
     for (int r = 0; r < K; ++r) {
         unsigned long long best = 0ull;
-#pragma unroll
+#pragma unroll 1
         for (int c = 0; c < NV; ++c) {
+            if ((vmask >> c) & 1u) {
+                const int col0 = 4 * (16 * c + j);
+                const float4 s4 = *reinterpret_cast<const float4*>(row + col0);
+                const float4 b4 = *reinterpret_cast<const float4*>(bias_s + col0);
+                const float4 v4 = make_float4(s4.x + b4.x, s4.y + b4.y, s4.z + b4.z, s4.w + b4.w);
 #pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                const unsigned long long kk = rank_key(f4_at(vv[c], q), 4 * (16 * c + j) + q);
-                if (((vmask >> c) & 1u) && kk < prev && kk > best) best = kk;
+                for (int q = 0; q < 4; ++q) {
+                    const unsigned long long kk = rank_key(f4_at(v4, q), col0 + q);
+                    if (kk < prev && kk > best) best = kk;
+                }
             }
         }
         best = row_max_key(best);
@@ -251,10 +247,17 @@ __global__ __launch_bounds__(64 * WAVES) void select_reg_kernel(RouterArgs a, co
         const float* row = scores + (valid ? t : 0) * (int64_t)E;
 
         float4 sv[NV];
+        // a tile of real tokens whose rows fill all 64 NV columns loads
+        // without per-chunk conditions (uniform over the workgroup)
+        if (64 * NV == E && (tile + 1) * TPB <= T) {
 #pragma unroll
-        for (int c = 0; c < NV; ++c) {
-            sv[c] = make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY);
-            if (valid && ((vmask >> c) & 1u)) sv[c] = *reinterpret_cast<const float4*>(row + 4 * (16 * c + j));
+            for (int c = 0; c < NV; ++c) sv[c] = *reinterpret_cast<const float4*>(row + 4 * (16 * c + j));
+        } else {
+#pragma unroll
+            for (int c = 0; c < NV; ++c) {
+                sv[c] = make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY);
+                if (valid && ((vmask >> c) & 1u)) sv[c] = *reinterpret_cast<const float4*>(row + 4 * (16 * c + j));
+            }
         }
         // chunk and lane maxima of v = s + b
         float cm[NV];
