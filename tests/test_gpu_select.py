@@ -35,7 +35,7 @@ def check(s, b, K):
     np.testing.assert_array_equal(c, rc)
 
 
-@pytest.mark.parametrize("E", [32, 64, 100, 256, 768, 1024])
+@pytest.mark.parametrize("E", [32, 64, 100, 256, 512, 768, 1024])
 @pytest.mark.parametrize("kind", ["beta", "grid", "edges", "saturated"])
 def test_select_matches_oracle(E, kind):
     for T, K, bkind in ((1, 1, "zero"), (17, 3, "small"), (333, 10, "grid"), (1000, min(16, E), "large"),
@@ -53,12 +53,13 @@ def test_all_equal_scores_take_lowest_indices():
         assert np.all(idx == np.arange(K)[None, :])
 
 
-def test_overflowing_and_listed_tokens_share_waves():
+@pytest.mark.parametrize("E", [256, 512, 768, 1024])
+def test_overflowing_and_listed_tokens_share_waves(E):
     # constant rows (every score tied: the list overflows) between rows of
     # distinct scores, so both paths run inside one wave
-    s = synth.scores(200, 768, "beta", seed=12)
+    s = synth.scores(200, E, "beta", seed=12)
     s[::4] = np.float32(0.25)
-    b = np.zeros(768, np.float32)
+    b = np.zeros(E, np.float32)
     for K in (1, 10, 32):
         check(s, b, K)
 
@@ -93,12 +94,14 @@ def test_gate_weights_sum_to_one_and_ignore_bias():
     np.testing.assert_array_equal(w1, w2)
 
 
-def test_more_tiles_than_workgroups():
-    # 70001 tokens in 16-token tiles: more tiles than the launch has
-    # workgroups, so each walks several (grid-stride), ragged last tile
-    s = synth.scores(70001, 64, "beta", seed=21)
-    b = synth.bias(64, "small", seed=22)
-    check(s, b, 4)
+@pytest.mark.parametrize("T,E,K", [(70001, 64, 4), (40001, 768, 10), (33000, 1024, 8)])
+def test_more_tiles_than_workgroups(T, E, K):
+    # more 64-token tiles than the launch has workgroups, so each walks
+    # several (grid-stride), ragged last tile; with E a multiple of 256 the
+    # full tiles take the load path without per-chunk conditions
+    s = synth.scores(T, E, "beta", seed=21 + E)
+    b = synth.bias(E, "small", seed=22 + E)
+    check(s, b, K)
 
 
 @pytest.mark.parametrize("E", [30, 770])
