@@ -785,12 +785,12 @@ def qb_report(args, wl, rs, xs, nbuf, stream, capture, ms_step, stats, spread) -
     per = nbuf * max(1, 16 // nbuf)
     reps = max(1, -(-max(args.steps, 64) // per))
     route_ms = time_per_call(lambda i: rs.qb_route(xs[i % nbuf], None, stream=stream), per, reps)
-    upd_ms = time_per_call(lambda i: B.idb_qb_update(rs.scores_t, rs.alpha, wl.K, args.rho, rs.state.bias, stream),
-                           per, reps)
+    upd_ms = time_per_call(lambda i: B.idb_qb_update(rs.scores_t, rs.alpha, wl.K, args.rho, rs.state.bias, stream,
+                                                     counts=rs.counts, stats=rs.stats), per, reps)
     log(f"router in QB mode (fused kernel + slice merge): {route_ms * 1000:.2f} us; update {upd_ms * 1000:.2f} us")
     achieved = wl.flops / (route_ms * 1e-3) / 1e12
     peak = PEAK_BF16_TFLOPS if wl.dtype == "bf16" else PEAK_F32_TFLOPS
-    upd_bytes = wl.E * wl.T * 4 + wl.T * 4 + 2 * wl.E * 4
+    upd_bytes = wl.E * wl.T * 4 + wl.T * 4 + 3 * wl.E * 4 + 16
     upd_gbs = upd_bytes / (upd_ms * 1e-3) / 1e9
     out = {
         "metric": "routed tokens/sec for router + Quantile Balancing step (the paper's baseline controller)",
@@ -814,7 +814,8 @@ def qb_report(args, wl, rs, xs, nbuf, stream, capture, ms_step, stats, spread) -
                                "scores written) + slice merge",
                      "kernel_us": round(route_ms * 1000, 2), "flops_per_launch": wl.flops},
         "qb_update_roofline": {"bound": "hbm", "achieved": round(upd_gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                               "frac": round(upd_gbs / PEAK_HBM_GBS, 4), "kernel": "qb_update_kernel",
+                               "frac": round(upd_gbs / PEAK_HBM_GBS, 4),
+                               "kernel": "qb_update_reg_kernel (MaxVio/MinVio in its first workgroup)",
                                "kernel_us": round(upd_ms * 1000, 2), "bytes_per_launch": upd_bytes},
         "last_step": {"maxvio": stats[0], "minvio": stats[1]},
         "step_spread": spread,

@@ -364,6 +364,13 @@ idb_status idb_routing_entropy_softmax(const float* gate_w, int64_t T, int32_t K
  * alpha [T] as written by idb_qb_router_forward; bias [E] is updated in
  * place.  1 <= T <= 2^26, 1 <= K < E <= 1024, 0 <= rho < 1.  One workgroup
  * per expert (exact radix select of the k-th margin).
+ *   counts            nullable [E] int32 in: the step's assignments per
+ *                     expert (as written by idb_qb_router_forward);
+ *   out_maxvio_minvio nullable fp64 [2] out: MaxVio, MinVio of those counts
+ *                     (Eq. vio; the same bits as idb_load_stats), written by
+ *                     the first workgroup in the same launch.
+ * counts and out_maxvio_minvio are both given or both null (else
+ * IDB_ERR_INVALID_ARG, nothing launched); out_maxvio_minvio 8-byte aligned.
  * ------------------------------------------------------------------------- */
 size_t idb_qb_router_workspace_bytes(int64_t T, int32_t d, int32_t E, int32_t K, idb_dtype dtype,
                                      int32_t variant);
@@ -373,7 +380,7 @@ idb_status idb_qb_router_forward(const void* x, const void* W_g, idb_dtype dtype
                                  float* alpha, void* workspace, size_t workspace_bytes, int32_t variant,
                                  hipStream_t stream);
 idb_status idb_qb_update(const float* scores_t, const float* alpha, int64_t T, int32_t E, int32_t K, float rho,
-                         float* bias, hipStream_t stream);
+                         float* bias, const int32_t* counts, double* out_maxvio_minvio, hipStream_t stream);
 
 /* ---------------------------------------------------------------------------
  * Auxiliary-loss balancing's forward statistics (Eq. pid-auxloss), on the

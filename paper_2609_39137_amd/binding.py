@@ -106,7 +106,7 @@ def lib() -> ctypes.CDLL:
     L.idb_qb_router_workspace_bytes.restype = sz
     L.idb_qb_router_forward.argtypes = [P, P, i32, i32, P, i64, i32, i32, i32, P, P, P, i32, P, P, P, sz, i32, P]
     L.idb_qb_router_forward.restype = ctypes.c_int
-    L.idb_qb_update.argtypes = [P, P, i64, i32, i32, ctypes.c_float, P, P]
+    L.idb_qb_update.argtypes = [P, P, i64, i32, i32, ctypes.c_float, P, P, P, P]
     L.idb_qb_update.restype = ctypes.c_int
     L.idb_controller_update_layers.argtypes = [P, i32, ctypes.POINTER(idb_controller_cfg),
                                                ctypes.POINTER(idb_controller_state), P, P, P]
@@ -416,12 +416,20 @@ def idb_qb_router_forward(x, W_g, bias, K, expert_idx, gate_w, counts, scores_t,
     _check("idb_qb_router_forward", st)
 
 
-def idb_qb_update(scores_t, alpha, K, rho, bias, stream=None):
-    """Quantile Balancing's bias update (exact per-expert quantile; EMA for ``rho`` > 0), ``bias`` in place."""
+def idb_qb_update(scores_t, alpha, K, rho, bias, stream=None, counts=None, stats=None):
+    """Quantile Balancing's bias update (exact per-expert quantile; EMA for ``rho`` > 0), ``bias`` in place;
+    with ``counts`` and ``stats`` (fp64 [2]) also MaxVio/MinVio of the counts, in the same launch."""
     E, T = scores_t.shape
     if scores_t.dtype != torch.float32 or alpha.shape != (T,) or bias.shape != (E,) or bias.dtype != torch.float32:
         raise ValueError("Quantile Balancing operands have the wrong shape or dtype")
-    st = lib().idb_qb_update(_ptr(scores_t), _ptr(alpha), T, E, K, float(rho), _ptr(bias), _stream(stream))
+    if (counts is None) != (stats is None):
+        raise ValueError("counts and stats go together")
+    if counts is not None and (counts.shape != (E,) or counts.dtype != torch.int32 or stats.shape != (2,)
+                               or stats.dtype != torch.float64):
+        raise ValueError("counts must be int32 [E] and stats fp64 [2]")
+    st = lib().idb_qb_update(_ptr(scores_t), _ptr(alpha), T, E, K, float(rho), _ptr(bias),
+                             _ptr(counts) if counts is not None else None,
+                             _ptr(stats) if stats is not None else None, _stream(stream))
     _check("idb_qb_update", st)
 
 

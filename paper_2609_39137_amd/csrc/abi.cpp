@@ -492,15 +492,19 @@ idb_status idb_qb_router_forward(const void* x, const void* W_g, idb_dtype dtype
 }
 
 idb_status idb_qb_update(const float* scores_t, const float* alpha, int64_t T, int32_t E, int32_t K, float rho,
-                         float* bias, hipStream_t stream) {
+                         float* bias, const int32_t* counts, double* out_maxvio_minvio, hipStream_t stream) {
     if (!scores_t || !alpha || !bias) return fail(IDB_ERR_INVALID_ARG, "null pointer");
+    if (!counts != !out_maxvio_minvio)
+        return fail(IDB_ERR_INVALID_ARG, "counts and out_maxvio_minvio go together (both or neither)");
     if (T < 1 || T > kMaxTokens) return fail(IDB_ERR_INVALID_ARG, "T=%lld out of [1, 2^26]", (long long)T);
     if (E < 2 || E > kMaxExperts) return fail(IDB_ERR_INVALID_ARG, "E=%d out of [2, %d]", E, kMaxExperts);
     if (K < 1 || K >= E) return fail(IDB_ERR_INVALID_ARG, "need 1 <= K < E (K=%d, E=%d)", K, E);
     if (!(rho >= 0.0f && rho < 1.0f)) return fail(IDB_ERR_INVALID_ARG, "rho must lie in [0, 1)");
-    if (!aligned(scores_t, 4) || !aligned(alpha, 4) || !aligned(bias, 4))
+    if (!aligned(scores_t, 4) || !aligned(alpha, 4) || !aligned(bias, 4) || !aligned(counts, 4) ||
+        !aligned(out_maxvio_minvio, 8))
         return fail(IDB_ERR_INVALID_ARG, "misaligned buffer");
-    return hip_result(idb::launch_qb_update(scores_t, alpha, T, E, K, rho, bias, stream), "Quantile Balancing launch");
+    return hip_result(idb::launch_qb_update(scores_t, alpha, T, E, K, rho, bias, counts, out_maxvio_minvio, stream),
+                      "Quantile Balancing launch");
 }
 
 size_t idb_aux_router_workspace_bytes(int64_t T, int32_t d, int32_t E, int32_t K, idb_dtype dtype,

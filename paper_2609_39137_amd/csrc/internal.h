@@ -45,9 +45,10 @@ size_t noalloc_scratch_bytes();
 hipError_t noalloc_scratch(int device, void** out);
 
 hipError_t launch_fill_i32(int32_t* p, int32_t value, int64_t n, hipStream_t stream);
-// Quantile Balancing's bias update from expert-major scores and cutoffs.
+// Quantile Balancing's bias update from expert-major scores and cutoffs;
+// with counts (nullable), workgroup 0 also writes MaxVio/MinVio to stats.
 hipError_t launch_qb_update(const float* scores_t, const float* alpha, int64_t T, int E, int K, float rho,
-                            float* bias, hipStream_t stream);
+                            float* bias, const int32_t* counts, double* stats, hipStream_t stream);
 // Selection from given scores; counts must already hold the starting values.
 hipError_t launch_select_from_scores(const float* scores, const float* bias, int64_t T, int E, int K,
                                      int32_t* idx, float* w, int32_t* counts, hipStream_t stream);

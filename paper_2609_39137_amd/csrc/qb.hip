@@ -16,6 +16,12 @@
 // threads) and the selection first narrows the keys to the few near the top
 // (see qb_update_reg_kernel).  Beyond 32768 tokens each pass recomputes the
 // keys from global memory.
+//
+// With a counts pointer, workgroup 0 also writes MaxVio/MinVio of the step's
+// counts (Eq. vio), as the stand-alone statistics kernel does: exact integer
+// sum, maximum and minimum, one fp64 division each (NaN for an empty batch),
+// after its own expert's selection (loading the counts at launch instead keeps
+// them in registers through the selection: more spills, slower).
 #include "common.h"
 #include "internal.h"
 
@@ -226,6 +232,62 @@ __device__ unsigned wave_select_reg(const unsigned* vals, unsigned n, unsigned k
     return prefix;
 }
 
+// MaxVio, MinVio of counts whose entries i = tid + NT q (q < NQ) thread tid
+// holds in n[] (0 past E), over a workgroup of NT threads.
+template <int NT, int NQ>
+__device__ void qb_block_stats(const int (&n)[NQ], int E, double* __restrict__ out) {
+    constexpr int NW = NT / 64;
+    __shared__ long long w_sum[NW];
+    __shared__ int w_max[NW], w_min[NW];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    long long S = 0;
+    int mx = INT32_MIN, mn = INT32_MAX;
+#pragma unroll
+    for (int q = 0; q < NQ; ++q)
+        if (tid + NT * q < E) {
+            S += n[q];
+            mx = max(mx, n[q]);
+            mn = min(mn, n[q]);
+        }
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) {
+        S += __shfl_xor(S, o);
+        mx = max(mx, __shfl_xor(mx, o));
+        mn = min(mn, __shfl_xor(mn, o));
+    }
+    __syncthreads();
+    if (lane == 0) {
+        w_sum[wave] = S;
+        w_max[wave] = mx;
+        w_min[wave] = mn;
+    }
+    __syncthreads();
+    if (tid == 0) {
+        for (int w = 1; w < NW; ++w) {
+            S += w_sum[w];
+            mx = max(mx, w_max[w]);
+            mn = min(mn, w_min[w]);
+        }
+        if (S == 0) {
+            out[0] = __builtin_nan("");
+            out[1] = __builtin_nan("");
+        } else {
+            out[0] = (double)((long long)E * mx - S) / (double)S;
+            out[1] = (double)(S - (long long)E * mn) / (double)S;
+        }
+    }
+}
+
+// The counts that thread tid of workgroup 0 holds for qb_block_stats.
+template <int NT, int NQ>
+__device__ __forceinline__ void qb_stats_load(const int32_t* __restrict__ counts, int E, int (&n)[NQ]) {
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+        const int i = threadIdx.x + NT * q;
+        n[q] = i < E ? counts[i] : 0;
+    }
+}
+
 // NT threads, R keys per thread in registers (T <= R * NT).  The wanted key
 // is the r-th largest, r = T - k + 1, normally far fewer than T.  When r <=
 // NT: tau = the r-th largest of the threads' maxima with its 16 low bits
@@ -239,8 +301,11 @@ template <int NT, int R, bool VEC>
 __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(NT == 512 ? 6 : 1)))
 void qb_update_reg_kernel(const float* __restrict__ scores_t,
                                                            const float* __restrict__ alpha, int64_t T, int E, int K,
-                                                           float rho, float* __restrict__ bias) {
+                                                           float rho, float* __restrict__ bias,
+                                                           const int32_t* __restrict__ counts,
+                                                           double* __restrict__ stats) {
     constexpr int NW = NT / 64;
+    constexpr int NQ = (1024 + NT - 1) / NT;  // counts per thread of workgroup 0 (E <= 1024)
     __shared__ unsigned hist[NW][256];
     __shared__ unsigned list[kQbList];
     __shared__ unsigned maxima[NT];
@@ -250,6 +315,7 @@ void qb_update_reg_kernel(const float* __restrict__ scores_t,
     const int lane = tid & 63, wave = tid >> 6;
     const int j = blockIdx.x;
     const float* row = scores_t + (int64_t)j * T;
+    const bool with_stats = counts && j == 0;  // uniform over the workgroup
 
     // Key slot r holds token tok(r): with VEC (T % 4 == 0) the tokens
     // 4 (tid + NT i) + c for r = 4 i + c, read as float4 pieces, every load of
@@ -354,40 +420,52 @@ void qb_update_reg_kernel(const float* __restrict__ scores_t,
             done = true;
         }
     }
-    if (done) return;
-    // full radix select over the registers
-    unsigned kleft = k, prefix = 0u, mask = 0u;
-    for (int shift = 24; shift >= 0; shift -= 8) {
-        __syncthreads();
-        for (int i = tid; i < NW * 256; i += NT) (&hist[0][0])[i] = 0u;
-        __syncthreads();
-        DigitCounter dc;
+    if (!done) {
+        // full radix select over the registers
+        unsigned kleft = k, prefix = 0u, mask = 0u;
+        for (int shift = 24; shift >= 0; shift -= 8) {
+            __syncthreads();
+            for (int i = tid; i < NW * 256; i += NT) (&hist[0][0])[i] = 0u;
+            __syncthreads();
+            DigitCounter dc;
 #pragma unroll
-        for (int r = 0; r < R; ++r)
-            if (live(r) && (key[r] & mask) == prefix) dc.add(hist[wave], (key[r] >> shift) & 255u);
-        dc.flush(hist[wave]);
-        __syncthreads();
-        if (wave == 0) pick_digit(hist, kleft, pick);
-        __syncthreads();
-        prefix |= pick[0] << shift;
-        mask |= 255u << shift;
-        kleft -= pick[1];
+            for (int r = 0; r < R; ++r)
+                if (live(r) && (key[r] & mask) == prefix) dc.add(hist[wave], (key[r] >> shift) & 255u);
+            dc.flush(hist[wave]);
+            __syncthreads();
+            if (wave == 0) pick_digit(hist, kleft, pick);
+            __syncthreads();
+            prefix |= pick[0] << shift;
+            mask |= 255u << shift;
+            kleft -= pick[1];
+        }
+        result = prefix;
+        if (tid == 0) write_bias(bias, j, result, rho);
     }
-    result = prefix;
-    if (tid == 0) write_bias(bias, j, result, rho);
+    if (with_stats) {
+        int cnt[NQ];
+        qb_stats_load<NT>(counts, E, cnt);
+        qb_block_stats<NT>(cnt, E, stats);
+    }
 }
 
 // Any T: the keys are recomputed from global memory in every pass.
 __global__ __launch_bounds__(kQbThreads) void qb_update_global_kernel(const float* __restrict__ scores_t,
                                                                       const float* __restrict__ alpha, int64_t T,
                                                                       int E, int K, float rho,
-                                                                      float* __restrict__ bias) {
+                                                                      float* __restrict__ bias,
+                                                                      const int32_t* __restrict__ counts,
+                                                                      double* __restrict__ stats) {
     constexpr int NW = kQbThreads / 64;
+    constexpr int NQ = (1024 + kQbThreads - 1) / kQbThreads;
     __shared__ unsigned hist[NW][256];
     __shared__ unsigned pick[3];
     const int tid = threadIdx.x;
     const int wave = tid >> 6;
     const int j = blockIdx.x;
+    const bool with_stats = counts && j == 0;
+    int cnt[NQ];
+    if (with_stats) qb_stats_load<kQbThreads>(counts, E, cnt);
     const float* row = scores_t + (int64_t)j * T;
     unsigned kleft = (unsigned)((T * (int64_t)(E - K) + E - 1) / E);
     unsigned prefix = 0u, mask = 0u;
@@ -409,35 +487,36 @@ __global__ __launch_bounds__(kQbThreads) void qb_update_global_kernel(const floa
         __syncthreads();  // pick[] is rewritten by the next pass
     }
     if (tid == 0) write_bias(bias, j, prefix, rho);
+    if (with_stats) qb_block_stats<kQbThreads>(cnt, E, stats);
 }
 
 template <int NT, int R>
 void launch_reg(const float* scores_t, const float* alpha, int64_t T, int E, int K, float rho, float* bias,
-                hipStream_t stream) {
+                const int32_t* counts, double* stats, hipStream_t stream) {
     // float4 pieces need T % 4 == 0 (16-byte aligned rows) and aligned buffers
     const bool vec = (T % 4 == 0) && ((reinterpret_cast<uintptr_t>(scores_t) | reinterpret_cast<uintptr_t>(alpha)) &
                                       15) == 0;
     if (vec)
         hipLaunchKernelGGL((qb_update_reg_kernel<NT, R, true>), dim3((unsigned)E), dim3(NT), 0, stream, scores_t,
-                           alpha, T, E, K, rho, bias);
+                           alpha, T, E, K, rho, bias, counts, stats);
     else
         hipLaunchKernelGGL((qb_update_reg_kernel<NT, R, false>), dim3((unsigned)E), dim3(NT), 0, stream, scores_t,
-                           alpha, T, E, K, rho, bias);
+                           alpha, T, E, K, rho, bias, counts, stats);
 }
 
 }  // namespace
 
 hipError_t launch_qb_update(const float* scores_t, const float* alpha, int64_t T, int E, int K, float rho,
-                            float* bias, hipStream_t stream) {
+                            float* bias, const int32_t* counts, double* stats, hipStream_t stream) {
     if (T <= 16 * 512)
-        launch_reg<512, 16>(scores_t, alpha, T, E, K, rho, bias, stream);
+        launch_reg<512, 16>(scores_t, alpha, T, E, K, rho, bias, counts, stats, stream);
     else if (T <= 32 * 512)
-        launch_reg<512, 32>(scores_t, alpha, T, E, K, rho, bias, stream);
+        launch_reg<512, 32>(scores_t, alpha, T, E, K, rho, bias, counts, stats, stream);
     else if (T <= 32 * 1024)
-        launch_reg<1024, 32>(scores_t, alpha, T, E, K, rho, bias, stream);
+        launch_reg<1024, 32>(scores_t, alpha, T, E, K, rho, bias, counts, stats, stream);
     else
         hipLaunchKernelGGL(qb_update_global_kernel, dim3((unsigned)E), dim3(kQbThreads), 0, stream, scores_t, alpha,
-                           T, E, K, rho, bias);
+                           T, E, K, rho, bias, counts, stats);
     return hipGetLastError();
 }
 

@@ -109,10 +109,11 @@ class RouterStep:
                                 self.alpha, accumulate, self.qb_workspace, self.variant, stream, layout)
 
     def qb_step(self, x, W=None, rho: float = 0.0, stream=None):
-        """One Quantile Balancing iteration (Eq. pid-quantile): route, MaxVio/MinVio, then the bias target."""
+        """One Quantile Balancing iteration (Eq. pid-quantile): route, then the bias target and MaxVio/MinVio of
+        the counts (one launch)."""
         self.qb_route(x, W, stream=stream)
-        B.idb_load_stats(self.counts, self.stats, stream)
-        B.idb_qb_update(self.scores_t, self.alpha, self.K, rho, self.state.bias, stream)
+        B.idb_qb_update(self.scores_t, self.alpha, self.K, rho, self.state.bias, stream, counts=self.counts,
+                        stats=self.stats)
 
     # ------------------------------------------------------------ auxiliary-loss statistics
 

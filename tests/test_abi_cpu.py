@@ -249,11 +249,16 @@ def test_qb_router_rejects_invalid_arguments(kw, code):
     (dict(rho=-0.25), B.IDB_ERR_INVALID_ARG),
     (dict(rho=float("nan")), B.IDB_ERR_INVALID_ARG),
     (dict(alpha=A16 + 1), B.IDB_ERR_INVALID_ARG),
+    (dict(counts=A16), B.IDB_ERR_INVALID_ARG),             # statistics output missing
+    (dict(stats=A16), B.IDB_ERR_INVALID_ARG),              # counts missing
+    (dict(counts=A16, stats=A16 + 4), B.IDB_ERR_INVALID_ARG),  # fp64 output not 8-byte aligned
+    (dict(counts=A16 + 2, stats=A16), B.IDB_ERR_INVALID_ARG),  # misaligned counts
 ])
 def test_qb_update_rejects_invalid_arguments(kw, code):
     a = dict(st=A16, alpha=A16, T=16384, E=768, K=10, rho=0.0, bias=A16)
     a.update(kw)
-    assert B.lib().idb_qb_update(a["st"], a["alpha"], a["T"], a["E"], a["K"], a["rho"], a["bias"], None) == code
+    assert B.lib().idb_qb_update(a["st"], a["alpha"], a["T"], a["E"], a["K"], a["rho"], a["bias"], a.get("counts"),
+                                 a.get("stats"), None) == code
 
 
 def test_qb_workspace_holds_k_plus_one_candidates():

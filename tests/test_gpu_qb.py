@@ -110,6 +110,34 @@ def test_qb_update_matches_oracle(T, E, K, kind, rho):
     np.testing.assert_array_equal(bits(bt), want.view(np.uint32))
 
 
+@pytest.mark.parametrize("T,E,K", [(1000, 768, 10), (16384, 768, 10), (32768, 64, 3), (40000, 32, 4),
+                                   (500, 1024, 8)])
+def test_qb_update_writes_load_statistics_in_the_same_launch(T, E, K):
+    # the first workgroup's MaxVio/MinVio (Eq. vio) equal the oracle's bit for
+    # bit, and the bias is the same as without them (every kernel form: 512
+    # and 1024 threads with keys in registers, keys recomputed from memory)
+    s = synth.scores(T, E, "beta", seed=T + 3)
+    b = synth.bias(E, "small", seed=E + 1)
+    alpha = oracle.qb_alpha(s, b, K)
+    st = torch.from_numpy(np.ascontiguousarray(s.T)).to(DEV)
+    at = torch.from_numpy(alpha).to(DEV)
+    rng = np.random.default_rng(E)
+    for c in (rng.integers(0, 3 * T * K // E + 2, E).astype(np.int32), np.zeros(E, np.int32),
+              np.full(E, 7, np.int32)):
+        plain = torch.from_numpy(b.copy()).to(DEV)
+        B.idb_qb_update(st, at, K, 0.5, plain)
+        bt = torch.from_numpy(b.copy()).to(DEV)
+        stats = torch.full((2,), -1.0, dtype=torch.float64, device=DEV)
+        B.idb_qb_update(st, at, K, 0.5, bt, counts=torch.from_numpy(c).to(DEV), stats=stats)
+        np.testing.assert_array_equal(bits(bt), bits(plain))
+        want = np.asarray(oracle.load_stats(c), np.float64)
+        got = stats.cpu().numpy()
+        if c.sum() == 0:
+            assert np.isnan(got).all() and np.isnan(want).all()  # empty batch
+        else:
+            np.testing.assert_array_equal(got.view(np.uint64), want.view(np.uint64))
+
+
 def test_qb_closed_loop():
     """Quantile Balancing steps on the skewed mixture inputs (see the module
     notes): GPU-internal consistency every step, and a free-running oracle
