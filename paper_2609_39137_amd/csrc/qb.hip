@@ -255,7 +255,6 @@ __device__ void qb_block_stats(const int (&n)[NQ], int E, double* __restrict__ o
         mx = max(mx, __shfl_xor(mx, o));
         mn = min(mn, __shfl_xor(mn, o));
     }
-    __syncthreads();
     if (lane == 0) {
         w_sum[wave] = S;
         w_max[wave] = mx;
