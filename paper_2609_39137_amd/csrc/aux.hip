@@ -85,24 +85,25 @@ __global__ __launch_bounds__(kAuxThreads) void aux_stats_kernel(const float* __r
             mn = min(mn, __shfl_xor(mn, o));
         }
         if (lane == 0) {
-            partial[blockIdx.x].fp = fp;
-            partial[blockIdx.x].sum = nsum;
-            partial[blockIdx.x].max = mx;
-            partial[blockIdx.x].min = mn;
+            // agent-scope stores: coherent across the XCDs' L2s without a
+            // cache write-back
+            __hip_atomic_store(&partial[blockIdx.x].fp, fp, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_store(&partial[blockIdx.x].sum, nsum, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_store(&partial[blockIdx.x].max, mx, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_store(&partial[blockIdx.x].min, mn, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
     }
-    // publish partial[] before taking a ticket: every wave's stores complete,
-    // one agent-scope release fence, a relaxed increment; the last workgroup
-    // orders its reads with an acquire fence
+    // The records are written and read only by agent-scope atomic accesses:
+    // a workgroup waits for its own stores to complete before it takes a
+    // ticket (a relaxed increment), and the workgroup that takes the last one
+    // reads the records after its ticket, so no cache write-back or
+    // invalidation is needed around the ticket.
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
-    if (threadIdx.x == 0) {
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+    if (threadIdx.x == 0)
         last = __hip_atomic_fetch_add(ticket, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == gridDim.x - 1;
-    }
     __syncthreads();
     if (!last) return;
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
     if (threadIdx.x == 0) {
         double L = 0.0;
         long long S = 0;
