@@ -10,6 +10,9 @@
   selection is decided identically: indices and counts exact, gate weights
   within the score error, and the new bias, e_prev and MaxVio/MinVio bit for
   bit equal to the oracle's controller on the same counts.
+* One Quantile Balancing iteration: the same selection check, then the
+  cutoffs, the new bias (EMA weight 0 or 0.5) and MaxVio/MinVio bit for bit
+  against the oracle on the GPU's own expert-major scores.
 """
 import numpy as np
 import pytest
@@ -76,4 +79,41 @@ def test_router_step_random_shapes(T, d, E, K, seed):
     oracle.controller(r_c, ref, Ki, Kd)
     np.testing.assert_array_equal(rs.state.bias.cpu().numpy(), ref.bias)
     np.testing.assert_array_equal(rs.state.e_prev.cpu().numpy(), ref.e_prev)
+    np.testing.assert_array_equal(rs.stats.cpu().numpy(), oracle.load_stats(r_c))
+
+
+def _qb_cases(n=24):
+    g = np.random.default_rng(20261204)
+    for i in range(n):
+        E = 32 * int(g.integers(1, 33))
+        K = int(g.integers(1, min(E - 1, 31) + 1))
+        d = 64 * int(g.integers(1, 9))
+        T = int(g.integers(1, 2049))
+        rho = float(g.choice([0.0, 0.5]))
+        yield T, d, E, K, rho, i
+
+
+@pytest.mark.parametrize("T,d,E,K,rho,seed", list(_qb_cases()))
+def test_qb_step_random_shapes(T, d, E, K, rho, seed):
+    # one Quantile Balancing iteration (Eq. pid-quantile, pid-quantile-def)
+    # from a zero bias on integer inputs: selection exact against the oracle;
+    # the cutoffs, the new bias and MaxVio/MinVio bit for bit against the
+    # oracle on the GPU's own expert-major scores
+    x, W = synth.integer_router_inputs(T, d, E, seed=4000 + seed, dtype="bf16", w_shift=6)
+    rs = RouterStep(T, d, E, K, torch.bfloat16, device=DEV)
+    xt = torch.from_numpy(x.view(np.int16)).to(DEV).view(torch.bfloat16)
+    Wt = torch.from_numpy(W.view(np.int16)).to(DEV).view(torch.bfloat16)
+    rs.qb_step(xt, Wt, rho=rho)
+    torch.cuda.synchronize()
+    b0 = np.zeros(E, np.float32)
+    r_idx, r_w, r_c = oracle.router(x, W, b0, K)
+    np.testing.assert_array_equal(rs.idx.cpu().numpy(), r_idx)
+    np.testing.assert_array_equal(rs.counts.cpu().numpy(), r_c)
+    np.testing.assert_allclose(rs.w.cpu().numpy(), r_w, rtol=2e-5)
+    s = np.ascontiguousarray(rs.scores_t.cpu().numpy().T)
+    np.testing.assert_allclose(s, oracle.router_scores(x, W), rtol=2e-6)
+    alpha = oracle.qb_alpha(s, b0, K)
+    np.testing.assert_array_equal(rs.alpha.cpu().numpy().view(np.uint32), alpha.view(np.uint32))
+    want = oracle.qb_update(s, alpha, K, rho, b0.copy())
+    np.testing.assert_array_equal(rs.state.bias.cpu().numpy().view(np.uint32), want.view(np.uint32))
     np.testing.assert_array_equal(rs.stats.cpu().numpy(), oracle.load_stats(r_c))
