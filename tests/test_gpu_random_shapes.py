@@ -13,6 +13,9 @@
 * One Quantile Balancing iteration: the same selection check, then the
   cutoffs, the new bias (EMA weight 0 or 0.5) and MaxVio/MinVio bit for bit
   against the oracle on the GPU's own expert-major scores.
+* The auxiliary-loss router's forward statistics (E up to 768): on integer
+  inputs selection, counts, f and MaxVio/MinVio exactly as the oracle's, P
+  and the loss within the bound derived in tests/test_gpu_aux.py.
 """
 import numpy as np
 import pytest
@@ -117,3 +120,25 @@ def test_qb_step_random_shapes(T, d, E, K, rho, seed):
     want = oracle.qb_update(s, alpha, K, rho, b0.copy())
     np.testing.assert_array_equal(rs.state.bias.cpu().numpy().view(np.uint32), want.view(np.uint32))
     np.testing.assert_array_equal(rs.stats.cpu().numpy(), oracle.load_stats(r_c))
+
+
+def _aux_cases(n=24):
+    g = np.random.default_rng(20261205)
+    for i in range(n):
+        E = 32 * int(g.integers(1, 25))  # one-slice tilings cover E <= 768
+        K = int(g.integers(1, min(E, 32) + 1))
+        d = 64 * int(g.integers(1, 9))
+        T = int(g.integers(1, 2049))
+        yield T, d, E, K, i
+
+
+@pytest.mark.parametrize("T,d,E,K,seed", list(_aux_cases()))
+def test_aux_router_random_shapes(T, d, E, K, seed):
+    # the auxiliary-loss forward statistics (Eq. pid-auxloss) on integer
+    # inputs: exact logits, so selection, counts, f and MaxVio/MinVio match
+    # the oracle exactly and P and the loss lie within the derived bound
+    from tests.test_gpu_aux import check_aux, run_aux
+
+    x, W = synth.integer_router_inputs(T, d, E, seed=5000 + seed, dtype="bf16", w_shift=6)
+    g = run_aux(x, W, K, 0.05)
+    check_aux(x, W, K, 0.05, g, exact=True)
