@@ -13,6 +13,10 @@
 * One Quantile Balancing iteration: the same selection check, then the
   cutoffs, the new bias (EMA weight 0 or 0.5) and MaxVio/MinVio bit for bit
   against the oracle on the GPU's own expert-major scores.
+* One routing with idb_router_forward on normally distributed inputs and a
+  bias: scores within the accumulation error of the oracle's, the selection
+  margin-aware against the oracle's, and bit-identical to the oracle's
+  selection on the kernel's own fp32 scores.
 * The auxiliary-loss router's forward statistics (E up to 768): on integer
   inputs selection, counts, f and MaxVio/MinVio exactly as the oracle's, P
   and the loss within the bound derived in tests/test_gpu_aux.py.
@@ -142,3 +146,34 @@ def test_aux_router_random_shapes(T, d, E, K, seed):
     x, W = synth.integer_router_inputs(T, d, E, seed=5000 + seed, dtype="bf16", w_shift=6)
     g = run_aux(x, W, K, 0.05)
     check_aux(x, W, K, 0.05, g, exact=True)
+
+
+def _forward_cases(n=32):
+    g = np.random.default_rng(20261206)
+    for i in range(n):
+        E = 32 * int(g.integers(1, 33))
+        K = int(g.integers(1, min(E, 32) + 1))
+        d = 64 * int(g.integers(1, 9))
+        T = int(g.integers(1, 2049))
+        bkind = str(g.choice(["zero", "small", "large", "grid"]))
+        yield T, d, E, K, bkind, i
+
+
+@pytest.mark.parametrize("T,d,E,K,bkind,seed", list(_forward_cases()))
+def test_router_forward_random_shapes(T, d, E, K, bkind, seed):
+    # normally distributed inputs and a biased selection (Eq. pid-routing):
+    # the fused kernel's scores within the fp32 accumulation error of the
+    # oracle's, its selection margin-aware against the oracle's, and, given
+    # its own fp32 scores, indices, gate weights and counts bit-identical to
+    # the oracle's selection
+    from tests.test_gpu_router import check_against_oracle, check_invariants, run_router
+
+    x, W = synth.normal_router_inputs(T, d, E, seed=6000 + seed, w_std=0.05)
+    b = synth.bias(E, bkind, seed=7000 + seed)
+    idx, w, c, s = run_router(x, W, b, K)
+    check_invariants(idx, w, c, T, E, K)
+    check_against_oracle(x, W, b, K, idx, w, c, s, max_uncertain=0.02)
+    r_idx, r_w, r_c = oracle.select(s, b, K)
+    np.testing.assert_array_equal(idx, r_idx)
+    np.testing.assert_array_equal(w.view(np.uint32), r_w.view(np.uint32))
+    np.testing.assert_array_equal(c, r_c)
