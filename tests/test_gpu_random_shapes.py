@@ -13,8 +13,8 @@
 * One Quantile Balancing iteration: the same selection check, then the
   cutoffs, the new bias (EMA weight 0 or 0.5) and MaxVio/MinVio bit for bit
   against the oracle on the GPU's own expert-major scores.
-* One routing with idb_router_forward on normally distributed inputs and a
-  bias: scores within the accumulation error of the oracle's, the selection
+* One routing with idb_router_forward on normally distributed inputs (bf16,
+  and fp32 with d a multiple of 32) and a bias: scores within the accumulation error of the oracle's, the selection
   margin-aware against the oracle's, and bit-identical to the oracle's
   selection on the kernel's own fp32 scores.
 * The auxiliary-loss router's forward statistics (E up to 768): on integer
@@ -148,19 +148,20 @@ def test_aux_router_random_shapes(T, d, E, K, seed):
     check_aux(x, W, K, 0.05, g, exact=True)
 
 
-def _forward_cases(n=32):
+def _forward_cases(n=32, n_f32=12):
     g = np.random.default_rng(20261206)
-    for i in range(n):
-        E = 32 * int(g.integers(1, 33))
+    for i in range(n + n_f32):
+        f32 = i >= n  # fp32 inputs (d a multiple of 32)
+        E = 32 * int(g.integers(1, 9 if f32 else 33))
         K = int(g.integers(1, min(E, 32) + 1))
-        d = 64 * int(g.integers(1, 9))
-        T = int(g.integers(1, 2049))
+        d = (32 if f32 else 64) * int(g.integers(1, 9))
+        T = int(g.integers(1, 1025 if f32 else 2049))
         bkind = str(g.choice(["zero", "small", "large", "grid"]))
-        yield T, d, E, K, bkind, i
+        yield T, d, E, K, bkind, "f32" if f32 else "bf16", i
 
 
-@pytest.mark.parametrize("T,d,E,K,bkind,seed", list(_forward_cases()))
-def test_router_forward_random_shapes(T, d, E, K, bkind, seed):
+@pytest.mark.parametrize("T,d,E,K,bkind,dtype,seed", list(_forward_cases()))
+def test_router_forward_random_shapes(T, d, E, K, bkind, dtype, seed):
     # normally distributed inputs and a biased selection (Eq. pid-routing):
     # the fused kernel's scores within the fp32 accumulation error of the
     # oracle's, its selection margin-aware against the oracle's, and, given
@@ -168,7 +169,7 @@ def test_router_forward_random_shapes(T, d, E, K, bkind, seed):
     # the oracle's selection
     from tests.test_gpu_router import check_against_oracle, check_invariants, run_router
 
-    x, W = synth.normal_router_inputs(T, d, E, seed=6000 + seed, w_std=0.05)
+    x, W = synth.normal_router_inputs(T, d, E, seed=6000 + seed, dtype=dtype, w_std=0.05)
     b = synth.bias(E, bkind, seed=7000 + seed)
     idx, w, c, s = run_router(x, W, b, K)
     check_invariants(idx, w, c, T, E, K)
