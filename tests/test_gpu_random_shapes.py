@@ -7,7 +7,8 @@
 * One router iteration (Alg. 1) with idb_router_step: E a multiple of 32 up
   to 1024, d a multiple of 64 up to 512, K up to 32, T up to 2048, integer
   inputs (exact logits on both sides) and a zero starting bias, so the
-  selection is decided identically: indices and counts exact, gate weights
+  selection is decided identically; error-scaled or DeepSeek's fixed-step
+  integral, with or without centring: indices and counts exact, gate weights
   within the score error, and the new bias, e_prev and MaxVio/MinVio bit for
   bit equal to the oracle's controller on the same counts.
 * One Quantile Balancing iteration: the same selection check, then the
@@ -52,7 +53,9 @@ def _router_cases(n=48):
         K = int(g.integers(1, min(E, 32) + 1))
         d = 64 * int(g.integers(1, 9))
         T = int(g.integers(1, 2049))
-        yield T, d, E, K, i
+        sign = bool(g.integers(0, 2))      # DeepSeek's fixed-step integral, else error-scaled
+        center = bool(g.integers(0, 2))
+        yield T, d, E, K, sign, center, i
 
 
 @pytest.mark.parametrize("T,E,K,kind,bkind,seed", list(_select_cases()))
@@ -69,11 +72,12 @@ def test_select_random_shapes(T, E, K, kind, bkind, seed):
     np.testing.assert_array_equal(c.cpu().numpy(), rc)
 
 
-@pytest.mark.parametrize("T,d,E,K,seed", list(_router_cases()))
-def test_router_step_random_shapes(T, d, E, K, seed):
+@pytest.mark.parametrize("T,d,E,K,sign,center,seed", list(_router_cases()))
+def test_router_step_random_shapes(T, d, E, K, sign, center, seed):
     Ki, Kd = 2.0 ** -7, 2.0 ** -6
+    mode = B.IDB_INTEGRAL_SIGN if sign else B.IDB_INTEGRAL_ERROR
     x, W = synth.integer_router_inputs(T, d, E, seed=3000 + seed, dtype="bf16", w_shift=6)
-    rs = RouterStep(T, d, E, K, torch.bfloat16, B.ControllerCfg(E, Ki, Kd), device=DEV)
+    rs = RouterStep(T, d, E, K, torch.bfloat16, B.ControllerCfg(E, Ki, Kd, mode, center), device=DEV)
     xt = torch.from_numpy(x.view(np.int16)).to(DEV).view(torch.bfloat16)
     Wt = torch.from_numpy(W.view(np.int16)).to(DEV).view(torch.bfloat16)
     rs.step(xt, Wt)
@@ -83,7 +87,7 @@ def test_router_step_random_shapes(T, d, E, K, seed):
     np.testing.assert_array_equal(rs.idx.cpu().numpy(), r_idx)
     np.testing.assert_array_equal(rs.counts.cpu().numpy(), r_c)
     np.testing.assert_allclose(rs.w.cpu().numpy(), r_w, rtol=2e-5)
-    oracle.controller(r_c, ref, Ki, Kd)
+    oracle.controller(r_c, ref, Ki, Kd, oracle.MODE_SIGN if sign else oracle.MODE_ERROR, center)
     np.testing.assert_array_equal(rs.state.bias.cpu().numpy(), ref.bias)
     np.testing.assert_array_equal(rs.state.e_prev.cpu().numpy(), ref.e_prev)
     np.testing.assert_array_equal(rs.stats.cpu().numpy(), oracle.load_stats(r_c))
